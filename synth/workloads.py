@@ -1,0 +1,246 @@
+"""Seeded synthetic workloads shaped like the paper's model pairs.
+
+This module is shared input generation only: it holds none of the codec's arithmetic (no
+RoPE, no encode, no decode, no projection).  It draws random tensors, builds orthonormal bases
+by QR, RMS-normalises hidden states (the producer and consumer models' own normalisation, which
+precedes the codec) and synthesises power-law K/V signals.  Both the oracle and the GPU path
+consume the tensors it returns, rounded once to the path's dtype.
+
+Every tensor is drawn from its own generator, seeded from (workload name, layer, tensor name),
+so any tensor can be regenerated alone.  Variance notation: ``N(0, s)`` has variance ``s``.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+import zlib
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    n_layers: int
+    d_model: int
+    n_kv_heads: int
+    head_dim: int
+    seq_lens: Tuple[int, ...]
+    ranks: Tuple[int, ...]            # per layer; r_K = r_V = r_H = ranks[l]
+    patch_layers: Tuple[int, ...]
+    rope_theta: float
+    dtype: str                        # "f32" or "bf16"
+    basis_width: Optional[int] = None  # None -> D = n_kv_heads * head_dim
+    power_law: bool = False           # K/V signal spectrum sigma_i ~ 1/i
+    pos0: Optional[Tuple[int, ...]] = None
+    with_bias: bool = False           # projection bias on the Patch branch (Qwen2-style)
+    with_mu: bool = True
+
+    @property
+    def kv_width(self) -> int:
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def w(self) -> int:
+        return self.basis_width or self.kv_width
+
+    @property
+    def g(self) -> int:
+        return self.kv_width // self.w
+
+    @property
+    def n_tokens(self) -> int:
+        return int(sum(self.seq_lens))
+
+    @property
+    def n_seqs(self) -> int:
+        return len(self.seq_lens)
+
+    @property
+    def is_patch(self) -> Tuple[int, ...]:
+        return tuple(1 if l in self.patch_layers else 0 for l in range(self.n_layers))
+
+    @property
+    def cu_seqlens(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.seq_lens)]).astype(np.int32)
+
+    @property
+    def max_position(self) -> int:
+        """One past the largest RoPE position any token of the batch takes."""
+        p0 = self.pos0 or (0,) * self.n_seqs
+        return int(max(a + n for a, n in zip(p0, self.seq_lens)))
+
+    @property
+    def torch_dtype(self):
+        return torch.float32 if self.dtype == "f32" else torch.bfloat16
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+def _ragged_lengths(seed: int, n: int, lo: int, hi: int) -> Tuple[int, ...]:
+    """``n`` integers uniform on ``[lo, hi]`` inclusive."""
+    return tuple(int(x) for x in np.random.default_rng(seed).integers(lo, hi + 1, n))
+
+
+# The five model-shaped workloads.
+TINY_F32 = Workload("tiny_f32", 4, 512, 4, 64, (512,), (32,) * 4, (2,), 1e4, "f32")
+LLAMA3_8B = Workload("llama3_8b_bf16", 32, 4096, 8, 128, (8192,), (128,) * 32,
+                     (0, 8, 16, 24), 5e5, "bf16", power_law=True)
+QWEN2_7B = Workload("qwen2_7b_bf16", 28, 3584, 4, 128, (32768,), (96,) * 28,
+                    (0, 7, 14, 21), 1e6, "bf16", power_law=True)
+BATCHED = Workload("batched_ragged_bf16", 32, 4096, 8, 128, _ragged_lengths(3, 16, 1024, 16384),
+                   tuple((64, 128, 256)[l % 3] for l in range(32)), (0, 8, 16, 24), 5e5, "bf16",
+                   power_law=True)
+LLAMA3_70B = Workload("llama3_70b_bf16", 80, 8192, 8, 128, (16384,), (128,) * 80,
+                      tuple(range(0, 80, 10)), 5e5, "bf16", power_law=True)
+
+CONFIGS = (TINY_F32, LLAMA3_8B, QWEN2_7B, BATCHED, LLAMA3_70B)
+
+# Small workloads the oracle finishes in seconds that still span several tiles, ragged tails,
+# per-layer ranks, the head-shared basis, biases and non-zero first positions.
+SMALL_BF16 = Workload("small_bf16", 5, 384, 2, 128, (300, 77, 650), (64, 128, 32, 256, 96),
+                      (1, 4), 5e5, "bf16", power_law=True)
+SMALL_HEAD_SHARED = Workload("small_head_shared_bf16", 3, 256, 4, 64, (129, 250), (32, 64, 48),
+                             (2,), 1e4, "bf16", basis_width=64, with_bias=True,
+                             pos0=(5, 1000))
+SMALL_F32 = Workload("small_f32", 3, 320, 2, 64, (97, 200, 31), (16, 48, 32), (0,), 1e4, "f32",
+                     with_bias=True)
+TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32)
+
+
+# --------------------------------------------------------------------------------------------
+# Seeded draws
+# --------------------------------------------------------------------------------------------
+def _seed(wl: Workload, layer: int, tensor: str) -> int:
+    return zlib.crc32(f"{wl.name}/{layer}/{tensor}".encode()) & 0x7FFFFFFF
+
+
+def _randn(wl, layer, tensor, shape, device) -> torch.Tensor:
+    g = torch.Generator(device=device)
+    g.manual_seed(_seed(wl, layer, tensor))
+    return torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+
+
+def _rms_normalize(x: torch.Tensor) -> torch.Tensor:
+    return x * torch.rsqrt(x.square().mean(dim=-1, keepdim=True) + 1e-6)
+
+
+def power_law_sigma(w: int) -> np.ndarray:
+    """``sigma_i = c / i`` (``i = 1..w``) with ``c`` chosen so the signal's per-element RMS is 1."""
+    i = np.arange(1, w + 1, dtype=np.float64)
+    c = np.sqrt(w / np.sum(1.0 / i ** 2))
+    return c / i
+
+
+@functools.lru_cache(maxsize=512)
+def _full_basis(wl: Workload, layer: int, branch: str) -> np.ndarray:
+    """Orthonormal ``[w, w]`` matrix (fp64, CPU); its first ``r`` columns are the layer's basis."""
+    g = np.random.default_rng(_seed(wl, layer, "basis_" + branch))
+    q, r = np.linalg.qr(g.standard_normal((wl.w, wl.w)))
+    return q * np.sign(np.diag(r))[None, :]
+
+
+def _cast(x: torch.Tensor, wl: Workload, device) -> torch.Tensor:
+    return x.to(device=device, dtype=wl.torch_dtype).contiguous()
+
+
+def basis(wl: Workload, layer: int, branch: str, device="cpu"):
+    """Reuse artifacts of one layer and branch: ``(W_enc [r, w], W_dec [w, r])`` with W_dec = Q."""
+    r = wl.ranks[layer]
+    q = torch.from_numpy(_full_basis(wl, layer, branch)[:, :r].copy())
+    return _cast(q.T.contiguous(), wl, device), _cast(q, wl, device)
+
+
+def mu(wl: Workload, layer: int, branch: str, device="cpu"):
+    """Offset ``mu ~ N(0, 0.1)`` of width ``w`` (the same for encoder and decoder), or None."""
+    if not wl.with_mu:
+        return None
+    return _cast(_randn(wl, layer, "mu_" + branch, (wl.w,), "cpu") * np.sqrt(0.1), wl, device)
+
+
+def codes(wl: Workload, layer: int, branch: str, device="cpu") -> torch.Tensor:
+    """Reuse codes ``[T*g, r]``: N(0,1), scaled per column by sigma_1..r when the spectrum is a
+    power law (the projection of the synthetic signal onto its top-r directions)."""
+    r = wl.ranks[layer]
+    z = _randn(wl, layer, "codes_" + branch, (wl.n_tokens * wl.g, r), device)
+    if wl.power_law:
+        sig = torch.tensor(power_law_sigma(wl.w)[:r], dtype=torch.float32, device=device)
+        z = z * sig[None, :]
+    return _cast(z, wl, device)
+
+
+def kv_input(wl: Workload, layer: int, branch: str, device="cpu") -> torch.Tensor:
+    """Producer K or V ``[T, D]``: ``mu + signal + N(0, 0.01)``.
+
+    The signal is rank ``r`` in the layer's basis (``C Q^T``, C ~ N(0,1)) for flat spectra, or
+    ``G diag(sigma) B^T`` over the full orthonormal ``B`` (first r columns = Q) for power-law
+    spectra.  It is drawn directly in the cache's own layout.
+    """
+    n = wl.n_tokens * wl.g
+    b = torch.from_numpy(_full_basis(wl, layer, branch)).to(device=device, dtype=torch.float32)
+    if wl.power_law:
+        sig = torch.tensor(power_law_sigma(wl.w), dtype=torch.float32, device=device)
+        gmat = _randn(wl, layer, "signal_" + branch, (n, wl.w), device) * sig[None, :]
+        x = gmat @ b.T
+    else:
+        r = wl.ranks[layer]
+        c = _randn(wl, layer, "signal_" + branch, (n, r), device)
+        x = c @ b[:, :r].T
+    x = x + _randn(wl, layer, "noise_" + branch, (n, wl.w), device) * 0.1
+    m = mu(wl, layer, branch, device)
+    if m is not None:
+        x = x + m.to(torch.float32)[None, :]
+    return _cast(x.reshape(wl.n_tokens, wl.kv_width), wl, device)
+
+
+def hidden(wl: Workload, layer: int, which: str, device="cpu") -> torch.Tensor:
+    """RMS-normalised N(0,1) hidden state ``[T, d_model]`` (``which`` = 'h_in' or 'h_hat')."""
+    x = _randn(wl, layer, which, (wl.n_tokens, wl.d_model), device)
+    return _cast(_rms_normalize(x), wl, device)
+
+
+def enc_h(wl: Workload, layer: int, device="cpu") -> torch.Tensor:
+    """Patch-layer code projection ``W_enc,H`` stored ``[r_H, d_model]`` (orthonormal rows)."""
+    r = wl.ranks[layer]
+    g = np.random.default_rng(_seed(wl, layer, "enc_h"))
+    q, rr = np.linalg.qr(g.standard_normal((wl.d_model, r)))
+    q = q * np.sign(np.diag(rr))[None, :]
+    return _cast(torch.from_numpy(q.T.copy()), wl, device)
+
+
+def proj_weights(wl: Workload, layer: int, device="cpu"):
+    """Consumer ``W_K, W_V ~ N(0, 1/d_model)`` stored ``[D, d_model]`` (k_proj/v_proj.weight)."""
+    s = 1.0 / np.sqrt(wl.d_model)
+    wk = _randn(wl, layer, "w_k", (wl.kv_width, wl.d_model), device) * s
+    wv = _randn(wl, layer, "w_v", (wl.kv_width, wl.d_model), device) * s
+    return _cast(wk, wl, device), _cast(wv, wl, device)
+
+
+def proj_bias(wl: Workload, layer: int, device="cpu"):
+    """Optional ``b_K, b_V ~ N(0, 0.1)`` of width D, or (None, None)."""
+    if not wl.with_bias:
+        return None, None
+    bk = _randn(wl, layer, "b_k", (wl.kv_width,), "cpu") * np.sqrt(0.1)
+    bv = _randn(wl, layer, "b_v", (wl.kv_width,), "cpu") * np.sqrt(0.1)
+    return _cast(bk, wl, device), _cast(bv, wl, device)
+
+
+def cu_seqlens(wl: Workload, device="cpu") -> torch.Tensor:
+    return torch.from_numpy(wl.cu_seqlens).to(device)
+
+
+def pos0(wl: Workload, device="cpu") -> Optional[torch.Tensor]:
+    if wl.pos0 is None:
+        return None
+    return torch.tensor(wl.pos0, dtype=torch.int32, device=device)
+
+
+def layer_set(wl: Workload, layers: Optional[Sequence[int]] = None):
+    return list(range(wl.n_layers)) if layers is None else list(layers)

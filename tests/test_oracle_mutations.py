@@ -1,0 +1,151 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check the pins catch every one.
+
+Each mutation replaces one oracle function with a subtly wrong variant; at least one pin of
+test_oracle_pins must then fail.  This is what makes the pins evidence for the oracle.
+"""
+import numpy as np
+import pytest
+
+from oracle import scd_oracle as O
+import tests.test_oracle_pins as P
+
+F64 = np.float64
+_rope = O.rope
+_positions = O.positions
+_encode_k = O.encode_k
+_encode_v = O.encode_v
+_decode_k = O.decode_k
+_decode_v = O.decode_v
+_patch_k = O.patch_k
+
+
+def rope_wrong_sign(x, pos, n, dh, theta, inverse=False):
+    return _rope(x, pos, n, dh, theta, inverse=not inverse)
+
+
+def rope_wrong_freq(x, pos, n, dh, theta, inverse=False):
+    return _rope(x, pos, n, dh, theta ** 0.5, inverse=inverse)
+
+
+def rope_interleaved(x, pos, n, dh, theta, inverse=False):
+    # pairs (2i, 2i+1) instead of (i, i + d/2)
+    t = x.shape[0]
+    xh = np.asarray(x, F64).reshape(t, n, dh)
+    perm = np.concatenate([np.arange(0, dh, 2), np.arange(1, dh, 2)])
+    y = _rope(xh[..., perm].reshape(t, n * dh), pos, n, dh, theta, inverse).reshape(t, n, dh)
+    out = np.empty_like(y)
+    out[..., perm] = y
+    return out.reshape(t, n * dh)
+
+
+def rope_head_mixed(x, pos, n, dh, theta, inverse=False):
+    # pairs across the whole row instead of within each head
+    return _rope(x, pos, 1, n * dh, theta, inverse).reshape(x.shape)
+
+
+def positions_off_by_one(cu, pos0=None):
+    return _positions(cu, pos0) + 1
+
+
+def positions_global(cu, pos0=None):
+    # forgets to restart every request at its own first position
+    return np.arange(int(np.asarray(cu)[-1]), dtype=np.int64)
+
+
+def encode_k_no_derope(k_a, pos, w_enc, mu_enc, n, dh, theta):
+    x = O.to_rows(k_a, np.asarray(w_enc).shape[1])
+    if mu_enc is not None:
+        x = x - np.asarray(mu_enc, F64)[None, :]
+    return x @ np.asarray(w_enc, F64).T
+
+
+def encode_v_mu_sign(v_a, w_enc, mu_enc):
+    return _encode_v(v_a, w_enc, None if mu_enc is None else -np.asarray(mu_enc, F64))
+
+
+def encode_v_mu_dropped(v_a, w_enc, mu_enc):
+    return _encode_v(v_a, w_enc, None)
+
+
+def decode_v_transposed(z, w_dec, mu_dec, d):
+    y = np.asarray(z, F64) @ np.asarray(w_dec, F64)
+    if mu_dec is not None:
+        y = y + np.asarray(mu_dec, F64)[None, :]
+    return O.from_rows(y, d)
+
+
+def decode_k_rope_before_mu(z, w_dec, mu_dec, pos, n, dh, theta):
+    y = O.from_rows(np.asarray(z, F64) @ np.asarray(w_dec, F64).T, n * dh)
+    y = _rope(y, pos, n, dh, theta)
+    if mu_dec is not None:
+        y = y + np.tile(np.asarray(mu_dec, F64), (n * dh) // len(mu_dec))[None, :]
+    return y
+
+
+def decode_k_no_rope(z, w_dec, mu_dec, pos, n, dh, theta):
+    return _decode_v(z, w_dec, mu_dec, n * dh)
+
+
+def patch_k_no_bias(h, w, b, pos, n, dh, theta):
+    return _patch_k(h, w, None, pos, n, dh, theta)
+
+
+def patch_k_bias_after_rope(h, w, b, pos, n, dh, theta):
+    y = _patch_k(h, w, None, pos, n, dh, theta)
+    return y if b is None else y + np.asarray(b, F64)[None, :]
+
+
+def _schedule_swapped(is_patch):
+    flags = [bool(v) for v in is_patch]
+    return [l for l, f in enumerate(flags) if f], [l for l, f in enumerate(flags) if not f]
+
+
+MUTATIONS = [
+    ("rope", rope_wrong_sign),
+    ("rope", rope_wrong_freq),
+    ("rope", rope_interleaved),
+    ("rope", rope_head_mixed),
+    ("positions", positions_off_by_one),
+    ("positions", positions_global),
+    ("encode_k", encode_k_no_derope),
+    ("encode_v", encode_v_mu_sign),
+    ("encode_v", encode_v_mu_dropped),
+    ("decode_v", decode_v_transposed),
+    ("decode_k", decode_k_rope_before_mu),
+    ("decode_k", decode_k_no_rope),
+    ("patch_k", patch_k_no_bias),
+    ("patch_k", patch_k_bias_after_rope),
+    ("schedule", _schedule_swapped),
+]
+
+PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]
+
+
+def _run_pin(fn):
+    import inspect
+    params = inspect.signature(fn).parameters
+    if "w_is_head" in params:
+        for v in (False, True):
+            fn(v)
+    elif "branch" in params:
+        for v in ("k", "v"):
+            fn(v)
+    else:
+        fn()
+
+
+@pytest.mark.parametrize("name,fn", MUTATIONS, ids=[f.__name__ for _, f in MUTATIONS])
+def test_pins_catch_planted_mistake(monkeypatch, name, fn):
+    monkeypatch.setattr(O, name, fn)
+    caught = []
+    for pin in PINS:
+        try:
+            _run_pin(pin)
+        except (AssertionError, ValueError, IndexError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin caught the planted mistake {fn.__name__}"
+
+
+def test_unmutated_oracle_passes_every_pin():
+    for pin in PINS:
+        _run_pin(pin)

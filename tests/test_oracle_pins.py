@@ -1,0 +1,413 @@
+"""Pins of the fp64 oracle against what the mathematics and the paper fix.
+
+None of these re-type the oracle's formulas: RoPE is checked against complex multiplication,
+a matrix exponential, closed-form points and its group properties; the linear maps against
+explicit loops, exact round trips, in-subspace recovery and the Eckart-Young tail energy.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+from oracle import scd_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------------------------------------
+# Independent RoPE formulations (test-side)
+# ------------------------------------------------------------------------------------------
+def rope_complex(x, pos, n_heads, head_dim, theta, sign=1.0):
+    """RoPE as multiplication of (x_i + 1j x_{i+d/2}) by exp(1j * sign * p * theta^(-2i/d))."""
+    t = x.shape[0]
+    half = head_dim // 2
+    xh = np.asarray(x, np.float64).reshape(t, n_heads, head_dim)
+    z = xh[..., :half] + 1j * xh[..., half:]
+    freq = np.array([theta ** (-2.0 * i / head_dim) for i in range(half)])
+    ph = np.exp(1j * sign * np.outer(np.asarray(pos, np.float64), freq))[:, None, :]
+    zr = z * ph
+    return np.concatenate([zr.real, zr.imag], axis=-1).reshape(t, n_heads * head_dim)
+
+
+def rope_expm_head(vec, p, head_dim, theta):
+    """RoPE of one head vector as expm(p * G) @ vec with G the skew generator of the rotation."""
+    half = head_dim // 2
+    g = np.zeros((head_dim, head_dim))
+    for i in range(half):
+        om = theta ** (-2.0 * i / head_dim)
+        g[i + half, i] = om
+        g[i, i + half] = -om
+    return scipy.linalg.expm(p * g) @ vec
+
+
+def rand_orthonormal(rng, n, k):
+    q, r = np.linalg.qr(rng.standard_normal((n, k)))
+    return q * np.sign(np.diag(r))[None, :]
+
+
+# ------------------------------------------------------------------------------------------
+# a0 routing and payload
+# ------------------------------------------------------------------------------------------
+def test_schedule_partitions_layers():
+    rng = np.random.default_rng(0)
+    for _ in range(20):
+        L = int(rng.integers(1, 90))
+        flags = rng.integers(0, 2, L)
+        reuse, patch = O.schedule(flags)
+        assert sorted(reuse + patch) == list(range(L))
+        assert not set(reuse) & set(patch)
+        assert all(flags[l] for l in patch) and not any(flags[l] for l in reuse)
+        assert reuse == sorted(reuse) and patch == sorted(patch)
+
+
+def test_schedule_reuse_only_and_patch_every_8th():
+    # "Reuse-only" is the empty Patch set (Section 6.1 baselines).
+    reuse, patch = O.schedule([0] * 32)
+    assert reuse == list(range(32)) and patch == []
+    reuse, patch = O.schedule([1 if l % 8 == 0 else 0 for l in range(32)])
+    assert patch == [0, 8, 16, 24] and len(reuse) == 28
+
+
+def test_payload_closed_form_and_offsets():
+    L, T, H, dh = 6, 37, 4, 16
+    D = H * dh
+    flags = [1, 0, 0, 1, 0, 0]
+    rk = [8, 16, 24, 32, 8, 16]
+    rv = [16, 16, 8, 8, 8, 32]
+    rh = [40, 8, 8, 24, 8, 8]
+    for w in (D, dh):
+        g = D // w
+        total, offs = O.payload_bytes(flags, T, H, dh, w, rk, rv, rh, 2)
+        expect = 0
+        for l in range(L):
+            n = T * rh[l] if flags[l] else T * g * (rk[l] + rv[l])
+            assert offs[l + 1] - offs[l] == 2 * n
+            expect += 2 * n
+        assert total == expect == offs[-1] and offs[0] == 0
+
+
+def test_payload_full_rank_identity_equals_raw_kv():
+    # With r = w (no compression) and no Patch layers the code set is exactly the raw cache.
+    L, T, H, dh = 5, 11, 2, 8
+    D = H * dh
+    for w in (D, dh):
+        total, _ = O.payload_bytes([0] * L, T, H, dh, w, [w] * L, [w] * L, [1] * L, 2)
+        assert total == 2 * L * T * D * 2
+
+
+def test_payload_is_linear_in_tokens_and_rank():
+    # O(T r) transmission (Section 4.5).
+    base, _ = O.payload_bytes([0, 1], 100, 8, 128, 1024, [64, 64], [64, 64], [64, 64], 2)
+    twice_t, _ = O.payload_bytes([0, 1], 200, 8, 128, 1024, [64, 64], [64, 64], [64, 64], 2)
+    twice_r, _ = O.payload_bytes([0, 1], 100, 8, 128, 1024, [128] * 2, [128] * 2, [128] * 2, 2)
+    assert twice_t == 2 * base and twice_r == 2 * base
+
+
+def test_paper_table2_payload_accounting():
+    # Table 2 prints raw BF16 and group-INT4 payloads for the same requests; 4-bit storage is a
+    # quarter of 16-bit storage, and SCD sits between Reuse-only and raw.
+    with open(os.path.join(GOLDEN, "table2_payload.json")) as f:
+        t2 = json.load(f)
+    assert round(t2["raw_bf16_mb"] / t2["int4_mb"], 2) == 4.00
+    assert t2["reuse_only_mb"] < t2["scd_mb"] < t2["raw_bf16_mb"]
+
+
+# ------------------------------------------------------------------------------------------
+# a1 positions
+# ------------------------------------------------------------------------------------------
+def test_positions_match_brute_force():
+    rng = np.random.default_rng(1)
+    for _ in range(10):
+        lens = rng.integers(0, 40, int(rng.integers(1, 8)))
+        cu = np.concatenate([[0], np.cumsum(lens)])
+        p0 = rng.integers(0, 1000, len(lens))
+        for use_p0 in (False, True):
+            got = O.positions(cu, p0 if use_p0 else None)
+            want = []
+            for b, n in enumerate(lens):
+                for k in range(n):
+                    want.append(k + (int(p0[b]) if use_p0 else 0))
+            assert got.tolist() == want
+
+
+# ------------------------------------------------------------------------------------------
+# RoPE
+# ------------------------------------------------------------------------------------------
+def test_rope_closed_form_points():
+    # theta = 1e4, d_h = 4: frequencies 1 and 0.01 rad per position.
+    e = np.eye(4)
+    out = O.rope(e[[0]], [1], 1, 4, 1e4)[0]
+    np.testing.assert_allclose(out, [math.cos(1), 0, math.sin(1), 0], atol=1e-15)
+    out = O.rope(e[[1]], [3], 1, 4, 1e4)[0]
+    np.testing.assert_allclose(out, [0, math.cos(0.03), 0, math.sin(0.03)], atol=1e-15)
+    out = O.rope(e[[2]], [2], 1, 4, 1e4)[0]
+    np.testing.assert_allclose(out, [-math.sin(2), 0, math.cos(2), 0], atol=1e-15)
+    # d_h = 2 is a plain 2-D rotation by p radians.
+    out = O.rope(np.array([[0.3, -0.7]]), [5], 1, 2, 123.0)[0]
+    c, s = math.cos(5), math.sin(5)
+    np.testing.assert_allclose(out, [0.3 * c + 0.7 * s, -0.7 * c + 0.3 * s], atol=1e-15)
+
+
+def test_rope_matches_complex_and_expm():
+    rng = np.random.default_rng(2)
+    H, dh, theta = 3, 16, 5e5
+    x = rng.standard_normal((7, H * dh))
+    pos = rng.integers(0, 40000, 7)
+    np.testing.assert_allclose(O.rope(x, pos, H, dh, theta), rope_complex(x, pos, H, dh, theta),
+                               atol=1e-12)
+    np.testing.assert_allclose(O.rope(x, pos, H, dh, theta, inverse=True),
+                               rope_complex(x, pos, H, dh, theta, sign=-1.0), atol=1e-12)
+    y = O.rope(x, pos, H, dh, theta)
+    for t in range(2):
+        for h in range(H):
+            np.testing.assert_allclose(y[t, h * dh:(h + 1) * dh],
+                                       rope_expm_head(x[t, h * dh:(h + 1) * dh], pos[t], dh,
+                                                      theta), atol=1e-9)
+
+
+def test_rope_group_properties():
+    rng = np.random.default_rng(3)
+    H, dh, theta = 2, 32, 1e4
+    x = rng.standard_normal((9, H * dh))
+    pos = rng.integers(0, 5000, 9)
+    y = O.rope(x, pos, H, dh, theta)
+    # norm of every (u, v) pair is preserved
+    half = dh // 2
+    xp = x.reshape(9, H, dh)
+    yp = y.reshape(9, H, dh)
+    np.testing.assert_allclose(xp[..., :half] ** 2 + xp[..., half:] ** 2,
+                               yp[..., :half] ** 2 + yp[..., half:] ** 2, rtol=1e-12)
+    # deRoPE o RoPE = id, RoPE at position 0 = id
+    np.testing.assert_allclose(O.rope(y, pos, H, dh, theta, inverse=True), x, atol=1e-12)
+    np.testing.assert_allclose(O.rope(x, np.zeros(9, int), H, dh, theta), x, atol=0)
+    # relative position: <RoPE_m q, RoPE_n k> = <RoPE_{m-n} q, k>
+    q = rng.standard_normal((1, dh))
+    k = rng.standard_normal((1, dh))
+    for m, n in [(7, 3), (1000, 999), (4, 4), (30000, 12)]:
+        lhs = float((O.rope(q, [m], 1, dh, theta) @ O.rope(k, [n], 1, dh, theta).T)[0, 0])
+        rhs = float((O.rope(q, [m - n], 1, dh, theta) @ k.T)[0, 0])
+        assert abs(lhs - rhs) < 1e-9 * (1 + abs(rhs))
+
+
+def test_rope_composes_additively():
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((5, 64))
+    a = rng.integers(0, 3000, 5)
+    b = rng.integers(0, 3000, 5)
+    two = O.rope(O.rope(x, a, 2, 32, 1e6), b, 2, 32, 1e6)
+    np.testing.assert_allclose(two, O.rope(x, a + b, 2, 32, 1e6), atol=1e-11)
+
+
+# ------------------------------------------------------------------------------------------
+# Linear maps: brute force on tiny inputs
+# ------------------------------------------------------------------------------------------
+def _loop_matmul_t(x, w):
+    """x[n, k] @ w[m, k]^T with explicit loops."""
+    n, k = x.shape
+    m = w.shape[0]
+    out = np.zeros((n, m))
+    for i in range(n):
+        for j in range(m):
+            s = 0.0
+            for q in range(k):
+                s += float(x[i, q]) * float(w[j, q])
+            out[i, j] = s
+    return out
+
+
+@pytest.mark.parametrize("w_is_head", [False, True])
+def test_encode_decode_brute_force(w_is_head):
+    rng = np.random.default_rng(5)
+    H, dh, theta = 2, 4, 1e4
+    D = H * dh
+    w = dh if w_is_head else D
+    g = D // w
+    T, r = 5, 3
+    pos = np.array([0, 1, 2, 0, 7])
+    k = rng.standard_normal((T, D))
+    v = rng.standard_normal((T, D))
+    e = rng.standard_normal((r, w))
+    f = rng.standard_normal((w, r))
+    mu_e = rng.standard_normal(w)
+    mu_d = rng.standard_normal(w)
+    # encode K: deRoPE by the complex formulation, then row loop
+    kc = rope_complex(k, pos, H, dh, theta, sign=-1.0)
+    rows = []
+    for t in range(T):
+        for j in range(g):
+            rows.append(kc[t, j * w:(j + 1) * w] - mu_e)
+    want_zk = _loop_matmul_t(np.array(rows), e)
+    np.testing.assert_allclose(O.encode_k(k, pos, e, mu_e, H, dh, theta), want_zk, atol=1e-12)
+    rows = [v[t, j * w:(j + 1) * w] - mu_e for t in range(T) for j in range(g)]
+    np.testing.assert_allclose(O.encode_v(v, e, mu_e), _loop_matmul_t(np.array(rows), e),
+                               atol=1e-12)
+    # decode: row loop, un-reshape, then RoPE via complex formulation
+    z = rng.standard_normal((T * g, r))
+    y = _loop_matmul_t(z, f) + mu_d[None, :]
+    tok = np.zeros((T, D))
+    for t in range(T):
+        for j in range(g):
+            tok[t, j * w:(j + 1) * w] = y[t * g + j]
+    np.testing.assert_allclose(O.decode_v(z, f, mu_d, D), tok, atol=1e-12)
+    np.testing.assert_allclose(O.decode_k(z, f, mu_d, pos, H, dh, theta),
+                               rope_complex(tok, pos, H, dh, theta), atol=1e-12)
+
+
+def test_patch_brute_force_and_encode_h():
+    rng = np.random.default_rng(6)
+    H, dh, d, T, theta = 2, 4, 5, 4, 1e4
+    D = H * dh
+    pos = np.array([3, 0, 1, 2])
+    hh = rng.standard_normal((T, d))
+    wk = rng.standard_normal((D, d))
+    wv = rng.standard_normal((D, d))
+    bk = rng.standard_normal(D)
+    bv = rng.standard_normal(D)
+    np.testing.assert_allclose(O.patch_v(hh, wv, bv), _loop_matmul_t(hh, wv) + bv, atol=1e-12)
+    np.testing.assert_allclose(O.patch_k(hh, wk, bk, pos, H, dh, theta),
+                               rope_complex(_loop_matmul_t(hh, wk) + bk, pos, H, dh, theta),
+                               atol=1e-12)
+    eh = rng.standard_normal((3, d))
+    np.testing.assert_allclose(O.encode_h(hh, eh), _loop_matmul_t(hh, eh), atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------------
+# Linear maps: exact structural results
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("w_is_head", [False, True])
+def test_full_rank_orthonormal_round_trip(w_is_head):
+    rng = np.random.default_rng(7)
+    H, dh, theta = 4, 16, 5e5
+    D = H * dh
+    w = dh if w_is_head else D
+    cu = [0, 13, 14, 40]
+    pos = O.positions(cu, [0, 5, 100])
+    T = cu[-1]
+    q = rand_orthonormal(rng, w, w)
+    mu = rng.standard_normal(w)
+    k = rng.standard_normal((T, D))
+    v = rng.standard_normal((T, D))
+    zk = O.encode_k(k, pos, q.T, mu, H, dh, theta)
+    zv = O.encode_v(v, q.T, mu)
+    np.testing.assert_allclose(O.decode_k(zk, q, mu, pos, H, dh, theta), k, atol=1e-12)
+    np.testing.assert_allclose(O.decode_v(zv, q, mu, D), v, atol=1e-12)
+
+
+def test_in_subspace_recovery():
+    rng = np.random.default_rng(8)
+    H, dh, theta, r = 2, 32, 1e4, 12
+    D = H * dh
+    T = 50
+    pos = np.arange(T) * 37
+    q = rand_orthonormal(rng, D, r)
+    mu = rng.standard_normal(D)
+    c = rng.standard_normal((T, r))
+    content = mu[None, :] + c @ q.T
+    k_a = rope_complex(content, pos, H, dh, theta)
+    np.testing.assert_allclose(O.encode_k(k_a, pos, q.T, mu, H, dh, theta), c, atol=1e-12)
+    np.testing.assert_allclose(O.decode_k(c, q, mu, pos, H, dh, theta), k_a, atol=1e-12)
+    np.testing.assert_allclose(O.encode_v(content, q.T, mu), c, atol=1e-12)
+    np.testing.assert_allclose(O.decode_v(c, q, mu, D), content, atol=1e-12)
+
+
+def test_invertible_nonorthogonal_pair_is_identity():
+    rng = np.random.default_rng(9)
+    H, dh, theta = 1, 8, 1e4
+    e = rng.standard_normal((8, 8)) + 3 * np.eye(8)
+    f = np.linalg.inv(e)
+    x = rng.standard_normal((6, 8))
+    pos = np.arange(6)
+    z = O.encode_k(x, pos, e, None, H, dh, theta)
+    np.testing.assert_allclose(O.decode_k(z, f, None, pos, H, dh, theta), x, atol=1e-10)
+    np.testing.assert_allclose(O.decode_v(O.encode_v(x, e, None), f, None, 8), x, atol=1e-10)
+
+
+def test_zero_code_gives_offset():
+    rng = np.random.default_rng(10)
+    H, dh, theta = 2, 8, 1e4
+    D = H * dh
+    mu = rng.standard_normal(D)
+    pos = np.array([0, 4, 9])
+    z = np.zeros((3, 5))
+    f = rng.standard_normal((D, 5))
+    np.testing.assert_allclose(O.decode_v(z, f, mu, D), np.tile(mu, (3, 1)), atol=0)
+    np.testing.assert_allclose(O.decode_k(z, f, mu, pos, H, dh, theta),
+                               rope_complex(np.tile(mu, (3, 1)), pos, H, dh, theta), atol=1e-14)
+
+
+@pytest.mark.parametrize("branch", ["k", "v"])
+def test_eckart_young_tail_energy(branch):
+    # Truncated SVD is the best rank-r approximation (Appendix F.1, Eckart-Young-Mirsky): with an
+    # exact synthetic SVD X - mu = U diag(s) B^T and the top-r right singular vectors as basis,
+    # the squared reconstruction error is the sum of the discarded squared singular values.
+    rng = np.random.default_rng(11)
+    H, dh, theta, r = 2, 16, 5e5, 9
+    D = H * dh
+    T = 80
+    u = rand_orthonormal(rng, T, D)
+    b = rand_orthonormal(rng, D, D)
+    s = np.sort(rng.uniform(0.1, 5.0, D))[::-1]
+    mu = rng.standard_normal(D)
+    content = mu[None, :] + (u * s[None, :]) @ b.T
+    pos = np.arange(T) + 11
+    qb = b[:, :r]
+    if branch == "k":
+        x = rope_complex(content, pos, H, dh, theta)
+        xr = O.decode_k(O.encode_k(x, pos, qb.T, mu, H, dh, theta), qb, mu, pos, H, dh, theta)
+    else:
+        x = content
+        xr = O.decode_v(O.encode_v(x, qb.T, mu), qb, mu, D)
+    err = np.sum((x - xr) ** 2)
+    np.testing.assert_allclose(err, np.sum(s[r:] ** 2), rtol=1e-10)
+    # and any other rank-r orthonormal basis does no better
+    qo = rand_orthonormal(rng, D, r)
+    if branch == "v":
+        xo = O.decode_v(O.encode_v(x, qo.T, mu), qo, mu, D)
+        assert np.sum((x - xo) ** 2) >= err
+
+
+def test_patch_identity_and_bias_only():
+    rng = np.random.default_rng(12)
+    H, dh, theta = 2, 8, 1e4
+    D = H * dh
+    T = 6
+    pos = np.array([0, 1, 2, 3, 100, 5000])
+    hh = rng.standard_normal((T, D))
+    eye = np.eye(D)
+    np.testing.assert_allclose(O.patch_v(hh, eye, None), hh, atol=0)
+    np.testing.assert_allclose(O.patch_k(hh, eye, None, pos, H, dh, theta),
+                               rope_complex(hh, pos, H, dh, theta), atol=1e-14)
+    b = rng.standard_normal(D)
+    zero = np.zeros((D, 7))
+    h7 = rng.standard_normal((T, 7))
+    np.testing.assert_allclose(O.patch_v(h7, zero, b), np.tile(b, (T, 1)), atol=0)
+    np.testing.assert_allclose(O.patch_k(h7, zero, b, pos, H, dh, theta),
+                               rope_complex(np.tile(b, (T, 1)), pos, H, dh, theta), atol=1e-14)
+
+
+def test_whole_model_routing_and_assembly():
+    rng = np.random.default_rng(13)
+    L, H, dh, d, theta = 5, 2, 8, 12, 1e4
+    D = H * dh
+    flags = [0, 1, 0, 0, 1]
+    T = 9
+    pos = np.arange(T)
+    r = 4
+    z = [rng.standard_normal((T, r)) for _ in range(L)]
+    f = [rng.standard_normal((D, r)) for _ in range(L)]
+    hh = [rng.standard_normal((T, d)) for _ in range(L)]
+    wk = [rng.standard_normal((D, d)) for _ in range(L)]
+    rk, rv = O.reuse_decode_all(flags, pos, H, dh, theta, z, z, f, f)
+    pk, pv = O.patch_all(flags, pos, H, dh, theta, hh, wk, wk)
+    ck, cv = O.assemble(flags, (rk, rv), (pk, pv))
+    for l in range(L):
+        assert ck[l] is not None and cv[l] is not None  # every layer filled: T_fill = 0
+        if flags[l]:
+            assert rk[l] is None and pk[l] is not None
+            np.testing.assert_allclose(cv[l], hh[l] @ wk[l].T)
+        else:
+            assert pk[l] is None and rk[l] is not None
+            np.testing.assert_allclose(cv[l], z[l] @ f[l].T)
