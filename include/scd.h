@@ -1,0 +1,176 @@
+/*
+ * scd.h -- C ABI of the SCD KV-state codec on MI355X (gfx950).
+ *
+ * Semantic Cache Distillation moves a consumer model's prefix KV cache as compact codes:
+ * the producer encodes each Reuse layer's de-RoPE'd keys and its values onto low-rank bases and
+ * each Patch layer's normalised attention input onto a code (Section 4.3.2, Eq. encode_z_kv;
+ * Section 4.4.1); the consumer decodes Reuse layers as code x basis (+ offset) and re-applies
+ * RoPE to keys (Eq. decode_kv), and regenerates Patch layers' KV by pushing the predicted
+ * normalised input through its own W_K / W_V with RoPE on keys (Section 4.4.2,
+ * Eq. kv_from_patch).  Algorithm 1 ("Split Inference with Reuse and Patch") fixes the order
+ * and the routing.  Every entry point below computes one of those steps on the GPU.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ *  - All tensors are dense, row-major and contiguous, in the model's dtype (scd_dtype_t):
+ *    fp32, or bf16 with fp32 accumulation and a single round-to-nearest-even at the store.
+ *  - Matrices use the [out, in] layout of a linear layer's weight, so every map is y = x W^T
+ *    (the paper writes x W with W of shape [in, out]; the maps are the same).
+ *  - The KV cache of one layer and branch is [T, H, d_h] (token-major, heads contiguous inside a
+ *    token), T = total packed tokens of the batch.  The consumer owns it; the library writes each
+ *    slot of a routed layer exactly once and never touches other layers.
+ *  - A basis of width w acts on rows of w consecutive channels: one token of D = H*d_h channels
+ *    is g = D / w code rows (w = D: one row per token; w = d_h: the head-shared basis, where
+ *    batch x heads x tokens form one sample axis, Section 4.1).  Codes are [T*g, r].
+ *  - Per-layer tensors are passed as HOST arrays of length n_layers holding DEVICE pointers.
+ *    Entries of layers the call does not route are ignored and may be NULL.
+ *  - RoPE pairs channel i of a head with channel i + d_h/2 and rotates the pair by
+ *    p * theta^(-2i/d_h), p the token's position in its own request (Section 4.1 names RoPE and
+ *    deRoPE as forward and inverse; Appendix F.2 keeps the framework's own cache positions).
+ *  - Device pointers must be 16-byte aligned.  Calls are asynchronous on the given stream, never
+ *    synchronise, and allocate nothing: the caller owns every buffer.
+ *  - Every argument is validated before any launch.  A non-OK status means nothing was launched
+ *    and no output was written; scd_last_error() then describes the problem.  Device-side
+ *    contents (cu_seqlens, pos0) are not validated: they must be non-decreasing with
+ *    cu_seqlens[0] = 0 and cu_seqlens[B] = n_tokens; positions at or beyond the RoPE table's
+ *    max_position give unspecified values (never an out-of-bounds access).
+ */
+#ifndef SCD_H_
+#define SCD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SCD_OK = 0,
+  SCD_ERR_NULL = 1,         /* a required pointer is NULL */
+  SCD_ERR_SHAPE = 2,        /* inconsistent or out-of-range sizes */
+  SCD_ERR_SCHEDULE = 3,     /* bad layer routing or ranks */
+  SCD_ERR_ALIGN = 4,        /* a device pointer is not 16-byte aligned */
+  SCD_ERR_UNSUPPORTED = 5,  /* valid per the paper but outside what the kernels implement */
+  SCD_ERR_WORKSPACE = 6,    /* RoPE table missing or too small */
+  SCD_ERR_HIP = 7           /* a HIP runtime call or kernel launch failed */
+} scd_status_t;
+
+typedef enum { SCD_F32 = 0, SCD_BF16 = 1 } scd_dtype_t;
+
+/* Model pair description (host memory, read only during the call).
+ * Section 4.1: layers 0..L-1 (0-based here); L_patch = {l : is_patch[l] != 0}, L_reuse its
+ * complement; independent branch ranks r_K, r_V, r_H.
+ * Supported by the kernels: head_dim a multiple of 32 and at most 256; basis_width a multiple of
+ * head_dim that divides D; every rank routed by a call a multiple of 16 with
+ * 16 <= rank_k, rank_v <= min(basis_width, 256) and 16 <= rank_h <= min(d_model, 256);
+ * d_model a multiple of 32. */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t basis_width;     /* w */
+  int32_t dtype;           /* scd_dtype_t: dtype of every tensor argument */
+  double rope_theta;
+  const uint8_t* is_patch; /* [n_layers] */
+  const int32_t* rank_k;   /* [n_layers] */
+  const int32_t* rank_v;   /* [n_layers] */
+  const int32_t* rank_h;   /* [n_layers] */
+} scd_model_t;
+
+/* A packed batch of B requests, T tokens in total (request b owns tokens
+ * [cu_seqlens[b], cu_seqlens[b+1])).  Positions restart at pos0[b] (0 when pos0 is NULL) for
+ * every request. */
+typedef struct {
+  int32_t n_seqs;              /* B >= 1 */
+  int64_t n_tokens;            /* T >= 0 */
+  const int32_t* cu_seqlens;   /* DEVICE [B+1], or NULL when B == 1 (one request of T tokens) */
+  const int32_t* pos0;         /* DEVICE [B], or NULL */
+} scd_batch_t;
+
+/* ---- RoPE table ------------------------------------------------------------------------------
+ * Opaque device table of rotation cosines and sines for positions [0, max_position), evaluated in
+ * fp64 and rounded once to fp32 (fp32-evaluated angles lose ~1e-5 absolute accuracy by position
+ * 512 and ~2e-3 by 32K).  It depends only on (head_dim, rope_theta, max_position): build it once
+ * per model and reuse it.  scd_rope_table_bytes returns its size; scd_rope_table fills it. */
+size_t scd_rope_table_bytes(const scd_model_t* model, int64_t max_position);
+scd_status_t scd_rope_table(const scd_model_t* model, int64_t max_position, void* table,
+                            size_t table_bytes, hipStream_t stream);
+
+/* ---- a1: token positions ---------------------------------------------------------------------
+ * pos_out[t] = t - cu_seqlens[b] + pos0[b] for every packed token t (DEVICE int32 [n_tokens]).
+ * The same mapping every RoPE/deRoPE step below uses internally. */
+scd_status_t scd_positions(const scd_batch_t* batch, int32_t* pos_out, hipStream_t stream);
+
+/* ---- a0: routing and payload (host only) -------------------------------------------------------
+ * scd_schedule writes the Reuse and Patch layer lists in increasing order (Section 4.5: the sets
+ * are fixed inputs, membership is a constant-time lookup).  Output arrays hold n_layers entries.
+ * scd_payload_bytes returns the bytes of the transmitted code set of Algorithm 1
+ * ({Z_K, Z_V} per Reuse layer, Z_H per Patch layer; O(T r), Section 4.5) for n_tokens tokens and,
+ * when offsets is not NULL, fills offsets[0..n_layers] with each layer's start in one packed buffer
+ * (layer order, K codes before V codes).  Returns 0 on invalid input. */
+scd_status_t scd_schedule(const scd_model_t* model, int32_t* reuse_layers, int32_t* n_reuse,
+                          int32_t* patch_layers, int32_t* n_patch);
+size_t scd_payload_bytes(const scd_model_t* model, int64_t n_tokens, int64_t* offsets);
+
+/* ---- a2-a4: producer encode (Section 4.3.2, Eq. encode_z_kv; Section 4.4.1; Algorithm 1) ----
+ * For every Reuse layer l:
+ *   z_k[l] = (rows(deRoPE(k_in[l])) - mu_k[l]) w_enc_k[l]^T      [T*g, rank_k[l]]
+ *   z_v[l] = (rows(v_in[l]) - mu_v[l]) w_enc_v[l]^T              [T*g, rank_v[l]]
+ * with k_in, v_in [T, H, d_h], w_enc_k [rank_k, w], w_enc_v [rank_v, w], mu [w] (the optional
+ * producer-side offset; NULL array or NULL entry = 0, which is the paper's equation).
+ * For every Patch layer l:  z_h[l] = h_in[l] w_enc_h[l]^T  with h_in [T, d_model] (the producer's
+ * normalised attention input) and w_enc_h [rank_h, d_model]; z_h [T, rank_h]. */
+scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
+                        const void* rope_table, int64_t max_position,
+                        const void* const* k_in, const void* const* v_in,
+                        const void* const* h_in,
+                        const void* const* w_enc_k, const void* const* w_enc_v,
+                        const void* const* w_enc_h,
+                        const void* const* mu_k, const void* const* mu_v,
+                        void* const* z_k, void* const* z_v, void* const* z_h,
+                        hipStream_t stream);
+
+/* ---- a5-a6, a8: consumer Reuse decode (Section 4.3.2, Eq. decode_kv; Algorithm 1) ------------
+ * For every Reuse layer l, written straight into the consumer's cache:
+ *   k_cache[l] = RoPE(unrows(z_k[l] w_dec_k[l]^T + mu_k[l]))     [T, H, d_h]
+ *   v_cache[l] = unrows(z_v[l] w_dec_v[l]^T + mu_v[l])           [T, H, d_h]
+ * with z [T*g, rank], w_dec [w, rank] and mu [w] the optional consumer-side offset (NULL = 0).
+ * The paper writes one W_dec,B for both branches; keys and values are fitted independently
+ * (Section 4.3.1), so each branch takes its own decoder.  Patch layers are not touched. */
+scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
+                              const void* rope_table, int64_t max_position,
+                              const void* const* z_k, const void* const* z_v,
+                              const void* const* w_dec_k, const void* const* w_dec_v,
+                              const void* const* mu_k, const void* const* mu_v,
+                              void* const* k_cache, void* const* v_cache, hipStream_t stream);
+
+/* ---- a7, a8: consumer Patch (Section 4.4.2, Eq. kv_from_patch; Appendix F.2; Algorithm 1) ----
+ * For every Patch layer l, written straight into the consumer's cache:
+ *   k_cache[l] = RoPE(h_hat[l] w_k[l]^T + b_k[l]),   v_cache[l] = h_hat[l] w_v[l]^T + b_v[l]
+ * with h_hat [T, d_model] the predicted normalised attention input (the aligner's output; this
+ * call does not normalise), w_k, w_v [D, d_model] the consumer's own key/value projection weights
+ * and b_k, b_v [D] optional projection biases (NULL array or NULL entry = none, as in the paper).
+ * Reuse layers are not touched. */
+scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
+                          const void* rope_table, int64_t max_position,
+                          const void* const* h_hat,
+                          const void* const* w_k, const void* const* w_v,
+                          const void* const* b_k, const void* const* b_v,
+                          void* const* k_cache, void* const* v_cache, hipStream_t stream);
+
+/* ---- diagnostics ---------------------------------------------------------------------------- */
+const char* scd_status_string(scd_status_t status);
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char* scd_last_error(void);
+/* ABI version: bumped whenever a signature or a struct above changes. */
+int32_t scd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCD_H_ */

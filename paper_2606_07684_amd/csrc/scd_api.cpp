@@ -1,0 +1,396 @@
+// Host side of the SCD codec's C ABI: argument validation, routing, job tables and launches.
+//
+// Every entry point validates all of its arguments before the first launch, so a non-OK status
+// means nothing ran.  No entry point allocates, synchronises or keeps state beyond the
+// thread-local text of the last error.
+#include "../../include/scd.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "scd_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+scd_status_t fail(scd_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+scd_status_t ok() {
+  g_last_error.clear();
+  return SCD_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+scd_status_t check_model(const scd_model_t* m) {
+  if (m == nullptr) return fail(SCD_ERR_NULL, "model is NULL");
+  if (m->is_patch == nullptr || m->rank_k == nullptr || m->rank_v == nullptr ||
+      m->rank_h == nullptr)
+    return fail(SCD_ERR_NULL, "model routing or rank arrays are NULL");
+  if (m->n_layers < 1) return fail(SCD_ERR_SHAPE, "n_layers must be >= 1 (got %d)", m->n_layers);
+  if (m->n_kv_heads < 1) return fail(SCD_ERR_SHAPE, "n_kv_heads must be >= 1 (got %d)", m->n_kv_heads);
+  if (m->head_dim <= 0 || (m->head_dim & 1))
+    return fail(SCD_ERR_SHAPE, "head_dim must be positive and even (got %d)", m->head_dim);
+  if (m->head_dim != 32 && m->head_dim != 64 && m->head_dim != 128)
+    return fail(SCD_ERR_UNSUPPORTED, "head_dim %d unsupported (32, 64 or 128)", m->head_dim);
+  const int64_t D = static_cast<int64_t>(m->n_kv_heads) * m->head_dim;
+  if (m->basis_width <= 0 || m->basis_width % m->head_dim != 0 || D % m->basis_width != 0)
+    return fail(SCD_ERR_SHAPE,
+                "basis_width %d must be a multiple of head_dim %d that divides D = %lld",
+                m->basis_width, m->head_dim, static_cast<long long>(D));
+  if (m->d_model <= 0 || m->d_model % 32 != 0)
+    return fail(SCD_ERR_UNSUPPORTED, "d_model %d must be a positive multiple of 32", m->d_model);
+  if (m->dtype != SCD_F32 && m->dtype != SCD_BF16)
+    return fail(SCD_ERR_SHAPE, "dtype %d unknown", m->dtype);
+  if (!(m->rope_theta > 1.0)) return fail(SCD_ERR_SHAPE, "rope_theta must be > 1");
+  return SCD_OK;
+}
+
+scd_status_t check_rank(const char* what, int layer, int32_t r, int32_t hi) {
+  if (r < 16 || r % 16 != 0 || r > hi)
+    return fail(SCD_ERR_SCHEDULE, "%s of layer %d is %d; must be a multiple of 16 in [16, %d]",
+                what, layer, r, hi);
+  return SCD_OK;
+}
+
+scd_status_t check_batch(const scd_batch_t* b) {
+  if (b == nullptr) return fail(SCD_ERR_NULL, "batch is NULL");
+  if (b->n_seqs < 1) return fail(SCD_ERR_SHAPE, "n_seqs must be >= 1 (got %d)", b->n_seqs);
+  if (b->n_tokens < 0) return fail(SCD_ERR_SHAPE, "n_tokens must be >= 0");
+  if (b->n_tokens > (int64_t{1} << 31) - 1)
+    return fail(SCD_ERR_UNSUPPORTED, "n_tokens above 2^31 - 1");
+  if (b->cu_seqlens == nullptr && b->n_seqs != 1)
+    return fail(SCD_ERR_NULL, "cu_seqlens is NULL but n_seqs = %d", b->n_seqs);
+  return SCD_OK;
+}
+
+scd_status_t check_rope(const void* table, int64_t max_position) {
+  if (table == nullptr) return fail(SCD_ERR_WORKSPACE, "RoPE table is NULL");
+  if (!aligned16(table)) return fail(SCD_ERR_ALIGN, "RoPE table is not 16-byte aligned");
+  if (max_position < 1) return fail(SCD_ERR_WORKSPACE, "max_position must be >= 1");
+  return SCD_OK;
+}
+
+// A required per-layer device pointer: the array and its entry must be non-NULL and aligned.
+scd_status_t need_ptr(const void* const* arr, int layer, const char* name) {
+  if (arr == nullptr) return fail(SCD_ERR_NULL, "%s array is NULL", name);
+  if (arr[layer] == nullptr) return fail(SCD_ERR_NULL, "%s[%d] is NULL", name, layer);
+  if (!aligned16(arr[layer]))
+    return fail(SCD_ERR_ALIGN, "%s[%d] is not 16-byte aligned", name, layer);
+  return SCD_OK;
+}
+
+// An optional per-layer device pointer: NULL array or NULL entry means absent.
+scd_status_t opt_ptr(const void* const* arr, int layer, const char* name, const void** out) {
+  *out = (arr == nullptr) ? nullptr : arr[layer];
+  if (*out != nullptr && !aligned16(*out))
+    return fail(SCD_ERR_ALIGN, "%s[%d] is not 16-byte aligned", name, layer);
+  return SCD_OK;
+}
+
+#define SCD_TRY(expr)                  \
+  do {                                 \
+    const scd_status_t s_ = (expr);    \
+    if (s_ != SCD_OK) return s_;       \
+  } while (0)
+
+// Packs jobs into launches of at most kMaxJobs jobs each.
+class JobPacker {
+ public:
+  JobPacker(const scd::GemmParams& base, int bm, int bn) : base_(base), bm_(bm), bn_(bn) {}
+  void add(const scd::GemmJob& j) { jobs_.push_back(j); }
+  std::vector<scd::GemmParams> build() const {
+    std::vector<scd::GemmParams> out;
+    const int64_t mt = (base_.m + bm_ - 1) / bm_;
+    for (size_t s = 0; s < jobs_.size(); s += scd::kMaxJobs) {
+      scd::GemmParams p = base_;
+      p.n_jobs = 0;
+      int64_t tiles = 0;
+      for (size_t i = s; i < jobs_.size() && i < s + scd::kMaxJobs; ++i) {
+        scd::GemmJob j = jobs_[i];
+        j.tile_begin = static_cast<int32_t>(tiles);
+        tiles += mt * ((j.n + bn_ - 1) / bn_);
+        p.jobs[p.n_jobs++] = j;
+      }
+      p.total_tiles = static_cast<int32_t>(tiles);
+      out.push_back(p);
+    }
+    return out;
+  }
+
+ private:
+  scd::GemmParams base_;
+  int bm_, bn_;
+  std::vector<scd::GemmJob> jobs_;
+};
+
+scd::GemmParams base_params(const scd_model_t* m, const scd_batch_t* b, int64_t rows, int g,
+                            const void* rope, int64_t max_pos) {
+  scd::GemmParams p{};
+  p.n_jobs = 0;
+  p.total_tiles = 0;
+  p.m = rows;
+  p.g = g;
+  p.head_dim = m->head_dim;
+  p.n_seqs = b->n_seqs;
+  p.cu_seqlens = b->cu_seqlens;
+  p.pos0 = b->pos0;
+  p.rope = static_cast<const float2*>(rope);
+  p.max_pos = max_pos;
+  return p;
+}
+
+scd_status_t run(const std::vector<scd::GemmParams>& launches, int dtype, hipStream_t stream) {
+  for (const auto& p : launches) {
+    const hipError_t e = dtype == SCD_BF16 ? scd::launch_gemm_bf16(p, stream)
+                                           : scd::launch_gemm_f32(p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+int64_t kv_width(const scd_model_t* m) {
+  return static_cast<int64_t>(m->n_kv_heads) * m->head_dim;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t scd_abi_version(void) { return 1; }
+
+const char* scd_status_string(scd_status_t s) {
+  switch (s) {
+    case SCD_OK: return "ok";
+    case SCD_ERR_NULL: return "null pointer";
+    case SCD_ERR_SHAPE: return "invalid shape";
+    case SCD_ERR_SCHEDULE: return "invalid schedule or rank";
+    case SCD_ERR_ALIGN: return "misaligned pointer";
+    case SCD_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SCD_ERR_WORKSPACE: return "missing or invalid RoPE table";
+    case SCD_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* scd_last_error(void) { return g_last_error.c_str(); }
+
+size_t scd_rope_table_bytes(const scd_model_t* model, int64_t max_position) {
+  if (model == nullptr || model->head_dim <= 0 || max_position < 1) return 0;
+  return static_cast<size_t>(max_position) * static_cast<size_t>(model->head_dim / 2) *
+         sizeof(float2);
+}
+
+scd_status_t scd_rope_table(const scd_model_t* model, int64_t max_position, void* table,
+                            size_t table_bytes, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_rope(table, max_position));
+  if (table_bytes < scd_rope_table_bytes(model, max_position))
+    return fail(SCD_ERR_WORKSPACE, "table_bytes %zu < %zu needed", table_bytes,
+                scd_rope_table_bytes(model, max_position));
+  if (max_position > (int64_t{1} << 31))
+    return fail(SCD_ERR_UNSUPPORTED, "max_position above 2^31");
+  const hipError_t e = scd::launch_rope_table(static_cast<float2*>(table), max_position,
+                                              model->head_dim, model->rope_theta, stream);
+  if (e != hipSuccess) return fail(SCD_ERR_HIP, "rope table launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+scd_status_t scd_positions(const scd_batch_t* batch, int32_t* pos_out, hipStream_t stream) {
+  SCD_TRY(check_batch(batch));
+  if (batch->n_tokens == 0) return ok();
+  if (pos_out == nullptr) return fail(SCD_ERR_NULL, "pos_out is NULL");
+  const hipError_t e = scd::launch_positions(pos_out, batch->n_tokens, batch->n_seqs,
+                                             batch->cu_seqlens, batch->pos0, stream);
+  if (e != hipSuccess) return fail(SCD_ERR_HIP, "positions launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+scd_status_t scd_schedule(const scd_model_t* model, int32_t* reuse_layers, int32_t* n_reuse,
+                          int32_t* patch_layers, int32_t* n_patch) {
+  if (model == nullptr || model->is_patch == nullptr) return fail(SCD_ERR_NULL, "model is NULL");
+  if (model->n_layers < 1) return fail(SCD_ERR_SHAPE, "n_layers must be >= 1");
+  if (n_reuse == nullptr || n_patch == nullptr) return fail(SCD_ERR_NULL, "count outputs are NULL");
+  int32_t nr = 0, np = 0;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) {
+      if (patch_layers != nullptr) patch_layers[np] = l;
+      ++np;
+    } else {
+      if (reuse_layers != nullptr) reuse_layers[nr] = l;
+      ++nr;
+    }
+  }
+  *n_reuse = nr;
+  *n_patch = np;
+  return ok();
+}
+
+size_t scd_payload_bytes(const scd_model_t* model, int64_t n_tokens, int64_t* offsets) {
+  if (check_model(model) != SCD_OK || n_tokens < 0) return 0;
+  const int64_t g = kv_width(model) / model->basis_width;
+  const int64_t eb = model->dtype == SCD_BF16 ? 2 : 4;
+  int64_t total = 0;
+  if (offsets != nullptr) offsets[0] = 0;
+  for (int l = 0; l < model->n_layers; ++l) {
+    const int64_t n = model->is_patch[l]
+                          ? n_tokens * model->rank_h[l]
+                          : n_tokens * g * (int64_t{model->rank_k[l]} + model->rank_v[l]);
+    total += n * eb;
+    if (offsets != nullptr) offsets[l + 1] = total;
+  }
+  return static_cast<size_t>(total);
+}
+
+scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
+                        const void* rope_table, int64_t max_position,
+                        const void* const* k_in, const void* const* v_in,
+                        const void* const* h_in,
+                        const void* const* w_enc_k, const void* const* w_enc_v,
+                        const void* const* w_enc_h,
+                        const void* const* mu_k, const void* const* mu_v,
+                        void* const* z_k, void* const* z_v, void* const* z_h,
+                        hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  const int w = model->basis_width;
+  const int g = static_cast<int>(kv_width(model) / w);
+  const int rk_max = w < 256 ? w : 256;
+  const int rh_max = model->d_model < 256 ? model->d_model : 256;
+  bool any_reuse = false;
+  for (int l = 0; l < model->n_layers; ++l) {
+    const void* tmp;
+    if (model->is_patch[l]) {
+      SCD_TRY(check_rank("rank_h", l, model->rank_h[l], rh_max));
+      SCD_TRY(need_ptr(h_in, l, "h_in"));
+      SCD_TRY(need_ptr(w_enc_h, l, "w_enc_h"));
+      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_h), l, "z_h"));
+    } else {
+      any_reuse = true;
+      SCD_TRY(check_rank("rank_k", l, model->rank_k[l], rk_max));
+      SCD_TRY(check_rank("rank_v", l, model->rank_v[l], rk_max));
+      SCD_TRY(need_ptr(k_in, l, "k_in"));
+      SCD_TRY(need_ptr(v_in, l, "v_in"));
+      SCD_TRY(need_ptr(w_enc_k, l, "w_enc_k"));
+      SCD_TRY(need_ptr(w_enc_v, l, "w_enc_v"));
+      SCD_TRY(opt_ptr(mu_k, l, "mu_k", &tmp));
+      SCD_TRY(opt_ptr(mu_v, l, "mu_v", &tmp));
+      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_k), l, "z_k"));
+      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_v), l, "z_v"));
+    }
+  }
+  if (any_reuse && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
+  if (batch->n_tokens == 0) return ok();
+
+  const int64_t T = batch->n_tokens;
+  JobPacker kv(base_params(model, batch, T * g, g, rope_table, max_position), scd::kGenericBM,
+               scd::kGenericBN);
+  JobPacker hh(base_params(model, batch, T, 1, rope_table, max_position), scd::kGenericBM,
+               scd::kGenericBN);
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) {
+      hh.add({h_in[l], w_enc_h[l], z_h[l], nullptr, nullptr, model->rank_h[l], model->d_model, 0, 0});
+    } else {
+      const void* mk = mu_k ? mu_k[l] : nullptr;
+      const void* mv = mu_v ? mu_v[l] : nullptr;
+      kv.add({k_in[l], w_enc_k[l], z_k[l], nullptr, mk, model->rank_k[l], w, scd::kDeropeIn, 0});
+      kv.add({v_in[l], w_enc_v[l], z_v[l], nullptr, mv, model->rank_v[l], w, 0, 0});
+    }
+  }
+  SCD_TRY(run(kv.build(), model->dtype, stream));
+  return run(hh.build(), model->dtype, stream);
+}
+
+scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
+                              const void* rope_table, int64_t max_position,
+                              const void* const* z_k, const void* const* z_v,
+                              const void* const* w_dec_k, const void* const* w_dec_v,
+                              const void* const* mu_k, const void* const* mu_v,
+                              void* const* k_cache, void* const* v_cache, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  const int w = model->basis_width;
+  const int g = static_cast<int>(kv_width(model) / w);
+  const int rk_max = w < 256 ? w : 256;
+  bool any = false;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) continue;
+    any = true;
+    const void* tmp;
+    SCD_TRY(check_rank("rank_k", l, model->rank_k[l], rk_max));
+    SCD_TRY(check_rank("rank_v", l, model->rank_v[l], rk_max));
+    SCD_TRY(need_ptr(z_k, l, "z_k"));
+    SCD_TRY(need_ptr(z_v, l, "z_v"));
+    SCD_TRY(need_ptr(w_dec_k, l, "w_dec_k"));
+    SCD_TRY(need_ptr(w_dec_v, l, "w_dec_v"));
+    SCD_TRY(opt_ptr(mu_k, l, "mu_k", &tmp));
+    SCD_TRY(opt_ptr(mu_v, l, "mu_v", &tmp));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache"));
+  }
+  if (any && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
+  if (!any || batch->n_tokens == 0) return ok();
+
+  const int64_t T = batch->n_tokens;
+  JobPacker jp(base_params(model, batch, T * g, g, rope_table, max_position), scd::kGenericBM,
+               scd::kGenericBN);
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) continue;
+    const void* mk = mu_k ? mu_k[l] : nullptr;
+    const void* mv = mu_v ? mu_v[l] : nullptr;
+    jp.add({z_k[l], w_dec_k[l], k_cache[l], mk, nullptr, w, model->rank_k[l], scd::kRopeOut, 0});
+    jp.add({z_v[l], w_dec_v[l], v_cache[l], mv, nullptr, w, model->rank_v[l], 0, 0});
+  }
+  return run(jp.build(), model->dtype, stream);
+}
+
+scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
+                          const void* rope_table, int64_t max_position,
+                          const void* const* h_hat,
+                          const void* const* w_k, const void* const* w_v,
+                          const void* const* b_k, const void* const* b_v,
+                          void* const* k_cache, void* const* v_cache, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  bool any = false;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    any = true;
+    const void* tmp;
+    SCD_TRY(need_ptr(h_hat, l, "h_hat"));
+    SCD_TRY(need_ptr(w_k, l, "w_k"));
+    SCD_TRY(need_ptr(w_v, l, "w_v"));
+    SCD_TRY(opt_ptr(b_k, l, "b_k", &tmp));
+    SCD_TRY(opt_ptr(b_v, l, "b_v", &tmp));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache"));
+  }
+  if (any && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
+  if (!any || batch->n_tokens == 0) return ok();
+
+  const int64_t T = batch->n_tokens;
+  const int D = static_cast<int>(kv_width(model));
+  JobPacker jp(base_params(model, batch, T, 1, rope_table, max_position), scd::kGenericBM,
+               scd::kGenericBN);
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    const void* bk = b_k ? b_k[l] : nullptr;
+    const void* bv = b_v ? b_v[l] : nullptr;
+    jp.add({h_hat[l], w_k[l], k_cache[l], bk, nullptr, D, model->d_model, scd::kRopeOut, 0});
+    jp.add({h_hat[l], w_v[l], v_cache[l], bv, nullptr, D, model->d_model, 0, 0});
+  }
+  return run(jp.build(), model->dtype, stream);
+}
+
+}  // extern "C"

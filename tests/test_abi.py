@@ -1,0 +1,194 @@
+"""C ABI tests that need no GPU: the library loads and exports every declared symbol, every
+validation path returns its status before any launch, and the host-only entry points (routing and
+payload accounting) agree bit for bit with the oracle."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_07684_amd as scd
+from oracle import scd_oracle as O
+from synth import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "scd.h")
+
+OK, NULL, SHAPE, SCHED, ALIGN, UNSUP, WS, HIP = range(8)
+FAKE = 0x7f0000000000  # a 16-byte aligned address that is never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return scd.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(scd_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(lib, n), f"libscd.so does not export {n}"
+    assert set(names) == set(scd.EXPORTED_SYMBOLS)
+    assert scd.scd_abi_version() == 1
+
+
+def test_status_strings(lib):
+    for s in range(8):
+        assert lib.scd_status_string(s)
+    assert lib.scd_status_string(99) == b"unknown status"
+
+
+def _model(**kw):
+    base = dict(n_layers=3, d_model=256, n_kv_heads=2, head_dim=64, rope_theta=1e4, dtype="bf16",
+                is_patch=[0, 1, 0], rank_k=[32, 32, 32], rank_v=[32, 32, 32],
+                rank_h=[32, 32, 32])
+    base.update(kw)
+    return scd.Model(**base)
+
+
+def _ptrs(L, value=FAKE, skip=()):
+    arr = (ctypes.c_void_p * L)()
+    for l in range(L):
+        if l not in skip:
+            arr[l] = value
+    return ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), arr
+
+
+def _decode(lib, model, batch, rope=FAKE, maxp=100, **over):
+    L = model.n_layers
+    keep = []
+    args = {}
+    for name in ("z_k", "z_v", "w_dec_k", "w_dec_v", "mu_k", "mu_v", "k_cache", "v_cache"):
+        if name in over:
+            args[name] = over[name]
+        else:
+            p, a = _ptrs(L)
+            keep.append(a)
+            args[name] = p
+    st = lib.scd_reuse_decode(ctypes.byref(model._c), ctypes.byref(batch._c), rope, maxp,
+                              args["z_k"], args["z_v"], args["w_dec_k"], args["w_dec_v"],
+                              args["mu_k"], args["mu_v"], args["k_cache"], args["v_cache"], None)
+    return st, lib.scd_last_error().decode()
+
+
+def _batch(n_tokens=10, n_seqs=1, cu=None):
+    b = scd.Batch(n_tokens=n_tokens)
+    b._c.n_seqs = n_seqs
+    b._c.cu_seqlens = cu
+    return b
+
+
+def test_validation_paths_return_before_launch(lib):
+    m = _model()
+    b = _batch()
+    # model problems
+    assert lib.scd_reuse_decode(None, ctypes.byref(b._c), FAKE, 10, *([None] * 8), None) == NULL
+    assert _decode(lib, _model(head_dim=80, rope_theta=1e4), b)[0] == UNSUP
+    mm = _model()
+    mm._c.head_dim = 63
+    assert _decode(lib, mm, b)[0] == SHAPE
+    assert _decode(lib, _model(basis_width=96), b)[0] == SHAPE
+    assert _decode(lib, _model(d_model=250), b)[0] == UNSUP
+    mm = _model()
+    mm._c.dtype = 7
+    assert _decode(lib, mm, b)[0] == SHAPE
+    # ranks
+    st, msg = _decode(lib, _model(rank_k=[32, 32, 40]), b)
+    assert st == SCHED and "rank_k of layer 2" in msg
+    assert _decode(lib, _model(rank_v=[256, 32, 32]), b)[0] == SCHED  # > basis width 128
+    assert _decode(lib, _model(rank_v=[0, 32, 32]), b)[0] == SCHED
+    # patch layer ranks are not the decode's business
+    assert _decode(lib, _model(rank_k=[32, 8, 32]), _batch(n_tokens=0))[0] == OK
+    # batch problems
+    assert _decode(lib, m, _batch(n_seqs=0))[0] == SHAPE
+    assert _decode(lib, m, _batch(n_tokens=-1))[0] == SHAPE
+    assert _decode(lib, m, _batch(n_seqs=3, cu=None))[0] == NULL
+    # pointers
+    p, keep = _ptrs(3, skip=(2,))
+    st, msg = _decode(lib, m, b, z_k=p)
+    assert st == NULL and "z_k[2]" in msg
+    p2, keep2 = _ptrs(3, skip=(0,))  # layer 0 missing but ... layer 0 is Reuse: required
+    assert _decode(lib, m, b, k_cache=p2)[0] == NULL
+    p3, keep3 = _ptrs(3, skip=(1,))  # layer 1 is Patch: entry ignored
+    assert _decode(lib, m, _batch(n_tokens=0), z_v=p3)[0] == OK
+    p4, keep4 = _ptrs(3, value=FAKE + 2)
+    assert _decode(lib, m, b, v_cache=p4)[0] == ALIGN
+    # RoPE table
+    assert _decode(lib, m, b, rope=None)[0] == WS
+    assert _decode(lib, m, b, rope=FAKE + 4)[0] == ALIGN
+    assert _decode(lib, m, b, maxp=0)[0] == WS
+    assert lib.scd_last_error().decode() != ""
+
+
+def test_zero_tokens_is_ok_without_launch(lib):
+    m = _model()
+    assert _decode(lib, m, _batch(n_tokens=0), rope=None)[0] == OK
+    assert lib.scd_last_error().decode() == ""
+    L = m.n_layers
+    p, keep = _ptrs(L)
+    st = lib.scd_patch_kv(ctypes.byref(m._c), ctypes.byref(_batch(n_tokens=0)._c), None, 0,
+                          p, p, p, None, None, p, p, None)
+    assert st == OK
+    st = lib.scd_encode(ctypes.byref(m._c), ctypes.byref(_batch(n_tokens=0)._c), None, 0,
+                        *([p] * 6), None, None, p, p, p, None)
+    assert st == OK
+
+
+def test_encode_and_patch_validation(lib):
+    m = _model()
+    b = _batch()
+    L = m.n_layers
+    p, keep = _ptrs(L)
+    q, keepq = _ptrs(L, skip=(1,))
+    # encode: Patch layer 1 needs h_in
+    st = lib.scd_encode(ctypes.byref(m._c), ctypes.byref(b._c), FAKE, 10, p, p, q, p, p, p,
+                        None, None, p, p, p, None)
+    assert st == NULL and "h_in[1]" in lib.scd_last_error().decode()
+    # encode: rank_h above d_model
+    mh = _model(rank_h=[32, 512, 32])
+    st = lib.scd_encode(ctypes.byref(mh._c), ctypes.byref(b._c), FAKE, 10, *([p] * 6), None,
+                        None, p, p, p, None)
+    assert st == SCHED
+    # patch: bias entries optional but must be aligned
+    r, keepr = _ptrs(L, value=FAKE + 8)
+    st = lib.scd_patch_kv(ctypes.byref(m._c), ctypes.byref(b._c), FAKE, 10, p, p, p, r, None, p,
+                          p, None)
+    assert st == ALIGN
+    st = lib.scd_patch_kv(ctypes.byref(m._c), ctypes.byref(b._c), None, 10, p, p, p, None, None,
+                          p, p, None)
+    assert st == WS
+    # positions / rope-table argument checks
+    assert lib.scd_positions(ctypes.byref(b._c), None, None) == NULL
+    assert lib.scd_rope_table(ctypes.byref(m._c), 0, FAKE, 1 << 20, None) == WS
+    need = lib.scd_rope_table_bytes(ctypes.byref(m._c), 100)
+    assert need == 100 * 32 * 8
+    assert lib.scd_rope_table(ctypes.byref(m._c), 100, FAKE, need - 1, None) == WS
+
+
+@pytest.mark.parametrize("wl", [*W.CONFIGS, *W.TEST_WORKLOADS], ids=lambda w: w.name)
+def test_schedule_and_payload_match_oracle(wl):
+    m = scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
+                  head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
+                  is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.ranks, rank_h=wl.ranks,
+                  basis_width=wl.w)
+    reuse, patch = scd.scd_schedule(m)
+    assert (reuse, patch) == O.schedule(wl.is_patch)
+    total, offs = scd.scd_payload_bytes(m, wl.n_tokens)
+    t2, o2 = O.payload_bytes(wl.is_patch, wl.n_tokens, wl.n_kv_heads, wl.head_dim, wl.w,
+                             wl.ranks, wl.ranks, wl.ranks, wl.elem_bytes)
+    assert total == t2 and offs == o2
+
+
+def test_workload_shapes_are_the_stated_ones():
+    assert W.BATCHED.n_tokens == 111169 and W.BATCHED.n_seqs == 16
+    assert min(W.BATCHED.seq_lens) >= 1024 and max(W.BATCHED.seq_lens) <= 16384
+    assert W.LLAMA3_8B.patch_layers == (0, 8, 16, 24)
+    assert W.LLAMA3_70B.patch_layers == tuple(range(0, 80, 10))
+    assert W.QWEN2_7B.n_tokens == 32768 and W.QWEN2_7B.kv_width == 512
+    assert W.TINY_F32.kv_width == 256 and W.TINY_F32.is_patch == (0, 0, 1, 0)
