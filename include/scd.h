@@ -23,7 +23,8 @@
  *    is g = D / w code rows (w = D: one row per token; w = d_h: the head-shared basis, where
  *    batch x heads x tokens form one sample axis, Section 4.1).  Codes are [T*g, r].
  *  - Per-layer tensors are passed as HOST arrays of length n_layers holding DEVICE pointers.
- *    Entries of layers the call does not route are ignored and may be NULL.
+ *    Entries of layers the call does not route are ignored and may be NULL.  When the batch has
+ *    no tokens every call is a no-op, and buffers sized by the token count may be NULL.
  *  - RoPE pairs channel i of a head with channel i + d_h/2 and rotates the pair by
  *    p * theta^(-2i/d_h), p the token's position in its own request (Section 4.1 names RoPE and
  *    deRoPE as forward and inverse; Appendix F.2 keeps the framework's own cache positions).
@@ -63,8 +64,8 @@ typedef enum { SCD_F32 = 0, SCD_BF16 = 1 } scd_dtype_t;
 /* Model pair description (host memory, read only during the call).
  * Section 4.1: layers 0..L-1 (0-based here); L_patch = {l : is_patch[l] != 0}, L_reuse its
  * complement; independent branch ranks r_K, r_V, r_H.
- * Supported by the kernels: head_dim a multiple of 32 and at most 256; basis_width a multiple of
- * head_dim that divides D; every rank routed by a call a multiple of 16 with
+ * Supported by the kernels: head_dim 32, 64 or 128; basis_width a multiple of head_dim that
+ * divides D; every rank routed by a call a multiple of 16 with
  * 16 <= rank_k, rank_v <= min(basis_width, 256) and 16 <= rank_h <= min(d_model, 256);
  * d_model a multiple of 32. */
 typedef struct {

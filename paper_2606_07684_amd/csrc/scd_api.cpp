@@ -91,6 +91,12 @@ scd_status_t need_ptr(const void* const* arr, int layer, const char* name) {
   return SCD_OK;
 }
 
+// A per-layer buffer sized by the token count: it may be NULL when the batch has no tokens.
+scd_status_t need_tok_ptr(const void* const* arr, int layer, const char* name, int64_t n_tokens) {
+  if (n_tokens == 0 && (arr == nullptr || arr[layer] == nullptr)) return SCD_OK;
+  return need_ptr(arr, layer, name);
+}
+
 // An optional per-layer device pointer: NULL array or NULL entry means absent.
 scd_status_t opt_ptr(const void* const* arr, int layer, const char* name, const void** out) {
   *out = (arr == nullptr) ? nullptr : arr[layer];
@@ -273,21 +279,21 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
     const void* tmp;
     if (model->is_patch[l]) {
       SCD_TRY(check_rank("rank_h", l, model->rank_h[l], rh_max));
-      SCD_TRY(need_ptr(h_in, l, "h_in"));
+      SCD_TRY(need_tok_ptr(h_in, l, "h_in", batch->n_tokens));
       SCD_TRY(need_ptr(w_enc_h, l, "w_enc_h"));
-      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_h), l, "z_h"));
+      SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(z_h), l, "z_h", batch->n_tokens));
     } else {
       any_reuse = true;
       SCD_TRY(check_rank("rank_k", l, model->rank_k[l], rk_max));
       SCD_TRY(check_rank("rank_v", l, model->rank_v[l], rk_max));
-      SCD_TRY(need_ptr(k_in, l, "k_in"));
-      SCD_TRY(need_ptr(v_in, l, "v_in"));
+      SCD_TRY(need_tok_ptr(k_in, l, "k_in", batch->n_tokens));
+      SCD_TRY(need_tok_ptr(v_in, l, "v_in", batch->n_tokens));
       SCD_TRY(need_ptr(w_enc_k, l, "w_enc_k"));
       SCD_TRY(need_ptr(w_enc_v, l, "w_enc_v"));
       SCD_TRY(opt_ptr(mu_k, l, "mu_k", &tmp));
       SCD_TRY(opt_ptr(mu_v, l, "mu_v", &tmp));
-      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_k), l, "z_k"));
-      SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(z_v), l, "z_v"));
+      SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(z_k), l, "z_k", batch->n_tokens));
+      SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(z_v), l, "z_v", batch->n_tokens));
     }
   }
   if (any_reuse && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
@@ -330,14 +336,14 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
     const void* tmp;
     SCD_TRY(check_rank("rank_k", l, model->rank_k[l], rk_max));
     SCD_TRY(check_rank("rank_v", l, model->rank_v[l], rk_max));
-    SCD_TRY(need_ptr(z_k, l, "z_k"));
-    SCD_TRY(need_ptr(z_v, l, "z_v"));
+    SCD_TRY(need_tok_ptr(z_k, l, "z_k", batch->n_tokens));
+    SCD_TRY(need_tok_ptr(z_v, l, "z_v", batch->n_tokens));
     SCD_TRY(need_ptr(w_dec_k, l, "w_dec_k"));
     SCD_TRY(need_ptr(w_dec_v, l, "w_dec_v"));
     SCD_TRY(opt_ptr(mu_k, l, "mu_k", &tmp));
     SCD_TRY(opt_ptr(mu_v, l, "mu_v", &tmp));
-    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache"));
-    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache"));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache", batch->n_tokens));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache", batch->n_tokens));
   }
   if (any && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
   if (!any || batch->n_tokens == 0) return ok();
@@ -368,13 +374,13 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
     if (!model->is_patch[l]) continue;
     any = true;
     const void* tmp;
-    SCD_TRY(need_ptr(h_hat, l, "h_hat"));
+    SCD_TRY(need_tok_ptr(h_hat, l, "h_hat", batch->n_tokens));
     SCD_TRY(need_ptr(w_k, l, "w_k"));
     SCD_TRY(need_ptr(w_v, l, "w_v"));
     SCD_TRY(opt_ptr(b_k, l, "b_k", &tmp));
     SCD_TRY(opt_ptr(b_v, l, "b_v", &tmp));
-    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache"));
-    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache"));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache", batch->n_tokens));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache", batch->n_tokens));
   }
   if (any && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
   if (!any || batch->n_tokens == 0) return ok();
