@@ -27,6 +27,7 @@ __all__ = [
     "Model", "Batch", "RopeTable", "ScdError", "lib_path", "load_library",
     "scd_rope_table", "scd_positions", "scd_schedule", "scd_payload_bytes",
     "scd_encode", "scd_reuse_decode", "scd_patch_kv", "scd_abi_version",
+    "Prepared", "prepare_encode", "prepare_reuse_decode", "prepare_patch_kv",
 ]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -293,8 +294,19 @@ def _rope_args(rope: Optional[RopeTable]):
     return rope.buffer.data_ptr(), rope.max_position
 
 
-def scd_encode(model: Model, batch: Batch, rope: Optional[RopeTable], k_in, v_in, h_in,
-               w_enc_k, w_enc_v, w_enc_h, mu_k, mu_v, z_k, z_v, z_h, stream=None) -> None:
+class Prepared:
+    """An entry-point call with its arguments marshalled once; calling it launches the kernels on
+    the given (or current) stream.  The referenced tensors must stay alive and unchanged in shape."""
+
+    def __init__(self, fn, args, keep):
+        self._fn, self._args, self._keep = fn, args, keep
+
+    def __call__(self, stream=None) -> None:
+        _check(self._fn(*self._args, _stream(stream)))
+
+
+def prepare_encode(model: Model, batch: Batch, rope: Optional[RopeTable], k_in, v_in, h_in,
+                   w_enc_k, w_enc_v, w_enc_h, mu_k, mu_v, z_k, z_v, z_h) -> Prepared:
     lib = load_library()
     L, T, D, w, g, d = (model.n_layers, batch.n_tokens, model.kv_width, model.basis_width,
                         model.g, model.d_model)
@@ -315,12 +327,18 @@ def scd_encode(model: Model, batch: Batch, rope: Optional[RopeTable], k_in, v_in
         _ptr_array(z_h, L, "z_h", {l: (T, model.rank_h[l]) for l in P}, dt),
     ]
     tab, maxp = _rope_args(rope)
-    _check(lib.scd_encode(ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
-                          *[_as_pp(a) for a in args], _stream(stream)))
+    return Prepared(lib.scd_encode, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
+                                     *[_as_pp(a) for a in args]), (model, batch, rope, args))
 
 
-def scd_reuse_decode(model: Model, batch: Batch, rope: Optional[RopeTable], z_k, z_v,
-                     w_dec_k, w_dec_v, mu_k, mu_v, k_cache, v_cache, stream=None) -> None:
+def scd_encode(model: Model, batch: Batch, rope: Optional[RopeTable], k_in, v_in, h_in,
+               w_enc_k, w_enc_v, w_enc_h, mu_k, mu_v, z_k, z_v, z_h, stream=None) -> None:
+    prepare_encode(model, batch, rope, k_in, v_in, h_in, w_enc_k, w_enc_v, w_enc_h, mu_k, mu_v,
+                   z_k, z_v, z_h)(stream)
+
+
+def prepare_reuse_decode(model: Model, batch: Batch, rope: Optional[RopeTable], z_k, z_v,
+                         w_dec_k, w_dec_v, mu_k, mu_v, k_cache, v_cache) -> Prepared:
     lib = load_library()
     L, T, D, w, g = model.n_layers, batch.n_tokens, model.kv_width, model.basis_width, model.g
     dt = model.torch_dtype
@@ -336,12 +354,19 @@ def scd_reuse_decode(model: Model, batch: Batch, rope: Optional[RopeTable], z_k,
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in R}, dt),
     ]
     tab, maxp = _rope_args(rope)
-    _check(lib.scd_reuse_decode(ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
-                                *[_as_pp(a) for a in args], _stream(stream)))
+    return Prepared(lib.scd_reuse_decode, (ctypes.byref(model._c), ctypes.byref(batch._c), tab,
+                                           maxp, *[_as_pp(a) for a in args]),
+                    (model, batch, rope, args))
 
 
-def scd_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_hat, w_k, w_v,
-                 b_k, b_v, k_cache, v_cache, stream=None) -> None:
+def scd_reuse_decode(model: Model, batch: Batch, rope: Optional[RopeTable], z_k, z_v,
+                     w_dec_k, w_dec_v, mu_k, mu_v, k_cache, v_cache, stream=None) -> None:
+    prepare_reuse_decode(model, batch, rope, z_k, z_v, w_dec_k, w_dec_v, mu_k, mu_v, k_cache,
+                         v_cache)(stream)
+
+
+def prepare_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_hat, w_k, w_v,
+                     b_k, b_v, k_cache, v_cache) -> Prepared:
     lib = load_library()
     L, T, D, d = model.n_layers, batch.n_tokens, model.kv_width, model.d_model
     dt = model.torch_dtype
@@ -356,5 +381,10 @@ def scd_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_hat, w
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in P}, dt),
     ]
     tab, maxp = _rope_args(rope)
-    _check(lib.scd_patch_kv(ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
-                            *[_as_pp(a) for a in args], _stream(stream)))
+    return Prepared(lib.scd_patch_kv, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
+                                       *[_as_pp(a) for a in args]), (model, batch, rope, args))
+
+
+def scd_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_hat, w_k, w_v,
+                 b_k, b_v, k_cache, v_cache, stream=None) -> None:
+    prepare_patch_kv(model, batch, rope, h_hat, w_k, w_v, b_k, b_v, k_cache, v_cache)(stream)

@@ -157,10 +157,10 @@ scd::GemmParams base_params(const scd_model_t* m, const scd_batch_t* b, int64_t 
   return p;
 }
 
-scd_status_t run(const std::vector<scd::GemmParams>& launches, int dtype, hipStream_t stream) {
+scd_status_t run(scd::Op op, const std::vector<scd::GemmParams>& launches, int dtype,
+                 hipStream_t stream) {
   for (const auto& p : launches) {
-    const hipError_t e = dtype == SCD_BF16 ? scd::launch_gemm_bf16(p, stream)
-                                           : scd::launch_gemm_f32(p, stream);
+    const hipError_t e = scd::launch_gemm(op, dtype == SCD_BF16, p, stream);
     if (e != hipSuccess) return fail(SCD_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   }
   return ok();
@@ -306,16 +306,16 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
                scd::kGenericBN);
   for (int l = 0; l < model->n_layers; ++l) {
     if (model->is_patch[l]) {
-      hh.add({h_in[l], w_enc_h[l], z_h[l], nullptr, nullptr, model->rank_h[l], model->d_model, 0, 0});
+      hh.add({h_in[l], w_enc_h[l], z_h[l], nullptr, model->rank_h[l], model->d_model, 0, 0});
     } else {
       const void* mk = mu_k ? mu_k[l] : nullptr;
       const void* mv = mu_v ? mu_v[l] : nullptr;
-      kv.add({k_in[l], w_enc_k[l], z_k[l], nullptr, mk, model->rank_k[l], w, scd::kDeropeIn, 0});
-      kv.add({v_in[l], w_enc_v[l], z_v[l], nullptr, mv, model->rank_v[l], w, 0, 0});
+      kv.add({k_in[l], w_enc_k[l], z_k[l], mk, model->rank_k[l], w, scd::kDeropeIn | scd::kVecIn, 0});
+      kv.add({v_in[l], w_enc_v[l], z_v[l], mv, model->rank_v[l], w, scd::kVecIn, 0});
     }
   }
-  SCD_TRY(run(kv.build(), model->dtype, stream));
-  return run(hh.build(), model->dtype, stream);
+  SCD_TRY(run(scd::Op::kEncodeKV, kv.build(), model->dtype, stream));
+  return run(scd::Op::kEncodeH, hh.build(), model->dtype, stream);
 }
 
 scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
@@ -355,10 +355,10 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
     if (model->is_patch[l]) continue;
     const void* mk = mu_k ? mu_k[l] : nullptr;
     const void* mv = mu_v ? mu_v[l] : nullptr;
-    jp.add({z_k[l], w_dec_k[l], k_cache[l], mk, nullptr, w, model->rank_k[l], scd::kRopeOut, 0});
-    jp.add({z_v[l], w_dec_v[l], v_cache[l], mv, nullptr, w, model->rank_v[l], 0, 0});
+    jp.add({z_k[l], w_dec_k[l], k_cache[l], mk, w, model->rank_k[l], scd::kRopeOut | scd::kVecOut, 0});
+    jp.add({z_v[l], w_dec_v[l], v_cache[l], mv, w, model->rank_v[l], scd::kVecOut, 0});
   }
-  return run(jp.build(), model->dtype, stream);
+  return run(scd::Op::kReuseDecode, jp.build(), model->dtype, stream);
 }
 
 scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
@@ -393,10 +393,10 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
     if (!model->is_patch[l]) continue;
     const void* bk = b_k ? b_k[l] : nullptr;
     const void* bv = b_v ? b_v[l] : nullptr;
-    jp.add({h_hat[l], w_k[l], k_cache[l], bk, nullptr, D, model->d_model, scd::kRopeOut, 0});
-    jp.add({h_hat[l], w_v[l], v_cache[l], bv, nullptr, D, model->d_model, 0, 0});
+    jp.add({h_hat[l], w_k[l], k_cache[l], bk, D, model->d_model, scd::kRopeOut | scd::kVecOut, 0});
+    jp.add({h_hat[l], w_v[l], v_cache[l], bv, D, model->d_model, scd::kVecOut, 0});
   }
-  return run(jp.build(), model->dtype, stream);
+  return run(scd::Op::kPatchKV, jp.build(), model->dtype, stream);
 }
 
 }  // extern "C"

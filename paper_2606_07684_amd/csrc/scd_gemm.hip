@@ -106,7 +106,13 @@ template <> struct Elem<false> {
   }
 };
 
-template <bool BF16, int BM, int BN, int WM, int WN>
+// Tag types that name each step's kernel.
+struct ReuseDecode {};
+struct PatchKV {};
+struct EncodeKV {};
+struct EncodeH {};
+
+template <typename OP, bool BF16, int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
   using EL = Elem<BF16>;
   using T = typename EL::T;
@@ -144,6 +150,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
   const int n0 = (local % ntn) * BN;
   const bool derope = (job.flags & kDeropeIn) != 0;
   const bool rope_out = (job.flags & kRopeOut) != 0;
+  const bool vec_in = (job.flags & kVecIn) != 0 && job.vec != nullptr;
+  const bool vec_out = (job.flags & kVecOut) != 0 && job.vec != nullptr;
   const int dh = p.head_dim, half = dh / 2;
   const int K = job.k, N = job.n;
   const int64_t M = p.m;
@@ -210,7 +218,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
       const int task = tid + t * NT, row = task >> 1, q = task & 1;
       uint4* d0 = reinterpret_cast<uint4*>(As + (buf * BM + row) * LDK + 8 * q);
       uint4* d1 = reinterpret_cast<uint4*>(As + (buf * BM + row) * LDK + 16 + 8 * q);
-      if (derope || job.mu_in != nullptr) {
+      if (derope || vec_in) {
         float u[8], v[8];
         EL::unpack(ra[t][0], u);
         EL::unpack(ra[t][1], v);
@@ -225,12 +233,12 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
             v[e] = vv * c.x - uu * c.y;
           }
         }
-        if (job.mu_in != nullptr) {
+        if (vec_in) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int c0 = b0 + 8 * q + e, c1 = b1 + 8 * q + e;
-            if (c0 < K) u[e] -= EL::load1(job.mu_in, c0);
-            if (c1 < K) v[e] -= EL::load1(job.mu_in, c1);
+            if (c0 < K) u[e] -= EL::load1(job.vec, c0);
+            if (c1 < K) v[e] -= EL::load1(job.vec, c1);
           }
         }
         uint4 o0[NV], o1[NV];
@@ -342,11 +350,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
       float u[8], v[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) { u[e] = Cs[row * LDC + c0 + e]; v[e] = Cs[row * LDC + c1 + e]; }
-      if (job.bias != nullptr) {
+      if (vec_out) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          u[e] += EL::load1(job.bias, gc0 + e);
-          v[e] += EL::load1(job.bias, gc1 + e);
+          u[e] += EL::load1(job.vec, gc0 + e);
+          v[e] += EL::load1(job.vec, gc1 + e);
         }
       }
       const float2* cs = p.rope + table_row(p, s_pos[row]) * half + o;
@@ -375,9 +383,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
       float u[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) u[e] = Cs[row * LDC + c0 + e];
-      if (job.bias != nullptr) {
+      if (vec_out) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) u[e] += EL::load1(job.bias, gc0 + e);
+        for (int e = 0; e < 8; ++e) u[e] += EL::load1(job.vec, gc0 + e);
       }
       uint4 o0[NV];
       EL::pack(u, o0);
@@ -421,18 +429,27 @@ __global__ void positions_kernel(int32_t* out, int64_t n_tokens, int32_t n_seqs,
 
 }  // namespace
 
-hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t stream) {
-  if (p.total_tiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_nt_kernel<true, kGenericBM, kGenericBN, 2, 2>), dim3(p.total_tiles),
-                     dim3(256), 0, stream, p);
+template <typename OP, bool BF16>
+hipError_t launch_one(const GemmParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL((gemm_nt_kernel<OP, BF16, kGenericBM, kGenericBN, 2, 2>),
+                     dim3(p.total_tiles), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_f32(const GemmParams& p, hipStream_t stream) {
+template <typename OP>
+hipError_t launch_op(bool bf16, const GemmParams& p, hipStream_t stream) {
+  return bf16 ? launch_one<OP, true>(p, stream) : launch_one<OP, false>(p, stream);
+}
+
+hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream) {
   if (p.total_tiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_nt_kernel<false, kGenericBM, kGenericBN, 2, 2>), dim3(p.total_tiles),
-                     dim3(256), 0, stream, p);
-  return hipGetLastError();
+  switch (op) {
+    case Op::kReuseDecode: return launch_op<ReuseDecode>(bf16, p, stream);
+    case Op::kPatchKV: return launch_op<PatchKV>(bf16, p, stream);
+    case Op::kEncodeKV: return launch_op<EncodeKV>(bf16, p, stream);
+    case Op::kEncodeH: return launch_op<EncodeH>(bf16, p, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,

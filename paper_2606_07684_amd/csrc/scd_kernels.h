@@ -7,11 +7,14 @@
 namespace scd {
 
 // Most jobs one launch carries in its kernel arguments (jobs beyond it go to further launches).
-constexpr int kMaxJobs = 32;
+// 64 jobs keep the argument block near 3 KiB.
+constexpr int kMaxJobs = 64;
 
 enum JobFlags : int32_t {
   kRopeOut = 1,   // rotate output column pairs (i, i + d_h/2) of every head by the row's position
   kDeropeIn = 2,  // inverse-rotate input column pairs of A before the contraction
+  kVecOut = 4,    // vec[n] is added to every output row before RoPE (decoder offset, bias)
+  kVecIn = 8,     // vec[k] is subtracted from every row of A after deRoPE (encoder offset)
 };
 
 // One dense product C[M, n] = prologue(A)[M, k] * B[n, k]^T (+ bias[n]) followed by the epilogue
@@ -20,13 +23,13 @@ struct GemmJob {
   const void* a;
   const void* b;
   void* c;
-  const void* bias;   // [n] added before RoPE, or null
-  const void* mu_in;  // [k] subtracted from A after deRoPE, or null
+  const void* vec;    // [n] (kVecOut) or [k] (kVecIn); null when neither flag is set
   int32_t n;
   int32_t k;
   int32_t flags;
   int32_t tile_begin;  // first tile index of this job within the launch
 };
+static_assert(sizeof(GemmJob) == 48, "job descriptor size");
 
 struct GemmParams {
   GemmJob jobs[kMaxJobs];
@@ -42,14 +45,18 @@ struct GemmParams {
   const float2* rope;         // [max_pos][head_dim / 2] (cos, sin)
   int64_t max_pos;
 };
+static_assert(sizeof(GemmParams) <= 4096, "kernel argument block");
 
 // Tile shape of the generic launcher (rows x columns of C per workgroup).
 constexpr int kGenericBM = 128;
 constexpr int kGenericBN = 128;
 
+// The codec step a launch performs; each step is its own kernel symbol so profiles attribute time
+// per step.
+enum class Op : int { kReuseDecode = 0, kPatchKV = 1, kEncodeKV = 2, kEncodeH = 3 };
+
 // Launchers (return the hipError_t of the launch).
-hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t stream);
-hipError_t launch_gemm_f32(const GemmParams& p, hipStream_t stream);
+hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream);
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,
                              hipStream_t stream);
 hipError_t launch_positions(int32_t* out, int64_t n_tokens, int32_t n_seqs,

@@ -244,3 +244,67 @@ def pos0(wl: Workload, device="cpu") -> Optional[torch.Tensor]:
 
 def layer_set(wl: Workload, layers: Optional[Sequence[int]] = None):
     return list(range(wl.n_layers)) if layers is None else list(layers)
+
+
+# --------------------------------------------------------------------------------------------
+# Whole input sets and output buffers
+# --------------------------------------------------------------------------------------------
+class Inputs:
+    """All per-layer inputs of a workload on one device (None where a layer has no such tensor)."""
+
+    def __init__(self, wl: Workload, device, encode=True, decode=True, patch=True):
+        L = wl.n_layers
+        R = [l for l in range(L) if not wl.is_patch[l]]
+        P = [l for l in range(L) if wl.is_patch[l]]
+        none = lambda: [None] * L  # noqa: E731
+        self.wl = wl
+        self.R, self.P = R, P
+        self.w_enc_k, self.w_dec_k, self.w_enc_v, self.w_dec_v = none(), none(), none(), none()
+        self.mu_k, self.mu_v = none(), none()
+        self.z_k, self.z_v, self.k_in, self.v_in = none(), none(), none(), none()
+        self.h_in, self.w_enc_h, self.h_hat = none(), none(), none()
+        self.w_k, self.w_v, self.b_k, self.b_v = none(), none(), none(), none()
+        for l in R:
+            self.w_enc_k[l], self.w_dec_k[l] = basis(wl, l, "k", device)
+            self.w_enc_v[l], self.w_dec_v[l] = basis(wl, l, "v", device)
+            self.mu_k[l] = mu(wl, l, "k", device)
+            self.mu_v[l] = mu(wl, l, "v", device)
+            if decode:
+                self.z_k[l] = codes(wl, l, "k", device)
+                self.z_v[l] = codes(wl, l, "v", device)
+            if encode:
+                self.k_in[l] = kv_input(wl, l, "k", device)
+                self.v_in[l] = kv_input(wl, l, "v", device)
+        for l in P:
+            if encode:
+                self.h_in[l] = hidden(wl, l, "h_in", device)
+                self.w_enc_h[l] = enc_h(wl, l, device)
+            if patch:
+                self.h_hat[l] = hidden(wl, l, "h_hat", device)
+                self.w_k[l], self.w_v[l] = proj_weights(wl, l, device)
+                self.b_k[l], self.b_v[l] = proj_bias(wl, l, device)
+
+
+def alloc_caches(wl: Workload, device, fill=None):
+    """Per-layer K and V caches [T, D]; optionally filled with a sentinel bit pattern."""
+    ks, vs = [], []
+    for _ in range(wl.n_layers):
+        for lst in (ks, vs):
+            t = torch.empty((wl.n_tokens, wl.kv_width), dtype=wl.torch_dtype, device=device)
+            if fill is not None:
+                t.fill_(fill)
+            lst.append(t)
+    return ks, vs
+
+
+def alloc_codes(wl: Workload, device):
+    L = wl.n_layers
+    z_k, z_v, z_h = [None] * L, [None] * L, [None] * L
+    for l in range(L):
+        if wl.is_patch[l]:
+            z_h[l] = torch.empty((wl.n_tokens, wl.ranks[l]), dtype=wl.torch_dtype, device=device)
+        else:
+            for lst in (z_k, z_v):
+                lst[l] = torch.empty((wl.n_tokens * wl.g, wl.ranks[l]), dtype=wl.torch_dtype,
+                                     device=device)
+    return z_k, z_v, z_h

@@ -12,6 +12,11 @@ from synth import workloads as W
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
+Inputs = W.Inputs
+alloc_caches = W.alloc_caches
+alloc_codes = W.alloc_codes
+
+
 def model_of(wl: W.Workload) -> scd.Model:
     return scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
                      head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
@@ -41,67 +46,6 @@ def max_abs_rel(got, want) -> float:
         return float("inf")
     den = np.max(np.abs(want))
     return float(np.max(np.abs(got - want)) / (den if den > 0 else 1.0))
-
-
-class Inputs:
-    """All per-layer inputs of a workload on one device (None where a layer has no such tensor)."""
-
-    def __init__(self, wl: W.Workload, device, encode=True, decode=True, patch=True):
-        L = wl.n_layers
-        R = [l for l in range(L) if not wl.is_patch[l]]
-        P = [l for l in range(L) if wl.is_patch[l]]
-        none = lambda: [None] * L  # noqa: E731
-        self.wl = wl
-        self.R, self.P = R, P
-        self.w_enc_k, self.w_dec_k, self.w_enc_v, self.w_dec_v = none(), none(), none(), none()
-        self.mu_k, self.mu_v = none(), none()
-        self.z_k, self.z_v, self.k_in, self.v_in = none(), none(), none(), none()
-        self.h_in, self.w_enc_h, self.h_hat = none(), none(), none()
-        self.w_k, self.w_v, self.b_k, self.b_v = none(), none(), none(), none()
-        for l in R:
-            self.w_enc_k[l], self.w_dec_k[l] = W.basis(wl, l, "k", device)
-            self.w_enc_v[l], self.w_dec_v[l] = W.basis(wl, l, "v", device)
-            self.mu_k[l] = W.mu(wl, l, "k", device)
-            self.mu_v[l] = W.mu(wl, l, "v", device)
-            if decode:
-                self.z_k[l] = W.codes(wl, l, "k", device)
-                self.z_v[l] = W.codes(wl, l, "v", device)
-            if encode:
-                self.k_in[l] = W.kv_input(wl, l, "k", device)
-                self.v_in[l] = W.kv_input(wl, l, "v", device)
-        for l in P:
-            if encode:
-                self.h_in[l] = W.hidden(wl, l, "h_in", device)
-                self.w_enc_h[l] = W.enc_h(wl, l, device)
-            if patch:
-                self.h_hat[l] = W.hidden(wl, l, "h_hat", device)
-                self.w_k[l], self.w_v[l] = W.proj_weights(wl, l, device)
-                self.b_k[l], self.b_v[l] = W.proj_bias(wl, l, device)
-
-
-def alloc_caches(wl: W.Workload, device, fill=None):
-    """Per-layer K and V caches [T, D]; optionally filled with a sentinel bit pattern."""
-    ks, vs = [], []
-    for _ in range(wl.n_layers):
-        for lst in (ks, vs):
-            t = torch.empty((wl.n_tokens, wl.kv_width), dtype=wl.torch_dtype, device=device)
-            if fill is not None:
-                t.fill_(fill)
-            lst.append(t)
-    return ks, vs
-
-
-def alloc_codes(wl: W.Workload, device):
-    L = wl.n_layers
-    z_k, z_v, z_h = [None] * L, [None] * L, [None] * L
-    for l in range(L):
-        if wl.is_patch[l]:
-            z_h[l] = torch.empty((wl.n_tokens, wl.ranks[l]), dtype=wl.torch_dtype, device=device)
-        else:
-            for lst in (z_k, z_v):
-                lst[l] = torch.empty((wl.n_tokens * wl.g, wl.ranks[l]), dtype=wl.torch_dtype,
-                                     device=device)
-    return z_k, z_v, z_h
 
 
 def run_gpu(wl: W.Workload, inp: Inputs, rope, which=("decode", "patch", "encode"), fill=None):
