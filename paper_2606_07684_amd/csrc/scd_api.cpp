@@ -387,8 +387,10 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
 
   const int64_t T = batch->n_tokens;
   const int D = static_cast<int>(kv_width(model));
-  JobPacker jp(base_params(model, batch, T, 1, rope_table, max_position), scd::kGenericBM,
-               scd::kGenericBN);
+  const bool fast = model->dtype == SCD_BF16 && model->d_model % 64 == 0 &&
+                    (model->head_dim == 64 || model->head_dim == 128) && D % 128 == 0;
+  JobPacker jp(base_params(model, batch, T, 1, rope_table, max_position),
+               fast ? scd::kPatchBM : scd::kGenericBM, fast ? scd::kPatchBN : scd::kGenericBN);
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
     const void* bk = b_k ? b_k[l] : nullptr;
@@ -396,7 +398,12 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
     jp.add({h_hat[l], w_k[l], k_cache[l], bk, D, model->d_model, scd::kRopeOut | scd::kVecOut, 0});
     jp.add({h_hat[l], w_v[l], v_cache[l], bv, D, model->d_model, scd::kVecOut, 0});
   }
-  return run(scd::Op::kPatchKV, jp.build(), model->dtype, stream);
+  if (!fast) return run(scd::Op::kPatchKV, jp.build(), model->dtype, stream);
+  for (const auto& p : jp.build()) {
+    const hipError_t e = scd::launch_patch_bf16(p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "patch launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
 }
 
 }  // extern "C"

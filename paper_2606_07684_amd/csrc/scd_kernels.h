@@ -57,6 +57,12 @@ enum class Op : int { kReuseDecode = 0, kPatchKV = 1, kEncodeKV = 2, kEncodeH = 
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream);
+
+// Patch on the bf16 path: 256 x 256 tiles (tokens x channels), d_model % 64 == 0, head_dim 64 or
+// 128, D % 128 == 0.
+constexpr int kPatchBM = 256;
+constexpr int kPatchBN = 256;
+hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,
                              hipStream_t stream);
 hipError_t launch_positions(int32_t* out, int64_t n_tokens, int32_t n_seqs,
