@@ -166,6 +166,40 @@ scd_status_t run(scd::Op op, const std::vector<scd::GemmParams>& launches, int d
   return ok();
 }
 
+// Splits jobs into launches that each hold one rank (jobs of equal key), in first-seen order.
+template <typename KeyFn>
+std::vector<std::vector<scd::GemmJob>> group_by(const std::vector<scd::GemmJob>& jobs, KeyFn key) {
+  std::vector<std::vector<scd::GemmJob>> groups;
+  std::vector<int> keys;
+  for (const auto& j : jobs) {
+    const int k = key(j);
+    size_t g = 0;
+    while (g < keys.size() && keys[g] != k) ++g;
+    if (g == keys.size()) {
+      keys.push_back(k);
+      groups.emplace_back();
+    }
+    groups[g].push_back(j);
+  }
+  return groups;
+}
+
+template <typename LaunchFn>
+scd_status_t run_groups(const scd::GemmParams& base, int bm, int bn,
+                        const std::vector<std::vector<scd::GemmJob>>& groups, LaunchFn launch,
+                        const char* what) {
+  for (const auto& g : groups) {
+    JobPacker jp(base, bm, bn);
+    for (const auto& j : g) jp.add(j);
+    for (const auto& p : jp.build()) {
+      const hipError_t e = launch(p);
+      if (e != hipSuccess)
+        return fail(SCD_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
+    }
+  }
+  return ok();
+}
+
 int64_t kv_width(const scd_model_t* m) {
   return static_cast<int64_t>(m->n_kv_heads) * m->head_dim;
 }
@@ -300,22 +334,38 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
   if (batch->n_tokens == 0) return ok();
 
   const int64_t T = batch->n_tokens;
-  JobPacker kv(base_params(model, batch, T * g, g, rope_table, max_position), scd::kGenericBM,
-               scd::kGenericBN);
-  JobPacker hh(base_params(model, batch, T, 1, rope_table, max_position), scd::kGenericBM,
-               scd::kGenericBN);
+  const bool bf16 = model->dtype == SCD_BF16;
+  const bool hd_ok = model->head_dim == 64 || model->head_dim == 128;
+  const bool fast_kv = bf16 && hd_ok && w % 128 == 0;
+  const bool fast_h = bf16 && model->d_model % 128 == 0;
+  std::vector<scd::GemmJob> kv_jobs, h_jobs;
   for (int l = 0; l < model->n_layers; ++l) {
     if (model->is_patch[l]) {
-      hh.add({h_in[l], w_enc_h[l], z_h[l], nullptr, model->rank_h[l], model->d_model, 0, 0});
+      h_jobs.push_back({h_in[l], w_enc_h[l], z_h[l], nullptr, model->rank_h[l], model->d_model, 0, 0});
     } else {
       const void* mk = mu_k ? mu_k[l] : nullptr;
       const void* mv = mu_v ? mu_v[l] : nullptr;
-      kv.add({k_in[l], w_enc_k[l], z_k[l], mk, model->rank_k[l], w, scd::kDeropeIn | scd::kVecIn, 0});
-      kv.add({v_in[l], w_enc_v[l], z_v[l], mv, model->rank_v[l], w, scd::kVecIn, 0});
+      kv_jobs.push_back({k_in[l], w_enc_k[l], z_k[l], mk, model->rank_k[l], w,
+                         scd::kDeropeIn | scd::kVecIn, 0});
+      kv_jobs.push_back({v_in[l], w_enc_v[l], z_v[l], mv, model->rank_v[l], w, scd::kVecIn, 0});
     }
   }
-  SCD_TRY(run(scd::Op::kEncodeKV, kv.build(), model->dtype, stream));
-  return run(scd::Op::kEncodeH, hh.build(), model->dtype, stream);
+  const scd::GemmParams kv_base = base_params(model, batch, T * g, g, rope_table, max_position);
+  const scd::GemmParams h_base = base_params(model, batch, T, 1, rope_table, max_position);
+  auto by_rank = [](const scd::GemmJob& j) { return j.n; };
+  auto enc = [&](const scd::GemmParams& p) { return scd::launch_encode_bf16(p, stream); };
+  if (fast_kv) {
+    SCD_TRY(run_groups(kv_base, scd::kEncodeRows, 256, group_by(kv_jobs, by_rank), enc, "encode"));
+  } else {
+    JobPacker jp(kv_base, scd::kGenericBM, scd::kGenericBN);
+    for (const auto& j : kv_jobs) jp.add(j);
+    SCD_TRY(run(scd::Op::kEncodeKV, jp.build(), model->dtype, stream));
+  }
+  if (fast_h)
+    return run_groups(h_base, scd::kEncodeRows, 256, group_by(h_jobs, by_rank), enc, "encode");
+  JobPacker hp(h_base, scd::kGenericBM, scd::kGenericBN);
+  for (const auto& j : h_jobs) hp.add(j);
+  return run(scd::Op::kEncodeH, hp.build(), model->dtype, stream);
 }
 
 scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
@@ -349,16 +399,29 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
   if (!any || batch->n_tokens == 0) return ok();
 
   const int64_t T = batch->n_tokens;
-  JobPacker jp(base_params(model, batch, T * g, g, rope_table, max_position), scd::kGenericBM,
-               scd::kGenericBN);
+  bool fast = model->dtype == SCD_BF16 && (model->head_dim == 64 || model->head_dim == 128) &&
+              w % 128 == 0;
+  std::vector<scd::GemmJob> jobs;
   for (int l = 0; l < model->n_layers; ++l) {
     if (model->is_patch[l]) continue;
     const void* mk = mu_k ? mu_k[l] : nullptr;
     const void* mv = mu_v ? mu_v[l] : nullptr;
-    jp.add({z_k[l], w_dec_k[l], k_cache[l], mk, w, model->rank_k[l], scd::kRopeOut | scd::kVecOut, 0});
-    jp.add({z_v[l], w_dec_v[l], v_cache[l], mv, w, model->rank_v[l], scd::kVecOut, 0});
+    jobs.push_back({z_k[l], w_dec_k[l], k_cache[l], mk, w, model->rank_k[l],
+                    scd::kRopeOut | scd::kVecOut, 0});
+    jobs.push_back({z_v[l], w_dec_v[l], v_cache[l], mv, w, model->rank_v[l], scd::kVecOut, 0});
+    if (model->rank_k[l] % 32 != 0 || model->rank_v[l] % 32 != 0) fast = false;
   }
-  return run(scd::Op::kReuseDecode, jp.build(), model->dtype, stream);
+  const scd::GemmParams base = base_params(model, batch, T * g, g, rope_table, max_position);
+  if (!fast) {
+    JobPacker jp(base, scd::kGenericBM, scd::kGenericBN);
+    for (const auto& j : jobs) jp.add(j);
+    return run(scd::Op::kReuseDecode, jp.build(), model->dtype, stream);
+  }
+  const int nwc = w % 256 == 0 ? 2 : 1;
+  const int rows_per_unit = scd::kTilesPerGroup * 32 * (4 / nwc);
+  auto dec = [&](const scd::GemmParams& p) { return scd::launch_decode_bf16(nwc, p, stream); };
+  return run_groups(base, rows_per_unit, 128 * nwc,
+                    group_by(jobs, [](const scd::GemmJob& j) { return j.k; }), dec, "decode");
 }
 
 scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,

@@ -190,9 +190,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
       for (int pc = 0; pc < 2; ++pc) {
         const int col = (pc ? b1 : b0) + 8 * q;
         const bool ok = gr < M && col < K;
-        const uint4* src = reinterpret_cast<const uint4*>(A + gr * K + col);
+        // out-of-range pieces read an in-bounds address and are replaced by zero
+        const uint4* src = reinterpret_cast<const uint4*>(A + (ok ? gr * K + col : 0));
 #pragma unroll
-        for (int v = 0; v < NV; ++v) ra[t][pc][v] = ok ? src[v] : zero;
+        for (int v = 0; v < NV; ++v) {
+          const uint4 x = src[v];
+          ra[t][pc][v] = ok ? x : zero;
+        }
       }
     }
 #pragma unroll
@@ -203,9 +207,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
       for (int pc = 0; pc < 2; ++pc) {
         const int col = (pc ? b1 : b0) + 8 * q;
         const bool ok = gn < N && col < K;
-        const uint4* src = reinterpret_cast<const uint4*>(B + static_cast<int64_t>(gn) * K + col);
+        const uint4* src =
+            reinterpret_cast<const uint4*>(B + (ok ? static_cast<int64_t>(gn) * K + col : 0));
 #pragma unroll
-        for (int v = 0; v < NV; ++v) rb[t][pc][v] = ok ? src[v] : zero;
+        for (int v = 0; v < NV; ++v) {
+          const uint4 x = src[v];
+          rb[t][pc][v] = ok ? x : zero;
+        }
       }
     }
   };

@@ -63,6 +63,17 @@ hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream
 constexpr int kPatchBM = 256;
 constexpr int kPatchBN = 256;
 hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
+
+// Reuse decode on the bf16 path: a unit is (channel chunk of 128 * nwc, group of kTilesPerGroup
+// token tiles of 32 * 4 / nwc rows); basis_width % (128 * nwc) == 0, ranks % 32 == 0 and <= 256,
+// head_dim 64 or 128.
+constexpr int kTilesPerGroup = 8;
+hipError_t launch_decode_bf16(int nwc, const GemmParams& p, hipStream_t stream);
+
+// Encode on the bf16 path: a unit is 128 rows x all code columns; k % 128 == 0, n <= 256,
+// head_dim 64 or 128 when a job de-rotates.
+constexpr int kEncodeRows = 128;
+hipError_t launch_encode_bf16(const GemmParams& p, hipStream_t stream);
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,
                              hipStream_t stream);
 hipError_t launch_positions(int32_t* out, int64_t n_tokens, int32_t n_seqs,
