@@ -226,9 +226,14 @@ const char* scd_status_string(scd_status_t s) {
 
 const char* scd_last_error(void) { return g_last_error.c_str(); }
 
+// Rows a RoPE table for max_position holds (never fewer than kRopeMinRows).
+static int64_t rope_rows(int64_t max_position) {
+  return max_position > scd::kRopeMinRows ? max_position : scd::kRopeMinRows;
+}
+
 size_t scd_rope_table_bytes(const scd_model_t* model, int64_t max_position) {
   if (model == nullptr || model->head_dim <= 0 || max_position < 1) return 0;
-  return static_cast<size_t>(max_position) * static_cast<size_t>(model->head_dim / 2) *
+  return static_cast<size_t>(rope_rows(max_position)) * static_cast<size_t>(model->head_dim / 2) *
          sizeof(float2);
 }
 
@@ -241,7 +246,7 @@ scd_status_t scd_rope_table(const scd_model_t* model, int64_t max_position, void
                 scd_rope_table_bytes(model, max_position));
   if (max_position > (int64_t{1} << 31))
     return fail(SCD_ERR_UNSUPPORTED, "max_position above 2^31");
-  const hipError_t e = scd::launch_rope_table(static_cast<float2*>(table), max_position,
+  const hipError_t e = scd::launch_rope_table(static_cast<float2*>(table), rope_rows(max_position),
                                               model->head_dim, model->rope_theta, stream);
   if (e != hipSuccess) return fail(SCD_ERR_HIP, "rope table launch failed: %s", hipGetErrorString(e));
   return ok();
@@ -400,7 +405,7 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
 
   const int64_t T = batch->n_tokens;
   bool fast = model->dtype == SCD_BF16 && (model->head_dim == 64 || model->head_dim == 128) &&
-              w % 128 == 0;
+              w % 128 == 0 && batch->n_seqs <= scd::kMaxLdsSeqs;
   std::vector<scd::GemmJob> jobs;
   for (int l = 0; l < model->n_layers; ++l) {
     if (model->is_patch[l]) continue;
@@ -417,11 +422,22 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
     for (const auto& j : jobs) jp.add(j);
     return run(scd::Op::kReuseDecode, jp.build(), model->dtype, stream);
   }
-  const int nwc = w % 256 == 0 ? 2 : 1;
-  const int rows_per_unit = scd::kTilesPerGroup * 32 * (4 / nwc);
-  auto dec = [&](const scd::GemmParams& p) { return scd::launch_decode_bf16(nwc, p, stream); };
-  return run_groups(base, rows_per_unit, 128 * nwc,
-                    group_by(jobs, [](const scd::GemmJob& j) { return j.k; }), dec, "decode");
+  // one launch per (rank, branch): key and value jobs run different kernel instances
+  for (const auto& grp : group_by(jobs, [](const scd::GemmJob& j) {
+         return j.k * 2 + ((j.flags & scd::kRopeOut) != 0 ? 1 : 0);
+       })) {
+    const int nhg = scd::decode_channel_groups(grp[0].k, w);
+    scd::GemmParams gp = base;
+    gp.tiles_per_unit = T * g >= 4 * scd::kDecodeTileRows ? 2 : 1;
+    JobPacker jp(gp, gp.tiles_per_unit * scd::kDecodeTileRows, 128 * nhg);
+    for (const auto& j : grp) jp.add(j);
+    for (const auto& lp : jp.build()) {
+      const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream);
+      if (e != hipSuccess)
+        return fail(SCD_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+    }
+  }
+  return ok();
 }
 
 scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,

@@ -12,65 +12,16 @@
 // ends with 16 consecutive code columns of one row) is double-buffered in LDS and shared by the
 // four waves.  Both operands visit the columns of a chunk in the same order, so the contraction
 // is unchanged.
-#include "scd_kernels.h"
+#include "scd_device.h"
 
 namespace scd {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+using namespace dev;
 
-constexpr int kNumXcd = 8;
 constexpr int kThreads = 256;
 constexpr int kChunk = 128;          // input columns per chunk
 constexpr int kLdc = kChunk + 8;     // padded LDS row of a weight chunk (elements)
-
-__device__ inline int xcd_remap(int bid, int nb) {
-  const int q = nb / kNumXcd, rem = nb % kNumXcd;
-  const int x = bid % kNumXcd, i = bid / kNumXcd;
-  return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + i;
-}
-
-__device__ inline int row_position(const GemmParams& p, int64_t row) {
-  const int64_t t = row / p.g;
-  int b = 0;
-  int64_t local = t;
-  if (p.cu_seqlens != nullptr) {
-    int lo = 0, hi = p.n_seqs - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (p.cu_seqlens[mid] <= t) lo = mid; else hi = mid - 1;
-    }
-    b = lo;
-    local = t - p.cu_seqlens[b];
-  }
-  int64_t pos = local + (p.pos0 != nullptr ? p.pos0[b] : 0);
-  pos = pos < 0 ? 0 : (pos >= p.max_pos ? p.max_pos - 1 : pos);
-  return static_cast<int>(pos);
-}
-
-__device__ inline int lds_row_of_code(int n) {
-  const int o = n & 31;
-  return (n & ~31) | (8 * ((o >> 2) & 3) + 4 * (o >> 4) + (o & 3));
-}
-
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ inline uint32_t pack_bf16x2(float a, float b) {
-  const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
-  const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<__bf16>(b));
-  return lo | (hi << 16);
-}
-__device__ inline void unpack8(const uint4& v, float* f) {
-  f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
-  f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
-}
-__device__ inline uint4 pack8(const float* f) {
-  uint4 v;
-  v.x = pack_bf16x2(f[0], f[1]); v.y = pack_bf16x2(f[2], f[3]);
-  v.z = pack_bf16x2(f[4], f[5]); v.w = pack_bf16x2(f[6], f[7]);
-  return v;
-}
 
 // Column (within a chunk) that lane half h supplies to MFMA k-step s (0..7).  With deRoPE, even
 // steps take the first half of a head and odd steps the matching second half:
@@ -96,9 +47,7 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   const int h = lane >> 5;
 
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
-  int j = 0;
-  while (j + 1 < p.n_jobs && unit >= p.jobs[j + 1].tile_begin) ++j;
-  const GemmJob job = p.jobs[j];
+  const GemmJob job = p.jobs[job_of(p, unit)];
   const int R = job.n, K = job.k;
   const int64_t M = p.m;
   const int64_t row = static_cast<int64_t>(unit - job.tile_begin) * 128 + wave * 32 + (lane & 31);
@@ -116,16 +65,13 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       *reinterpret_cast<uint4*>(mus + 8 * q) = *reinterpret_cast<const uint4*>(mu + 8 * q);
   }
 
-  // weight chunk c -> LDS buffer b (rows beyond R are zero)
+  // weight chunk c -> LDS buffer b, asynchronously; code rows beyond R read row 0 and only feed
+  // accumulator blocks that are never stored
   auto stage_weights = [&](int c, int b) {
-    uint16_t* dst = Es + b * RB * 32 * kLdc;
-    for (int q = tid; q < RB * 32 * (kChunk / 8); q += kThreads) {
-      const int r = q / (kChunk / 8), cc = q % (kChunk / 8);
-      const uint4 v = r < R ? *reinterpret_cast<const uint4*>(E + static_cast<int64_t>(r) * K +
-                                                              c * kChunk + 8 * cc)
-                            : make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4*>(dst + lds_row_of_code(r) * kLdc + 8 * cc) = v;
-    }
+    dma_rows(Es + b * RB * 32 * kLdc, RB * 32, kChunk / 8, kLdc / 8, wave, 4, lane, [&](int rho) {
+      const int r = row_of_lds(rho);
+      return E + static_cast<int64_t>(r < R ? r : 0) * K + c * kChunk;
+    });
   };
 
   // this lane's rotation factors for every pair index it touches: i = 16*o + 8*h + e
@@ -160,6 +106,7 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 
   stage_weights(0, 0);
   load_x(0, xc);
+  wait_vmem();
   __syncthreads();
 
   for (int c = 0; c < nchunks; ++c) {
@@ -219,6 +166,7 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
         acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
       }
     }
+    wait_vmem();
     __syncthreads();
 #pragma unroll
     for (int s = 0; s < 8; ++s) xc[s] = xn[s];
