@@ -4,83 +4,54 @@
 // One workgroup computes a 256 (channels n) x 256 (tokens t) tile of C^T = W * H_hat^T with four
 // waves, each owning 128 channels x 128 tokens as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.
 // The weight tile is the MFMA A operand, so an accumulator register holds one token's channels;
-// weight rows are stored into LDS in a permuted order that gives each lane 16 consecutive channels
+// weight rows are placed in LDS in a permuted order that gives each lane 16 consecutive channels
 // of one token.  A wave's 128 channels are whole heads, so every RoPE pair (i, i + d_h/2) meets in
 // one lane and the epilogue needs no LDS: bias, rotation and bf16 rounding happen in registers and
-// each lane stores two 16-byte vectors per block.  K advances 64 at a time through double-buffered
-// LDS (2 x 2 x 256 x 72 bf16 = 144 KiB, rows padded by 16 bytes so MFMA reads are conflict-free);
-// the next stage's global loads are in flight while the current stage is multiplied.
-#include "scd_kernels.h"
+// each lane stores two 16-byte vectors per block.
+//
+// K advances 64 at a time through two LDS stages (2 x (256 + 256) x 72 bf16 = 144 KiB, rows padded
+// by 16 bytes so MFMA operand reads are conflict-free).  Both operand tiles travel global -> LDS
+// directly (global_load_lds_dwordx4), so the copy of stage k+1 needs no registers and runs under
+// the MFMAs of stage k; inside a stage the operand fragments of the next 16-wide k-slice are read
+// from LDS while the MFMAs of the current one issue.
+#include "scd_device.h"
 
 namespace scd {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+using namespace dev;
 
-constexpr int kBM = 256;   // tokens per tile
-constexpr int kBN = 256;   // channels per tile
-constexpr int kBK = 64;    // contraction step
-constexpr int kLDK = kBK + 8;  // padded LDS row (bf16 elements)
+constexpr int kBM = kPatchBM;   // tokens per tile
+constexpr int kBN = kPatchBN;   // channels per tile
+constexpr int kBK = 64;         // contraction step
+constexpr int kLDK = kBK + 8;   // padded LDS row (bf16 elements)
+constexpr int kSlots = kLDK / 8;  // 16-byte slots per LDS row (8 data + 1 pad)
+constexpr int kStage = (kBN + kBM) * kLDK;  // elements per pipeline stage
 constexpr int kThreads = 256;
-constexpr int kNumXcd = 8;
 
-template <int V> struct IntC { static constexpr int value = V; };
-
-__device__ inline int xcd_remap(int bid, int nb) {
-  const int q = nb / kNumXcd, rem = nb % kNumXcd;
-  const int x = bid % kNumXcd, i = bid / kNumXcd;
-  return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + i;
-}
-
-__device__ inline int token_position(const GemmParams& p, int64_t t) {
-  int b = 0;
-  int64_t local = t;
-  if (p.cu_seqlens != nullptr) {
-    int lo = 0, hi = p.n_seqs - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (p.cu_seqlens[mid] <= t) lo = mid; else hi = mid - 1;
-    }
-    b = lo;
-    local = t - p.cu_seqlens[b];
-  }
-  int64_t pos = local + (p.pos0 != nullptr ? p.pos0[b] : 0);
-  pos = pos < 0 ? 0 : (pos >= p.max_pos ? p.max_pos - 1 : pos);
-  return static_cast<int>(pos);
-}
-
-// LDS row that holds weight row `n` of a 32-row block: the MFMA reads rows in natural order and
-// row i of the block must be channel 16*((i>>2)&1) + 4*(i>>3) + (i&3), so that accumulator
-// element r of lane l is channel 16*(l/32) + r.
-__device__ inline int lds_row_of_channel(int n) {
-  const int o = n & 31;
-  return (n & ~31) | (8 * ((o >> 2) & 3) + 4 * (o >> 4) + (o & 3));
-}
-
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ inline uint32_t pack_bf16x2(float a, float b) {
-  const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
-  const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<__bf16>(b));
-  return lo | (hi << 16);
+// Scheduling groups for one block of 16 MFMAs and 8 LDS reads that do not feed them: one read
+// after each of the first eight MFMAs.
+__device__ __forceinline__ void interleave_reads() {
+#define SCD_MFMA_THEN_READ                          \
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
+  __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+#undef SCD_MFMA_THEN_READ
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
 }
 
 __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * 2 * kBM * kLDK];
-  uint16_t* Ws = smem;                    // [2][kBN][kLDK]
-  uint16_t* Hs = smem + 2 * kBN * kLDK;   // [2][kBM][kLDK]
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wn = wave >> 1, wt = wave & 1;
 
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  int j = 0;
-  while (j + 1 < p.n_jobs && bid >= p.jobs[j + 1].tile_begin) ++j;
-  const GemmJob job = p.jobs[j];
-  const int local = bid - job.tile_begin;
+  const int unit = xcd_remap(blockIdx.x, gridDim.x);
+  const GemmJob job = p.jobs[job_of(p, unit)];
+  const int local = unit - job.tile_begin;
   const int N = job.n, K = job.k;
   const int64_t M = p.m;
   const int ntn = (N + kBN - 1) / kBN;
@@ -90,31 +61,36 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
   const uint16_t* Hh = static_cast<const uint16_t*>(job.a);
   const int nk = K / kBK;
 
-  // Global -> register staging: 8 16-byte chunks per tile row; 2048 chunks per operand tile.
-  uint4 rw[8], rh[8];
-  auto gload = [&](int kc) {
+  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x 9 slots = 2304
+  // 16-byte slots = 9 wave-wide instructions per wave; lane i of instruction j of wave w fills slot
+  // (4j + w) * 64 + i and pad slots (slot % 9 == 8) are masked off.  Weight rows past N repeat row
+  // N - 1 and token rows past M repeat row M - 1: they only feed accumulators that are never stored.
+  constexpr int kDmaIters = kBN * kSlots / (4 * 64);
+  static_assert(kBN == kBM && kBN * kSlots == kDmaIters * 4 * 64, "DMA slot cover");
+  const uint16_t* wsrc[kDmaIters];
+  const uint16_t* hsrc[kDmaIters];
+  bool live[kDmaIters];
+#pragma unroll
+  for (int j = 0; j < kDmaIters; ++j) {
+    const int slot = (4 * j + wave) * 64 + lane;
+    const int rho = slot / kSlots, cc = slot - rho * kSlots;
+    live[j] = cc < kBK / 8;
+    const int n = n0 + row_of_lds(rho) < N ? n0 + row_of_lds(rho) : N - 1;
+    const int64_t t = t0 + rho < M ? t0 + rho : M - 1;
+    wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * cc;
+    hsrc[j] = Hh + t * K + 8 * cc;
+  }
+  auto stage = [&](int kc, int b) {
+    uint16_t* ws = smem + b * kStage;
+    uint16_t* hs = ws + kBN * kLDK;
     const int kb = kc * kBK;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int q = tid + kThreads * i;
-      const int row = q >> 3, c = q & 7;
-      const int n = n0 + row;
-      rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + static_cast<int64_t>(n) * K + kb + 8 * c)
-                    : make_uint4(0, 0, 0, 0);
-      const int64_t t = t0 + row;
-      rh[i] = t < M ? *reinterpret_cast<const uint4*>(Hh + t * K + kb + 8 * c)
-                    : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-    uint16_t* wb = Ws + buf * kBN * kLDK;
-    uint16_t* hb = Hs + buf * kBM * kLDK;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int q = tid + kThreads * i;
-      const int row = q >> 3, c = q & 7;
-      *reinterpret_cast<uint4*>(wb + lds_row_of_channel(row) * kLDK + 8 * c) = rw[i];
-      *reinterpret_cast<uint4*>(hb + row * kLDK + 8 * c) = rh[i];
+    for (int j = 0; j < kDmaIters; ++j) {
+      const int base = (4 * j + wave) * 64;
+      if (live[j]) {
+        __builtin_amdgcn_global_load_lds(wsrc[j] + kb, (lds_void_t)(ws + 8 * base), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(hsrc[j] + kb, (lds_void_t)(hs + 8 * base), 16, 0, 0);
+      }
     }
   };
 
@@ -127,34 +103,49 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
       for (int e = 0; e < 16; ++e) acc[s][u][e] = 0.f;
 
   const int lr = lane & 31, lk = (lane >> 5) * 8;
-  auto compute = [&](int buf) {
-    const uint16_t* wb = Ws + buf * kBN * kLDK + (wn * 128 + lr) * kLDK + lk;
-    const uint16_t* hb = Hs + buf * kBM * kLDK + (wt * 128 + lr) * kLDK + lk;
+  // Fragments of k-slice ks (16 wide) of the current stage: 4 weight blocks, 4 token blocks.
+  auto frags = [&](const uint16_t* wb, const uint16_t* hb, int ks, bf16x8* af, bf16x8* bfr) {
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8 af[4], bfr[4];
+    for (int s = 0; s < 4; ++s)
+      af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + ks * 16);
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + ks * 16);
+    for (int u = 0; u < 4; ++u)
+      bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + ks * 16);
+  };
+  auto mma = [&](const bf16x8* af, const bf16x8* bfr) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + ks * 16);
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
-    }
+        acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
-  gload(0);
-  sstore(0);
+  stage(0, 0);
+  wait_vmem();
   __syncthreads();
   for (int kc = 0; kc < nk; ++kc) {
     const int cur = kc & 1;
-    if (kc + 1 < nk) gload(kc + 1);
-    compute(cur);
-    if (kc + 1 < nk) sstore(cur ^ 1);
+    if (kc + 1 < nk) stage(kc + 1, cur ^ 1);
+    const uint16_t* wb = smem + cur * kStage + (wn * 128 + lr) * kLDK + lk;
+    const uint16_t* hb = smem + cur * kStage + kBN * kLDK + (wt * 128 + lr) * kLDK + lk;
+    // Slice ks + 2's LDS reads are interleaved with slice ks + 1's MFMAs (one read after each of
+    // the first eight), so they have landed by the time their own MFMAs issue.
+    bf16x8 a0[4], b0[4], a1[4], b1[4];
+    frags(wb, hb, 0, a0, b0);
+    frags(wb, hb, 1, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a1, b1);
+    frags(wb, hb, 2, a0, b0);
+    interleave_reads();
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a0, b0);
+    frags(wb, hb, 3, a1, b1);
+    interleave_reads();
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a1, b1);
+    wait_vmem();
     __syncthreads();
   }
 
@@ -231,7 +222,7 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
     const int64_t t = t0 + wt * 128 + 32 * u + (lane & 31);
     if (t >= M) continue;
     const float2* cs_row =
-        rope ? p.rope + static_cast<int64_t>(token_position(p, t)) * half : nullptr;
+        rope ? p.rope + static_cast<int64_t>(row_position(p, t)) * half : nullptr;
     if (pstride == 2) {
       finish_pair(IntC<0>{}, IntC<2>{}, u, t, cs_row);
       finish_pair(IntC<1>{}, IntC<2>{}, u, t, cs_row);
