@@ -9,11 +9,13 @@
 // one lane and the epilogue needs no LDS: bias, rotation and bf16 rounding happen in registers and
 // each lane stores two 16-byte vectors per block.
 //
-// K advances 64 at a time through two LDS stages (2 x (256 + 256) x 72 bf16 = 144 KiB, rows padded
-// by 16 bytes so MFMA operand reads are conflict-free).  Both operand tiles travel global -> LDS
-// directly (global_load_lds_dwordx4), so the copy of stage k+1 needs no registers and runs under
-// the MFMAs of stage k; inside a stage the operand fragments of the next 16-wide k-slice are read
-// from LDS while the MFMAs of the current one issue.
+// K advances 32 at a time through a ring of kStages LDS stages ((256 + 256) x 32 bf16 = 32 KiB
+// each; the 16-byte chunks of each row are XOR-swizzled so MFMA operand reads are conflict-free).
+// Both operand tiles travel global -> LDS directly (global_load_lds_dwordx4): the copy of stage
+// k + kStages - 1 is issued between the MFMAs of stage k, so kStages - 1 stages are in flight and
+// the copy latency (over a microsecond under full load) hides behind that many steps of MFMAs.
+// Each step is two 16-wide k-slices; the workgroup barrier sits between them, so the operand reads
+// of the next stage's first slice also run under MFMAs.
 #include "scd_device.h"
 
 namespace scd {
@@ -23,14 +25,30 @@ using namespace dev;
 
 constexpr int kBM = kPatchBM;   // tokens per tile
 constexpr int kBN = kPatchBN;   // channels per tile
-constexpr int kBK = 64;         // contraction step
-constexpr int kLDK = kBK + 8;   // padded LDS row (bf16 elements)
-constexpr int kSlots = kLDK / 8;  // 16-byte slots per LDS row (8 data + 1 pad)
+constexpr int kBK = 32;         // contraction step (one pipeline stage)
+constexpr int kLDK = kBK;       // LDS row (bf16 elements): 4 16-byte chunks, stored swizzled
 constexpr int kStage = (kBN + kBM) * kLDK;  // elements per pipeline stage
+constexpr int kStages = 4;      // 4 x 32 KiB = 128 KiB of LDS
 constexpr int kThreads = 256;
+constexpr int kDmaPerStage = 2 * (kBN * kBK / 8) / kThreads;  // DMA instructions per wave per stage
+
+// Chunk c of LDS row r (64 bytes) sits at chunk position c ^ swz(r).  ds_read_b128 serves 8
+// lanes per cycle from 32 4-byte banks (128 bytes), and an MFMA operand read has lanes 8i..8i+7 on
+// rows 8i'..8i'+7 of one chunk: with swz(r) = (r >> 1) & 3 the two rows sharing a bank row take
+// different 16-byte positions, so the 8 lanes hit 8 distinct bank groups (measured conflict-free on
+// gfx950 with the SQ_LDS_BANK_CONFLICT counter).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
+
+// s_waitcnt immediates: at most n vector-memory operations outstanding (optionally with every LDS
+// access completed), or every LDS access completed.
+constexpr int vmcnt_imm(int n, bool lds_done = false) {
+  return (n & 15) | ((n >> 4) << 14) | (0x7 << 4) | ((lds_done ? 0 : 0xF) << 8);
+}
+constexpr int kLgkmDone = 0xF | (0x3 << 14) | (0x7 << 4);
 
 // Scheduling groups for one block of 16 MFMAs and 8 LDS reads that do not feed them: one read
-// after each of the first eight MFMAs.
+// after each of the first eight MFMAs.  interleave_reads_dma spreads the stage's LDS-DMA copies over
+// the first MFMAs of the block the same way.
 __device__ __forceinline__ void interleave_reads() {
 #define SCD_MFMA_THEN_READ                          \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
@@ -40,13 +58,23 @@ __device__ __forceinline__ void interleave_reads() {
 #undef SCD_MFMA_THEN_READ
   __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
 }
+__device__ __forceinline__ void interleave_reads_dma() {
+#define SCD_MFMA_READ_DMA                            \
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
+  __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); \
+  __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
+  SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
+#undef SCD_MFMA_READ_DMA
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+}
 
 __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave >> 1, wt = wave & 1;
 
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
@@ -61,24 +89,23 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
   const uint16_t* Hh = static_cast<const uint16_t*>(job.a);
   const int nk = K / kBK;
 
-  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x 9 slots = 2304
-  // 16-byte slots = 9 wave-wide instructions per wave; lane i of instruction j of wave w fills slot
-  // (4j + w) * 64 + i and pad slots (slot % 9 == 8) are masked off.  Weight rows past N repeat row
-  // N - 1 and token rows past M repeat row M - 1: they only feed accumulators that are never stored.
-  constexpr int kDmaIters = kBN * kSlots / (4 * 64);
-  static_assert(kBN == kBM && kBN * kSlots == kDmaIters * 4 * 64, "DMA slot cover");
+  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x 4 chunks = 1024
+  // 16-byte slots = 4 wave-wide instructions per wave; lane i of instruction j of wave w fills slot
+  // (4j + w) * 64 + i (row slot / 4, position slot % 4) with the chunk that belongs there.  Weight
+  // rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
+  // accumulators that are never stored.
+  constexpr int kDmaIters = kBN * (kBK / 8) / (4 * 64);
+  static_assert(kBN == kBM && 2 * kDmaIters == kDmaPerStage, "DMA slot cover");
   const uint16_t* wsrc[kDmaIters];
   const uint16_t* hsrc[kDmaIters];
-  bool live[kDmaIters];
 #pragma unroll
   for (int j = 0; j < kDmaIters; ++j) {
     const int slot = (4 * j + wave) * 64 + lane;
-    const int rho = slot / kSlots, cc = slot - rho * kSlots;
-    live[j] = cc < kBK / 8;
+    const int rho = slot >> 2, c = (slot & 3) ^ swz(slot >> 2);
     const int n = n0 + row_of_lds(rho) < N ? n0 + row_of_lds(rho) : N - 1;
     const int64_t t = t0 + rho < M ? t0 + rho : M - 1;
-    wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * cc;
-    hsrc[j] = Hh + t * K + 8 * cc;
+    wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * c;
+    hsrc[j] = Hh + t * K + 8 * c;
   }
   auto stage = [&](int kc, int b) {
     uint16_t* ws = smem + b * kStage;
@@ -87,10 +114,8 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
 #pragma unroll
     for (int j = 0; j < kDmaIters; ++j) {
       const int base = (4 * j + wave) * 64;
-      if (live[j]) {
-        __builtin_amdgcn_global_load_lds(wsrc[j] + kb, (lds_void_t)(ws + 8 * base), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(hsrc[j] + kb, (lds_void_t)(hs + 8 * base), 16, 0, 0);
-      }
+      __builtin_amdgcn_global_load_lds(wsrc[j] + kb, (lds_void_t)(ws + 8 * base), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(hsrc[j] + kb, (lds_void_t)(hs + 8 * base), 16, 0, 0);
     }
   };
 
@@ -102,15 +127,18 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[s][u][e] = 0.f;
 
-  const int lr = lane & 31, lk = (lane >> 5) * 8;
-  // Fragments of k-slice ks (16 wide) of the current stage: 4 weight blocks, 4 token blocks.
+  const int lr = lane & 31, lh = lane >> 5;
+  // Fragments of k-slice ks (16 wide) of the current stage: 4 weight blocks, 4 token blocks.  Lane
+  // half h reads chunk 2 ks + h of its row; every block starts at a multiple of 32 rows, so the
+  // row's swizzle is swz(lane % 32).
   auto frags = [&](const uint16_t* wb, const uint16_t* hb, int ks, bf16x8* af, bf16x8* bfr) {
+    const int co = 8 * ((2 * ks + lh) ^ swz(lr));
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + ks * 16);
+      af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + co);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + ks * 16);
+      bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + co);
   };
   auto mma = [&](const bf16x8* af, const bf16x8* bfr) {
 #pragma unroll
@@ -120,34 +148,52 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
         acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
-  stage(0, 0);
-  wait_vmem();
-  __syncthreads();
+  // Prologue: stages 0 .. kStages - 2 in flight, wait for stage 0, read its first slice.  A stage
+  // index past the end re-copies the last stage into a buffer that is never read for data (its
+  // reads only feed the discarded look-ahead of the final step), so every step issues the same
+  // number of copies and one vmcnt threshold holds throughout.
+  auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
+#pragma unroll
+  for (int st = 0; st < kStages - 1; ++st) stage(clamp(st), st);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
+  __builtin_amdgcn_s_barrier();
+  const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
+  const uint16_t* hrow = smem + kBN * kLDK + (wt * 128 + lr) * kLDK;
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  frags(wrow, hrow, 0, a0, b0);
+  int rb = 0;                // buffer holding stage kc
+  int wbuf = kStages - 1;    // buffer stage kc + kStages - 1 goes to
   for (int kc = 0; kc < nk; ++kc) {
-    const int cur = kc & 1;
-    if (kc + 1 < nk) stage(kc + 1, cur ^ 1);
-    const uint16_t* wb = smem + cur * kStage + (wn * 128 + lr) * kLDK + lk;
-    const uint16_t* hb = smem + cur * kStage + kBN * kLDK + (wt * 128 + lr) * kLDK + lk;
-    // Slice ks + 2's LDS reads are interleaved with slice ks + 1's MFMAs (one read after each of
-    // the first eight), so they have landed by the time their own MFMAs issue.
-    bf16x8 a0[4], b0[4], a1[4], b1[4];
-    frags(wb, hb, 0, a0, b0);
+    const int nb = rb + 1 == kStages ? 0 : rb + 1;
+    const uint16_t* wb = wrow + rb * kStage;
+    const uint16_t* hb = hrow + rb * kStage;
+    // Slice 0's operands were read between the previous MFMAs; retiring them here keeps the waits
+    // inside this block from covering the reads it issues itself.
+    __builtin_amdgcn_s_waitcnt(kLgkmDone);
+    __builtin_amdgcn_sched_barrier(0);
+    // Slice 0's MFMAs, with slice 1's reads and the next copy between them.  The copy overwrites
+    // the buffer stage kc - 1 used, whose last reads completed before the previous barrier.
+    mma(a0, b0);
     frags(wb, hb, 1, a1, b1);
+    stage(clamp(kc + kStages - 1), wbuf);
+    interleave_reads_dma();
     __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
+    // Stage kc + 1 has landed for this wave once at most kStages - 2 stages' copies are pending, and
+    // its reads of stage kc are complete once no LDS access is pending; the barrier makes both
+    // true for every wave.  (A plain s_barrier: a fenced one would wait for every copy in flight.)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
+    __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    // Slice 1's MFMAs, with the next stage's slice-0 reads between them.
     mma(a1, b1);
-    frags(wb, hb, 2, a0, b0);
+    frags(wrow + nb * kStage, hrow + nb * kStage, 0, a0, b0);
     interleave_reads();
     __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    frags(wb, hb, 3, a1, b1);
-    interleave_reads();
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a1, b1);
-    wait_vmem();
-    __syncthreads();
+    rb = nb;
+    wbuf = wbuf + 1 == kStages ? 0 : wbuf + 1;
   }
+  // drain the look-ahead copies before the workgroup's LDS is released
+  wait_vmem();
 
   // Epilogue.  Lane l holds, for block (s, u), token t0 + wt*128 + 32u + l%32 and channels
   // n0 + wn*128 + 32s + 16*(l/32) + r, r = 0..15.
