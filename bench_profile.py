@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""Summarise rocprofv3 runs of ``bench.py`` into the text files under ``profiles/``.
+
+Inputs are the CSV folders rocprofv3 writes:
+  --trace DIR   ``rocprofv3 --kernel-trace --stats --output-format csv -d DIR -o kt -- python bench.py ...``
+  --fetch DIR   ``rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR -o f -- python bench.py ... --copy-probe-gib 1``
+  --write DIR   the same with ``--pmc WRITE_SIZE``
+
+Writes ``profiles/kernels_<workload>.md`` (per-launch kernel durations, warm-up launches dropped) and,
+with the counter runs, ``profiles/traffic_<workload>.json`` + ``.md``: HBM bytes per entry-point
+call, calibrated against the plain 1 GiB copy that ``bench.py --copy-probe-gib 1`` runs after timing
+(FETCH_SIZE and WRITE_SIZE are in KiB; each is scaled by true bytes / counter bytes of that copy).
+The JSON carries the digest of the HIP sources it was measured on; ``bench.py`` reports ``traffic``
+only while that digest matches.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import glob
+import json
+import os
+import statistics
+
+import bench
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+PHASES = {"encode_bf16_kernel": "encode", "reuse_decode": "reuse_decode",
+          "patch_kv": "patch_kv", "EncodeKV": "encode", "EncodeH": "encode",
+          "ReuseDecode": "reuse_decode", "PatchKV": "patch_kv"}
+
+
+def phase_of(name: str):
+    for frag, ph in PHASES.items():
+        if frag in name:
+            return ph
+    return None
+
+
+def short(name: str) -> str:
+    name = name.replace("scd::(anonymous namespace)::", "").replace("(scd::GemmParams)", "")
+    return name.replace("void ", "")[:70]
+
+
+def one_csv(folder: str, suffix: str) -> str:
+    found = glob.glob(os.path.join(folder, "**", f"*{suffix}"), recursive=True)
+    if not found:
+        raise SystemExit(f"no *{suffix} under {folder}")
+    return found[0]
+
+
+def kernel_table(trace_dir: str, warmup_launches: int):
+    """Per (kernel, grid) group of codec kernels: launches, mean/min/max microseconds, with the first
+    ``warmup_launches`` launches of each group dropped."""
+    rows = list(csv.DictReader(open(one_csv(trace_dir, "kernel_trace.csv"))))
+    groups = collections.OrderedDict()
+    for r in rows:
+        if phase_of(r["Kernel_Name"]) is None:
+            continue
+        grid = r.get("Grid_Size") or r.get("Grid_Size_X") or 0
+        key = (r["Kernel_Name"], int(grid))
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        groups.setdefault(key, []).append(dur)
+    out = []
+    for (name, grid), d in groups.items():
+        d = d[warmup_launches:] or d
+        out.append({"kernel": short(name), "phase": phase_of(name), "grid": grid, "launches": len(d),
+                    "mean_us": statistics.mean(d), "min_us": min(d), "max_us": max(d)})
+    return out
+
+
+def counters(folder: str, counter: str):
+    rows = list(csv.DictReader(open(one_csv(folder, "counter_collection.csv"))))
+    return [r for r in rows if r["Counter_Name"] == counter]
+
+
+def calibration(rows, true_bytes: int) -> float:
+    """true bytes / counter bytes of the probe copy (the last three elementwise launches with the
+    probe's element count)."""
+    probe = [r for r in rows if "elementwise" in r["Kernel_Name"]
+             and int(r["Grid_Size"]) * 16 == true_bytes]
+    if not probe:
+        raise SystemExit("copy probe dispatches not found (run bench.py with --copy-probe-gib 1)")
+    kib = statistics.median(float(r["Counter_Value"]) for r in probe[-3:])
+    return true_bytes / (kib * 1024.0)
+
+
+def per_phase_bytes(rows, scale: float):
+    """Median counter bytes per (kernel, grid) group, summed per phase (one entry-point call)."""
+    groups = collections.defaultdict(list)
+    for r in rows:
+        ph = phase_of(r["Kernel_Name"])
+        if ph is not None:
+            groups[(ph, r["Kernel_Name"], r["Grid_Size"])].append(float(r["Counter_Value"]))
+    out = collections.defaultdict(float)
+    for (ph, _, _), v in groups.items():
+        out[ph] += statistics.median(v) * 1024.0 * scale
+    return dict(out)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--workload", default="llama3_8b_bf16")
+    ap.add_argument("--trace")
+    ap.add_argument("--trace-cmd", default="")
+    ap.add_argument("--warmup-launches", type=int, default=3)
+    ap.add_argument("--bench-log", help="log whose first JSON line is the traced bench run's")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--pmc-cmd", default="")
+    ap.add_argument("--probe-gib", type=float, default=1.0)
+    args = ap.parse_args()
+
+    from synth import workloads as W
+    wl = {w.name: w for w in (*W.CONFIGS, *W.TEST_WORKLOADS)}[args.workload]
+    alg = bench.algorithmic(wl)
+    digest = bench.source_digest()
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+
+    if args.trace:
+        tab = kernel_table(args.trace, args.warmup_launches)
+        lines = [f"# Codec kernels, {wl.name} (T={wl.n_tokens}, L={wl.n_layers}, d={wl.d_model}, "
+                 f"{wl.n_kv_heads}x{wl.head_dim}, r={sorted(set(wl.ranks))}, Patch layers "
+                 f"{list(wl.patch_layers)})", "",
+                 f"Command: `{args.trace_cmd}`", "",
+                 f"Source digest of csrc/: `{digest}`. Durations from the kernel trace, first "
+                 f"{args.warmup_launches} launches of each kernel (the warm-up steps) dropped.", "",
+                 "| kernel | step | grid (work-items) | launches | mean us | min us | max us |",
+                 "|---|---|---|---|---|---|---|"]
+        per_phase = collections.defaultdict(float)
+        for t in tab:
+            lines.append(f"| `{t['kernel']}` | {t['phase']} | {t['grid']} | {t['launches']} | "
+                         f"{t['mean_us']:.1f} | {t['min_us']:.1f} | {t['max_us']:.1f} |")
+            per_phase[t["phase"]] += t["mean_us"]
+        events = {}
+        if args.bench_log:
+            for line in open(args.bench_log):  # the first JSON line is the traced run's
+                if line.startswith("{"):
+                    events = json.loads(line).get("phase_ms", {})
+                    break
+        lines += ["", "Per entry-point call (sum of its launches) and the algorithmic roofline; "
+                  "\"bench events\" is bench.py's own HIP-event time of the same call in the "
+                  "same traced run:", "",
+                  "| step | us per call | bench events us | algorithmic | achieved | fraction of peak |",
+                  "|---|---|---|---|---|---|"]
+        for ph, us in per_phase.items():
+            ev = f"{events[ph] * 1e3:.1f}" if ph in events else "-"
+            b, f = alg[ph]
+            bound = bench.KERNELS[ph][1]
+            if bound == "hbm":
+                ach = b / (us * 1e-6) / 1e9
+                lines.append(f"| {ph} | {us:.1f} | {ev} | {b / 1e9:.4f} GB | {ach:.0f} GB/s | "
+                             f"{ach / bench.HBM_PEAK_GBPS:.3f} of 8 TB/s |")
+            else:
+                ach = f / (us * 1e-6) / 1e12
+                peak = bench.MFMA_PEAK_TFLOPS[wl.dtype]
+                lines.append(f"| {ph} | {us:.1f} | {ev} | {f / 1e9:.1f} GFLOP | {ach:.0f} TFLOP/s | "
+                             f"{ach / peak:.3f} of {peak:.0f} TFLOP/s |")
+        path = os.path.join(ROOT, "profiles", f"kernels_{wl.name}.md")
+        open(path, "w").write("\n".join(lines) + "\n")
+        print("wrote", path)
+
+    if args.fetch and args.write:
+        true_bytes = int(args.probe_gib * (1 << 30))
+        frows, wrows = counters(args.fetch, "FETCH_SIZE"), counters(args.write, "WRITE_SIZE")
+        fs, ws = calibration(frows, true_bytes), calibration(wrows, true_bytes)
+        fb, wb = per_phase_bytes(frows, fs), per_phase_bytes(wrows, ws)
+        steps = {}
+        for ph in ("encode", "reuse_decode", "patch_kv"):
+            if ph in fb and ph in wb:
+                tot = fb[ph] + wb[ph]
+                steps[ph] = {"fetch_bytes": round(fb[ph]), "write_bytes": round(wb[ph]),
+                             "hbm_bytes_per_launch": round(tot),
+                             "algorithmic_bytes": alg[ph][0],
+                             "ratio_to_algorithmic": round(tot / alg[ph][0], 4)}
+        rec = {"workload": wl.name, "source_digest": digest, "command": args.pmc_cmd,
+               "calibration": {"probe_bytes": true_bytes, "fetch_scale": round(fs, 4),
+                               "write_scale": round(ws, 4)},
+               "unit": "bytes per entry-point call (sum of its launches)", "steps": steps}
+        jpath = os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json")
+        json.dump(rec, open(jpath, "w"), indent=1)
+        lines = [f"# HBM traffic per entry-point call, {wl.name}", "",
+                 f"Command (one pass per counter): `{args.pmc_cmd}`", "",
+                 f"Source digest of csrc/: `{digest}`. Calibration: a plain copy of "
+                 f"{true_bytes} bytes reads FETCH_SIZE x {fs:.4f} and WRITE_SIZE x {ws:.4f} of its "
+                 f"true bytes; both scales are applied below.", "",
+                 "| step | fetch (GB) | write (GB) | total (GB) | algorithmic (GB) | ratio |",
+                 "|---|---|---|---|---|---|"]
+        for ph, s in steps.items():
+            lines.append(f"| {ph} | {s['fetch_bytes'] / 1e9:.4f} | {s['write_bytes'] / 1e9:.4f} | "
+                         f"{s['hbm_bytes_per_launch'] / 1e9:.4f} | "
+                         f"{s['algorithmic_bytes'] / 1e9:.4f} | {s['ratio_to_algorithmic']:.3f} |")
+        open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.md"), "w").write(
+            "\n".join(lines) + "\n")
+        print("wrote", jpath)
+
+
+if __name__ == "__main__":
+    main()

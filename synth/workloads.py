@@ -112,7 +112,9 @@ SMALL_HEAD_SHARED = Workload("small_head_shared_bf16", 3, 256, 4, 64, (129, 250)
                              pos0=(5, 1000))
 SMALL_F32 = Workload("small_f32", 3, 320, 2, 64, (97, 200, 31), (16, 48, 32), (0,), 1e4, "f32",
                      with_bias=True)
-TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32)
+# d_model = 64: the Patch contraction is shorter than the copy pipeline is deep; one KV head.
+SMALL_NARROW = Workload("small_narrow_bf16", 2, 64, 1, 128, (200, 57), (64, 32), (1,), 1e4, "bf16")
+TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW)
 
 
 # --------------------------------------------------------------------------------------------
