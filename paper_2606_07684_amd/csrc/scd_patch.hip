@@ -25,19 +25,33 @@ using namespace dev;
 
 constexpr int kBM = kPatchBM;   // tokens per tile
 constexpr int kBN = kPatchBN;   // channels per tile
-constexpr int kBK = 32;         // contraction step (one pipeline stage)
-constexpr int kLDK = kBK;       // LDS row (bf16 elements): 4 16-byte chunks, stored swizzled
+#ifndef SCD_PATCH_BK
+#define SCD_PATCH_BK 32
+#define SCD_PATCH_STAGES 4
+#endif
+constexpr int kBK = SCD_PATCH_BK;     // contraction step (one pipeline stage)
+constexpr int kLDK = kBK;             // LDS row (bf16 elements): kBK / 8 16-byte chunks, swizzled
+constexpr int kChunks = kBK / 8;
+constexpr int kSlices = kBK / 16;     // 16-wide MFMA k-slices per stage
 constexpr int kStage = (kBN + kBM) * kLDK;  // elements per pipeline stage
-constexpr int kStages = 4;      // 4 x 32 KiB = 128 KiB of LDS
+constexpr int kStages = SCD_PATCH_STAGES;   // ring depth; kStages * kStage * 2 bytes of LDS
 constexpr int kThreads = 256;
 constexpr int kDmaPerStage = 2 * (kBN * kBK / 8) / kThreads;  // DMA instructions per wave per stage
+static_assert(kSlices == 2 || kSlices == 4, "stage = 2 or 4 k-slices");
+static_assert(kStages * kStage * 2 <= 160 * 1024, "LDS");
 
-// Chunk c of LDS row r (64 bytes) sits at chunk position c ^ swz(r).  ds_read_b128 serves 8
-// lanes per cycle from 32 4-byte banks (128 bytes), and an MFMA operand read has lanes 8i..8i+7 on
-// rows 8i'..8i'+7 of one chunk: with swz(r) = (r >> 1) & 3 the two rows sharing a bank row take
-// different 16-byte positions, so the 8 lanes hit 8 distinct bank groups (measured conflict-free on
-// gfx950 with the SQ_LDS_BANK_CONFLICT counter).
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
+// Chunk c of LDS row r (64 bytes) sits at chunk position c ^ swz(r).  Among the swizzles tried on
+// this kernel's exact read sequence (both operand regions, 4 waves, both k-slices of a stage),
+// (r ^ (r >> 2)) & 3 is the fastest, together with ((r >> 2) ^ (r >> 1)) & 3 and 16-byte row
+// padding; no swizzle is 4x slower and (r >> 1) & 3 1.2x slower (SQ_LDS_BANK_CONFLICT agrees).
+// The fragment reads plus the copies' LDS writes come close to the LDS bandwidth, so this matters.
+#ifndef SCD_PATCH_SWZ8
+#define SCD_PATCH_SWZ8 0
+#endif
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (kChunks == 4) return (r ^ (r >> 2)) & 3;
+  return SCD_PATCH_SWZ8 == 0 ? r & 7 : (r ^ (r >> 3)) & 7;
+}
 
 // s_waitcnt immediates: at most n vector-memory operations outstanding (optionally with every LDS
 // access completed), or every LDS access completed.
@@ -62,7 +76,7 @@ __device__ __forceinline__ void interleave_reads_dma() {
 #define SCD_MFMA_READ_DMA                            \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
   __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  __builtin_amdgcn_sched_group_barrier(0x020, kDmaPerStage / 8, 0);
   SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
   SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
 #undef SCD_MFMA_READ_DMA
@@ -94,14 +108,14 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
   // (4j + w) * 64 + i (row slot / 4, position slot % 4) with the chunk that belongs there.  Weight
   // rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
   // accumulators that are never stored.
-  constexpr int kDmaIters = kBN * (kBK / 8) / (4 * 64);
+  constexpr int kDmaIters = kBN * kChunks / (4 * 64);
   static_assert(kBN == kBM && 2 * kDmaIters == kDmaPerStage, "DMA slot cover");
   const uint16_t* wsrc[kDmaIters];
   const uint16_t* hsrc[kDmaIters];
 #pragma unroll
   for (int j = 0; j < kDmaIters; ++j) {
     const int slot = (4 * j + wave) * 64 + lane;
-    const int rho = slot >> 2, c = (slot & 3) ^ swz(slot >> 2);
+    const int rho = slot / kChunks, c = (slot % kChunks) ^ swz(slot / kChunks);
     const int n = n0 + row_of_lds(rho) < N ? n0 + row_of_lds(rho) : N - 1;
     const int64_t t = t0 + rho < M ? t0 + rho : M - 1;
     wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * c;
@@ -178,13 +192,23 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
     stage(clamp(kc + kStages - 1), wbuf);
     interleave_reads_dma();
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kSlices == 4) {
+      mma(a1, b1);
+      frags(wb, hb, 2, a0, b0);
+      interleave_reads();
+      __builtin_amdgcn_sched_barrier(0);
+      mma(a0, b0);
+      frags(wb, hb, 3, a1, b1);
+      interleave_reads();
+      __builtin_amdgcn_sched_barrier(0);
+    }
     // Stage kc + 1 has landed for this wave once at most kStages - 2 stages' copies are pending, and
     // its reads of stage kc are complete once no LDS access is pending; the barrier makes both
     // true for every wave.  (A plain s_barrier: a fenced one would wait for every copy in flight.)
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // Slice 1's MFMAs, with the next stage's slice-0 reads between them.
+    // The last slice's MFMAs, with the next stage's slice-0 reads between them.
     mma(a1, b1);
     frags(wrow + nb * kStage, hrow + nb * kStage, 0, a0, b0);
     interleave_reads();
