@@ -124,7 +124,9 @@ size_t scd_payload_bytes(const scd_model_t* model, int64_t n_tokens, int64_t* of
  * with k_in, v_in [T, H, d_h], w_enc_k [rank_k, w], w_enc_v [rank_v, w], mu [w] (the optional
  * producer-side offset; NULL array or NULL entry = 0, which is the paper's equation).
  * For every Patch layer l:  z_h[l] = h_in[l] w_enc_h[l]^T  with h_in [T, d_model] (the producer's
- * normalised attention input) and w_enc_h [rank_h, d_model]; z_h [T, rank_h]. */
+ * normalised attention input) and w_enc_h [rank_h, d_model]; z_h [T, rank_h].
+ * bf16 keys: the de-rotated input is rounded to bf16 once before the product; the offset enters as
+ * the fp32 term mu w_enc^T subtracted from the accumulator, so it is never rounded. */
 scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
                         const void* rope_table, int64_t max_position,
                         const void* const* k_in, const void* const* v_in,

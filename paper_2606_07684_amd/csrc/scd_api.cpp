@@ -166,7 +166,7 @@ scd_status_t run(scd::Op op, const std::vector<scd::GemmParams>& launches, int d
   return ok();
 }
 
-// Splits jobs into launches that each hold one rank (jobs of equal key), in first-seen order.
+// Splits jobs into launches of equal key (one kernel instance each), in first-seen order.
 template <typename KeyFn>
 std::vector<std::vector<scd::GemmJob>> group_by(const std::vector<scd::GemmJob>& jobs, KeyFn key) {
   std::vector<std::vector<scd::GemmJob>> groups;
@@ -357,17 +357,21 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
   }
   const scd::GemmParams kv_base = base_params(model, batch, T * g, g, rope_table, max_position);
   const scd::GemmParams h_base = base_params(model, batch, T, 1, rope_table, max_position);
-  auto by_rank = [](const scd::GemmJob& j) { return j.n; };
+  // one launch per (rank, branch kind, offset present): each is its own kernel instance
+  auto by_kind = [](const scd::GemmJob& j) {
+    const bool mu = (j.flags & scd::kVecIn) != 0 && j.vec != nullptr;
+    return j.n * 4 + ((j.flags & scd::kDeropeIn) != 0 ? 2 : 0) + (mu ? 1 : 0);
+  };
   auto enc = [&](const scd::GemmParams& p) { return scd::launch_encode_bf16(p, stream); };
   if (fast_kv) {
-    SCD_TRY(run_groups(kv_base, scd::kEncodeRows, 256, group_by(kv_jobs, by_rank), enc, "encode"));
+    SCD_TRY(run_groups(kv_base, scd::kEncodeRows, 256, group_by(kv_jobs, by_kind), enc, "encode"));
   } else {
     JobPacker jp(kv_base, scd::kGenericBM, scd::kGenericBN);
     for (const auto& j : kv_jobs) jp.add(j);
     SCD_TRY(run(scd::Op::kEncodeKV, jp.build(), model->dtype, stream));
   }
   if (fast_h)
-    return run_groups(h_base, scd::kEncodeRows, 256, group_by(h_jobs, by_rank), enc, "encode");
+    return run_groups(h_base, scd::kEncodeRows, 256, group_by(h_jobs, by_kind), enc, "encode");
   JobPacker hp(h_base, scd::kGenericBM, scd::kGenericBN);
   for (const auto& j : h_jobs) hp.add(j);
   return run(scd::Op::kEncodeH, hp.build(), model->dtype, stream);

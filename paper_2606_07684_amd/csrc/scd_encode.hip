@@ -5,13 +5,18 @@
 // A workgroup of 4 waves owns 128 input rows of one layer-branch and produces all RB*32 code
 // columns for them.  Every wave streams its 32 rows straight from HBM into registers, 128 input
 // columns (one chunk) at a time, one chunk ahead of use.  With deRoPE each lane loads the same
-// 8 columns of both halves of a head, so every rotation pair meets in one lane; the rotated,
-// offset-subtracted values are rounded to bf16 and used directly as the B operand of
-// v_mfma_f32_32x32x16_bf16.  Each lane keeps the cosines and sines of its row in registers for
-// all heads.  The encoder weight chunk (all code rows x 128 columns, rows permuted so each lane
-// ends with 16 consecutive code columns of one row) is double-buffered in LDS and shared by the
-// four waves.  Both operands visit the columns of a chunk in the same order, so the contraction
-// is unchanged.
+// 8 columns of both halves of a head, so every rotation pair meets in one lane; the rotated values
+// are rounded to bf16 and used directly as the B operand of v_mfma_f32_32x32x16_bf16 (without
+// deRoPE the loaded bf16 values are the operand as they are).  Each lane keeps the cosines and
+// sines of its row in registers for all heads.  The encoder weight chunk (all code rows x 128
+// columns, rows permuted so each lane ends with 16 consecutive code columns of one row) is
+// double-buffered in LDS and shared by the four waves.  Both operands visit the columns of a chunk
+// in the same order, so the contraction is unchanged.
+//
+// The offset is folded into the product: (X - 1 mu^T) E^T = X E^T - 1 (E mu)^T.  E mu is one more
+// MFMA per k-step with mu as a B operand broadcast to all 32 columns; wave w computes it for the
+// code blocks b = w (mod 4), the workgroup shares it through LDS and every lane subtracts it from
+// its fp32 accumulators.  The offset therefore costs no per-element work and is never rounded.
 #include "scd_device.h"
 
 namespace scd {
@@ -34,12 +39,15 @@ __device__ constexpr int chunk_col(int s, int h, bool derope) {
   return hc * DH + (sw & 1) * (DH / 2) + 16 * (sw >> 1) + 8 * h;
 }
 
-// RB = code blocks of 32 (rank <= 32*RB); DH = head_dim (64 or 128, used with deRoPE).
-template <int RB, int DH>
+// RB = code blocks of 32 (rank <= 32*RB); DH = head_dim (64 or 128, used with deRoPE);
+// DEROPE = key jobs; MU = every job of the launch has an offset.
+template <int RB, int DH, bool DEROPE, bool MU>
 __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
+  constexpr int kMuBlocks = (RB + 3) / 4;  // offset blocks per wave (waves past RB idle)
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   uint16_t* Es = lds;                               // [2][RB*32][kLdc]
   uint16_t* mus = lds + 2 * RB * 32 * kLdc;         // [K] (deRoPE'd-space offset)
+  float* emu = reinterpret_cast<float*>(mus + (MU ? p.jobs[0].k : 0));  // [RB*32]: E mu
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -52,15 +60,14 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   const int64_t M = p.m;
   const int64_t row = static_cast<int64_t>(unit - job.tile_begin) * 128 + wave * 32 + (lane & 31);
   const bool valid = row < M;
-  const bool derope = (job.flags & kDeropeIn) != 0;
-  const bool sub_mu = (job.flags & kVecIn) != 0 && job.vec != nullptr;
+  constexpr bool derope = DEROPE;
   const uint16_t* X = static_cast<const uint16_t*>(job.a);
   const uint16_t* E = static_cast<const uint16_t*>(job.b);
   const uint16_t* mu = static_cast<const uint16_t*>(job.vec);
   const int nchunks = K / kChunk;
 
   // offsets -> LDS (whole row width)
-  if (sub_mu) {
+  if (MU) {
     for (int q = tid; q < K / 8; q += kThreads)
       *reinterpret_cast<uint4*>(mus + 8 * q) = *reinterpret_cast<const uint4*>(mu + 8 * q);
   }
@@ -98,11 +105,15 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       dst[s] = *reinterpret_cast<const uint4*>(xrow + c * kChunk + chunk_col<DH>(s, h, derope));
   };
 
-  f32x16 acc[RB];
+  f32x16 acc[RB], accm[kMuBlocks];
 #pragma unroll
   for (int b = 0; b < RB; ++b)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMuBlocks; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) accm[i][e] = 0.f;
 
   stage_weights(0, 0);
   load_x(0, xc);
@@ -115,38 +126,24 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       stage_weights(c + 1, buf ^ 1);
       load_x(c + 1, xn);
     }
-    // B operands, one (first half, second half) pair of k-steps at a time: deRoPE and offset in
-    // fp32, one bf16 rounding, then the MFMAs of both steps.
+    // B operands, one (first half, second half) pair of k-steps at a time: deRoPE in fp32 and one
+    // bf16 rounding (keys), or the loaded values themselves, then the MFMAs of both steps.
     const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
 #pragma unroll
     for (int s = 0; s < 8; s += 2) {
       bf16x8 bu, bv;
-      if (derope || sub_mu) {
+      if constexpr (DEROPE) {
         float u[8], v[8];
         unpack8(xc[s], u);
         unpack8(xc[s + 1], v);
-        const int cu = c * kChunk + chunk_col<DH>(s, h, derope);
-        const int cv = c * kChunk + chunk_col<DH>(s + 1, h, derope);
-        if (derope) {
-          constexpr int spH = DH / 16;
-          const int o = (s % spH) >> 1;
+        constexpr int spH = DH / 16;
+        const int o = (s % spH) >> 1;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float cc = cs_c[o][e], sn = cs_s[o][e];
-            const float a = u[e], b = v[e];
-            u[e] = a * cc + b * sn;
-            v[e] = b * cc - a * sn;
-          }
-        }
-        if (sub_mu) {
-          float mu_u[8], mu_v[8];
-          unpack8(*reinterpret_cast<const uint4*>(mus + cu), mu_u);
-          unpack8(*reinterpret_cast<const uint4*>(mus + cv), mu_v);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            u[e] -= mu_u[e];
-            v[e] -= mu_v[e];
-          }
+        for (int e = 0; e < 8; ++e) {
+          const float cc = cs_c[o][e], sn = cs_s[o][e];
+          const float a = u[e], b = v[e];
+          u[e] = a * cc + b * sn;
+          v[e] = b * cc - a * sn;
         }
         bu = __builtin_bit_cast(bf16x8, pack8(u));
         bv = __builtin_bit_cast(bf16x8, pack8(v));
@@ -165,6 +162,21 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
         const bf16x8 ae = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colv);
         acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
       }
+      if constexpr (MU) {
+        // E mu for this wave's offset blocks: mu (same columns as the inputs) in every B column
+        const bf16x8 mu_u = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colu);
+        const bf16x8 mu_v = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colv);
+#pragma unroll
+        for (int i = 0; i < kMuBlocks; ++i) {
+          const int b = wave + 4 * i;
+          if (b < RB) {
+            const bf16x8 au = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colu);
+            const bf16x8 av = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colv);
+            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(au, mu_u, accm[i], 0, 0, 0);
+            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, mu_v, accm[i], 0, 0, 0);
+          }
+        }
+      }
     }
     wait_vmem();
     __syncthreads();
@@ -172,6 +184,22 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
     for (int s = 0; s < 8; ++s) xc[s] = xn[s];
   }
 
+  if constexpr (MU) {
+    // every B column of the offset product is the same: lanes 0 and 32 publish their 16 values
+#pragma unroll
+    for (int i = 0; i < kMuBlocks; ++i) {
+      const int b = wave + 4 * i;
+      if (b < RB && (lane & 31) == 0) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) emu[32 * b + 16 * h + e] = accm[i][e];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < RB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[b][e] -= emu[32 * b + 16 * h + e];
+  }
   if (!valid) return;
   // lane holds, for block b, code columns 32*b + 16*h + (0..15) of its row
   uint16_t* Zo = static_cast<uint16_t*>(job.c) + row * R;
@@ -188,15 +216,25 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   }
 }
 
-template <int RB>
+template <int RB, bool DEROPE, bool MU>
 hipError_t launch_rb(int head_dim, const GemmParams& p, size_t lds, hipStream_t stream) {
   if (head_dim == 128)
-    hipLaunchKernelGGL((encode_bf16_kernel<RB, 128>), dim3(p.total_tiles), dim3(kThreads), lds,
-                       stream, p);
+    hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU>), dim3(p.total_tiles),
+                       dim3(kThreads), lds, stream, p);
   else
-    hipLaunchKernelGGL((encode_bf16_kernel<RB, 64>), dim3(p.total_tiles), dim3(kThreads), lds,
-                       stream, p);
+    hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU>), dim3(p.total_tiles),
+                       dim3(kThreads), lds, stream, p);
   return hipGetLastError();
+}
+
+template <int RB>
+hipError_t launch_kind(bool derope, bool mu, int head_dim, const GemmParams& p, size_t lds,
+                       hipStream_t stream) {
+  if (derope)
+    return mu ? launch_rb<RB, true, true>(head_dim, p, lds, stream)
+              : launch_rb<RB, true, false>(head_dim, p, lds, stream);
+  return mu ? launch_rb<RB, false, true>(head_dim, p, lds, stream)
+            : launch_rb<RB, false, false>(head_dim, p, lds, stream);
 }
 
 }  // namespace
@@ -207,22 +245,31 @@ int encode_code_blocks(int max_rank) {
   return rb <= 2 ? 2 : (rb <= 4 ? 4 : 8);
 }
 
-size_t encode_bf16_lds_bytes(int code_blocks, int k) {
-  return static_cast<size_t>(2) * code_blocks * 32 * kLdc * 2 + static_cast<size_t>(k) * 2;
+size_t encode_bf16_lds_bytes(int code_blocks, int k, bool mu) {
+  return static_cast<size_t>(2) * code_blocks * 32 * kLdc * 2 +
+         (mu ? static_cast<size_t>(k) * 2 + static_cast<size_t>(code_blocks) * 32 * 4 : 0);
 }
 
 hipError_t launch_encode_bf16(const GemmParams& p, hipStream_t stream) {
   if (p.total_tiles <= 0) return hipSuccess;
-  int max_r = 0, max_k = 0;
+  // every job of a launch has the same width, the same deRoPE flag and an offset either on every
+  // job or on none
+  const int k = p.jobs[0].k;
+  const bool derope = (p.jobs[0].flags & kDeropeIn) != 0;
+  const bool mu = (p.jobs[0].flags & kVecIn) != 0 && p.jobs[0].vec != nullptr;
+  int max_r = 0;
   for (int i = 0; i < p.n_jobs; ++i) {
-    max_r = p.jobs[i].n > max_r ? p.jobs[i].n : max_r;
-    max_k = p.jobs[i].k > max_k ? p.jobs[i].k : max_k;
+    const GemmJob& j = p.jobs[i];
+    if (j.k != k || ((j.flags & kDeropeIn) != 0) != derope ||
+        (((j.flags & kVecIn) != 0 && j.vec != nullptr) != mu))
+      return hipErrorInvalidValue;
+    max_r = j.n > max_r ? j.n : max_r;
   }
   const int rb = encode_code_blocks(max_r);
-  const size_t lds = encode_bf16_lds_bytes(rb, max_k);
-  if (rb == 2) return launch_rb<2>(p.head_dim, p, lds, stream);
-  if (rb == 4) return launch_rb<4>(p.head_dim, p, lds, stream);
-  return launch_rb<8>(p.head_dim, p, lds, stream);
+  const size_t lds = encode_bf16_lds_bytes(rb, k, mu);
+  if (rb == 2) return launch_kind<2>(derope, mu, p.head_dim, p, lds, stream);
+  if (rb == 4) return launch_kind<4>(derope, mu, p.head_dim, p, lds, stream);
+  return launch_kind<8>(derope, mu, p.head_dim, p, lds, stream);
 }
 
 }  // namespace scd
