@@ -51,10 +51,10 @@ def algorithmic(wl):
             "encode": (enc_b, enc_f), "kv_bytes": kv_bytes}
 
 
-KERNELS = {  # step -> (kernel symbol fragment, bound)
-    "encode": ("EncodeKV", "hbm"),
-    "reuse_decode": ("ReuseDecode", "hbm"),
-    "patch_kv": ("PatchKV", "mfma"),
+KERNELS = {  # step -> (kernel symbol of the bf16 path, bound)
+    "encode": ("encode_bf16_kernel", "hbm"),
+    "reuse_decode": ("reuse_decode_bf16_kernel", "hbm"),
+    "patch_kv": ("patch_kv_bf16_kernel", "mfma"),
 }
 
 
