@@ -34,18 +34,20 @@ def algorithmic(wl):
     eb, T, D, d, w, g = wl.elem_bytes, wl.n_tokens, wl.kv_width, wl.d_model, wl.w, wl.g
     dec_b = dec_f = pat_b = pat_f = enc_b = enc_f = 0
     for l in range(wl.n_layers):
-        r = wl.ranks[l]
         if wl.is_patch[l]:
+            r = wl.rank(l, "h")
             pat_b += (T * d + 2 * D * d + 2 * T * D + (2 * D if wl.with_bias else 0)) * eb
             pat_f += 2 * T * d * 2 * D
             enc_b += (T * d + r * d + T * r) * eb
             enc_f += 2 * T * d * r
         else:
             mu = w if wl.with_mu else 0
-            dec_b += 2 * (T * g * r + w * r + mu + T * D) * eb
-            dec_f += 2 * 2 * T * g * r * w
-            enc_b += 2 * (T * D + r * w + mu + T * g * r) * eb
-            enc_f += 2 * 2 * T * g * w * r
+            for br in ("k", "v"):
+                r = wl.rank(l, br)
+                dec_b += (T * g * r + w * r + mu + T * D) * eb
+                dec_f += 2 * T * g * r * w
+                enc_b += (T * D + r * w + mu + T * g * r) * eb
+                enc_f += 2 * T * g * w * r
     kv_bytes = wl.n_layers * 2 * T * D * eb
     return {"reuse_decode": (dec_b, dec_f), "patch_kv": (pat_b, pat_f),
             "encode": (enc_b, enc_f), "kv_bytes": kv_bytes}
@@ -169,7 +171,7 @@ def main():
     import paper_2606_07684_amd as scd
     from synth import workloads as W
 
-    wl = {w.name: w for w in (*W.CONFIGS, *W.TEST_WORKLOADS)}[args.workload]
+    wl = {w.name: w for w in (*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS)}[args.workload]
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
@@ -180,7 +182,7 @@ def main():
     inp = W.Inputs(wl, dev, decode=False)  # the decode consumes this step's encoded codes
     model = scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
                       head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
-                      is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.ranks, rank_h=wl.ranks,
+                      is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
                       basis_width=wl.w)
     cu = W.cu_seqlens(wl, dev) if wl.n_seqs > 1 or wl.pos0 is not None else None
     batch = scd.Batch(n_tokens=wl.n_tokens, cu_seqlens=cu, pos0=W.pos0(wl, dev))
@@ -265,7 +267,8 @@ def main():
         "config": {"workload": wl.name, "n_layers": wl.n_layers, "d_model": wl.d_model,
                    "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                    "n_tokens": wl.n_tokens, "n_requests": wl.n_seqs,
-                   "ranks": sorted(set(wl.ranks)), "patch_layers": list(wl.patch_layers),
+                   "ranks": sorted(set(wl.ranks)), "ranks_v": sorted(set(wl.rank_v)),
+                   "patch_layers": list(wl.patch_layers),
                    "basis_width": wl.w, "rope_theta": wl.rope_theta},
         "tokens_per_s": round(wl.n_tokens / (ms_per_step * 1e-3), 1),
         "phase_ms": {k: round(v, 4) for k, v in mean.items()},

@@ -113,7 +113,7 @@ def main():
     args = ap.parse_args()
 
     from synth import workloads as W
-    wl = {w.name: w for w in (*W.CONFIGS, *W.TEST_WORKLOADS)}[args.workload]
+    wl = {w.name: w for w in (*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS)}[args.workload]
     alg = bench.algorithmic(wl)
     digest = bench.source_digest()
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)

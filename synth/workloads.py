@@ -28,7 +28,7 @@ class Workload:
     n_kv_heads: int
     head_dim: int
     seq_lens: Tuple[int, ...]
-    ranks: Tuple[int, ...]            # per layer; r_K = r_V = r_H = ranks[l]
+    ranks: Tuple[int, ...]            # per layer: r_K = r_H = ranks[l], r_V too unless ranks_v
     patch_layers: Tuple[int, ...]
     rope_theta: float
     dtype: str                        # "f32" or "bf16"
@@ -37,6 +37,17 @@ class Workload:
     pos0: Optional[Tuple[int, ...]] = None
     with_bias: bool = False           # projection bias on the Patch branch (Qwen2-style)
     with_mu: bool = True
+    ranks_v: Optional[Tuple[int, ...]] = None  # per-layer r_V when it differs from r_K
+
+    def rank(self, layer: int, branch: str) -> int:
+        """Rank of one layer's branch ('k', 'v' or 'h')."""
+        if branch == "v" and self.ranks_v is not None:
+            return self.ranks_v[layer]
+        return self.ranks[layer]
+
+    @property
+    def rank_v(self) -> Tuple[int, ...]:
+        return self.ranks_v if self.ranks_v is not None else self.ranks
 
     @property
     def kv_width(self) -> int:
@@ -103,13 +114,19 @@ LLAMA3_70B = Workload("llama3_70b_bf16", 80, 8192, 8, 128, (16384,), (128,) * 80
 
 CONFIGS = (TINY_F32, LLAMA3_8B, QWEN2_7B, BATCHED, LLAMA3_70B)
 
+# The paper's head-shared basis (one basis of width d_h for all heads, Section 4.3.1) at the
+# Llama-3-8B shape, with different key and value ranks.
+LLAMA3_8B_HEAD_SHARED = LLAMA3_8B.replace(name="llama3_8b_head_shared_bf16", basis_width=128,
+                                          ranks=(64,) * 32, ranks_v=(32,) * 32)
+MODEL_SCALE_EXTRA = (LLAMA3_8B_HEAD_SHARED,)
+
 # Small workloads the oracle finishes in seconds that still span several tiles, ragged tails,
 # per-layer ranks, the head-shared basis, biases and non-zero first positions.
 SMALL_BF16 = Workload("small_bf16", 5, 384, 2, 128, (300, 77, 650), (64, 128, 32, 256, 96),
                       (1, 4), 5e5, "bf16", power_law=True)
 SMALL_HEAD_SHARED = Workload("small_head_shared_bf16", 3, 256, 4, 64, (129, 250), (32, 64, 48),
                              (2,), 1e4, "bf16", basis_width=64, with_bias=True,
-                             pos0=(5, 1000))
+                             pos0=(5, 1000), ranks_v=(64, 32, 48))
 SMALL_F32 = Workload("small_f32", 3, 320, 2, 64, (97, 200, 31), (16, 48, 32), (0,), 1e4, "f32",
                      with_bias=True)
 # d_model = 64: the Patch contraction is shorter than the copy pipeline is deep; one KV head.
@@ -155,7 +172,7 @@ def _cast(x: torch.Tensor, wl: Workload, device) -> torch.Tensor:
 
 def basis(wl: Workload, layer: int, branch: str, device="cpu"):
     """Reuse artifacts of one layer and branch: ``(W_enc [r, w], W_dec [w, r])`` with W_dec = Q."""
-    r = wl.ranks[layer]
+    r = wl.rank(layer, branch)
     q = torch.from_numpy(_full_basis(wl, layer, branch)[:, :r].copy())
     return _cast(q.T.contiguous(), wl, device), _cast(q, wl, device)
 
@@ -170,7 +187,7 @@ def mu(wl: Workload, layer: int, branch: str, device="cpu"):
 def codes(wl: Workload, layer: int, branch: str, device="cpu") -> torch.Tensor:
     """Reuse codes ``[T*g, r]``: N(0,1), scaled per column by sigma_1..r when the spectrum is a
     power law (the projection of the synthetic signal onto its top-r directions)."""
-    r = wl.ranks[layer]
+    r = wl.rank(layer, branch)
     z = _randn(wl, layer, "codes_" + branch, (wl.n_tokens * wl.g, r), device)
     if wl.power_law:
         sig = torch.tensor(power_law_sigma(wl.w)[:r], dtype=torch.float32, device=device)
@@ -192,7 +209,7 @@ def kv_input(wl: Workload, layer: int, branch: str, device="cpu") -> torch.Tenso
         gmat = _randn(wl, layer, "signal_" + branch, (n, wl.w), device) * sig[None, :]
         x = gmat @ b.T
     else:
-        r = wl.ranks[layer]
+        r = wl.rank(layer, branch)
         c = _randn(wl, layer, "signal_" + branch, (n, r), device)
         x = c @ b[:, :r].T
     x = x + _randn(wl, layer, "noise_" + branch, (n, wl.w), device) * 0.1
@@ -306,7 +323,7 @@ def alloc_codes(wl: Workload, device):
         if wl.is_patch[l]:
             z_h[l] = torch.empty((wl.n_tokens, wl.ranks[l]), dtype=wl.torch_dtype, device=device)
         else:
-            for lst in (z_k, z_v):
-                lst[l] = torch.empty((wl.n_tokens * wl.g, wl.ranks[l]), dtype=wl.torch_dtype,
+            for lst, br in ((z_k, "k"), (z_v, "v")):
+                lst[l] = torch.empty((wl.n_tokens * wl.g, wl.rank(l, br)), dtype=wl.torch_dtype,
                                      device=device)
     return z_k, z_v, z_h

@@ -20,7 +20,7 @@ alloc_codes = W.alloc_codes
 def model_of(wl: W.Workload) -> scd.Model:
     return scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
                      head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
-                     is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.ranks, rank_h=wl.ranks,
+                     is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
                      basis_width=wl.w)
 
 

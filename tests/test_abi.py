@@ -171,17 +171,18 @@ def test_encode_and_patch_validation(lib):
     assert lib.scd_rope_table(ctypes.byref(m._c), 100, FAKE, need - 1, None) == WS
 
 
-@pytest.mark.parametrize("wl", [*W.CONFIGS, *W.TEST_WORKLOADS], ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS],
+                         ids=lambda w: w.name)
 def test_schedule_and_payload_match_oracle(wl):
     m = scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
                   head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
-                  is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.ranks, rank_h=wl.ranks,
+                  is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
                   basis_width=wl.w)
     reuse, patch = scd.scd_schedule(m)
     assert (reuse, patch) == O.schedule(wl.is_patch)
     total, offs = scd.scd_payload_bytes(m, wl.n_tokens)
     t2, o2 = O.payload_bytes(wl.is_patch, wl.n_tokens, wl.n_kv_heads, wl.head_dim, wl.w,
-                             wl.ranks, wl.ranks, wl.ranks, wl.elem_bytes)
+                             wl.ranks, wl.rank_v, wl.ranks, wl.elem_bytes)
     assert total == t2 and offs == o2
 
 

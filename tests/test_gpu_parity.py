@@ -126,8 +126,8 @@ def test_empty_batch_and_reuse_only():
     assert all(c.numel() == 0 for c in out_e["k_cache"])
 
 
-@pytest.mark.parametrize("wl", [W.LLAMA3_8B, W.QWEN2_7B, W.BATCHED, W.LLAMA3_70B],
-                         ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [W.LLAMA3_8B, W.QWEN2_7B, W.BATCHED, W.LLAMA3_70B,
+                                *W.MODEL_SCALE_EXTRA], ids=lambda w: w.name)
 def test_full_size_sampled(wl):
     """Full-size configurations, launched exactly as the benchmark launches them; the oracle checks
     sampled token rows (random rows, request boundaries and tile edges) of every layer."""
