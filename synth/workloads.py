@@ -131,7 +131,20 @@ SMALL_F32 = Workload("small_f32", 3, 320, 2, 64, (97, 200, 31), (16, 48, 32), (0
                      with_bias=True)
 # d_model = 64: the Patch contraction is shorter than the copy pipeline is deep; one KV head.
 SMALL_NARROW = Workload("small_narrow_bf16", 2, 64, 1, 128, (200, 57), (64, 32), (1,), 1e4, "bf16")
-TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW)
+# Degenerate batches: empty and single-token requests between others, the smallest rank (16, which
+# the bf16 decode hands to the generic kernel) next to 32, the head-shared basis, and start positions
+# near the top of a long RoPE table.
+SMALL_DEGENERATE = Workload("small_degenerate_bf16", 3, 128, 2, 64, (1, 0, 5, 1, 0, 130),
+                            (16, 32, 32), (1,), 1e6, "bf16", basis_width=64,
+                            pos0=(30000, 7, 0, 29990, 1, 5), ranks_v=(32, 32, 16))
+# Full rank: r = w = 256 (the largest rank a launch takes) on the bf16 kernels.
+SMALL_FULL_RANK = Workload("small_full_rank_bf16", 2, 256, 2, 128, (300, 33), (256, 256), (1,),
+                           5e5, "bf16")
+# More requests than the bf16 decode stages in LDS (256): the generic kernel takes the batch.
+SMALL_MANY_REQUESTS = Workload("small_many_requests_bf16", 2, 128, 2, 64, _ragged_lengths(5, 300, 0, 3),
+                               (32, 32), (1,), 1e4, "bf16")
+TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
+                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS)
 
 
 # --------------------------------------------------------------------------------------------

@@ -143,3 +143,24 @@ def test_full_size_sampled(wl):
             assert bool(torch.isfinite(c).all())
     del out, inp
     torch.cuda.empty_cache()
+
+
+def test_full_rank_round_trip_reproduces_the_input():
+    """r = w with an orthonormal basis (W_enc = Q^T, W_dec = Q) and the same offset on both sides:
+    decoding the GPU's own codes returns the producer's K and V (keys through deRoPE then RoPE), up
+    to the bf16 roundings of the codes and the output (Section 4.3.2)."""
+    wl = W.SMALL_FULL_RANK
+    inp = U.Inputs(wl, "cuda")
+    rope = _rope_for(wl)
+    enc = U.run_gpu(wl, inp, rope, which=("encode",))
+    model, batch = U.model_of(wl), U.batch_of(wl, torch.device("cuda"))
+    kc, vc = U.alloc_caches(wl, torch.device("cuda"))
+    scd.scd_reuse_decode(model, batch, rope, enc["z_k"], enc["z_v"], inp.w_dec_k, inp.w_dec_v,
+                         inp.mu_k, inp.mu_v, kc, vc)
+    torch.cuda.synchronize()
+    worst = 0.0
+    for l in inp.R:
+        for got, want in ((kc[l], inp.k_in[l]), (vc[l], inp.v_in[l])):
+            worst = max(worst, U.max_abs_rel(U.f64(got), U.f64(want)))
+    print(f"full-rank round trip, worst max-abs-rel {worst:.2e}", flush=True)
+    assert worst <= U.TOL["bf16"]
