@@ -134,5 +134,12 @@ __device__ inline void dma_rows(uint16_t* dst, int nrows, int chunks, int stride
 // Wait until every vector-memory operation of this wave (loads, stores, LDS DMA) has completed.
 __device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// Workgroup barrier that waits for this wave's LDS accesses only.  __syncthreads() carries a
+// workgroup fence, which the compiler implements by also draining every vector-memory load and
+// store in flight (so no copy or store can stay outstanding across it).  Wait explicitly
+// (s_waitcnt) for the vector-memory operations a barrier publishes.  The memory clobber keeps the
+// compiler from moving memory accesses across the barrier.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 }  // namespace dev
 }  // namespace scd

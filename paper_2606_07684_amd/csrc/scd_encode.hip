@@ -26,7 +26,7 @@ using namespace dev;
 
 constexpr int kThreads = 256;
 constexpr int kChunk = 128;          // input columns per chunk
-constexpr int kLdc = kChunk + 8;     // padded LDS row of a weight chunk (elements)
+constexpr int kLdcPad = kChunk + 8;  // padded LDS row of a weight chunk (elements)
 
 // Column (within a chunk) that lane half h supplies to MFMA k-step s (0..7).  With deRoPE, even
 // steps take the first half of a head and odd steps the matching second half:
@@ -41,10 +41,14 @@ __device__ constexpr int chunk_col(int s, int h, bool derope) {
 
 // RB = code blocks of 32 (rank <= 32*RB); DH = head_dim (64 or 128, used with deRoPE);
 // DEROPE = key jobs; MU = every job of the launch has an offset.
-template <int RB, int DH, bool DEROPE, bool MU>
+template <int RB, int DH, bool DEROPE, bool MU, int DEPTH>
 __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   constexpr int kMuBlocks = (RB + 3) / 4;  // offset blocks per wave (waves past RB idle)
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  // Weight chunk rows: padded (DEPTH 1) or swizzled without padding (DEPTH 2, where every wave must
+  // issue a fixed number of copies so its waits can be counted).
+  constexpr bool kSwz = DEPTH == 2;
+  constexpr int kLdc = kSwz ? kChunk : kLdcPad;
   uint16_t* Es = lds;                               // [2][RB*32][kLdc]
   uint16_t* mus = lds + 2 * RB * 32 * kLdc;         // [K] (deRoPE'd-space offset)
   float* emu = reinterpret_cast<float*>(mus + (MU ? p.jobs[0].k : 0));  // [RB*32]: E mu
@@ -73,12 +77,33 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   }
 
   // weight chunk c -> LDS buffer b, asynchronously; code rows beyond R read row 0 and only feed
-  // accumulator blocks that are never stored
+  // accumulator blocks that are never stored.  Swizzled: RB*32 rows x 16 chunks of 16 bytes, chunk
+  // q of row rho at q ^ (rho & 7), exactly 2*RB copies per wave.  Padded: rows of 17 slots, the
+  // pad slot masked off.
+  constexpr int kEDma = RB * 32 * (kChunk / 8) / kThreads;
   auto stage_weights = [&](int c, int b) {
-    dma_rows(Es + b * RB * 32 * kLdc, RB * 32, kChunk / 8, kLdc / 8, wave, 4, lane, [&](int rho) {
-      const int r = row_of_lds(rho);
-      return E + static_cast<int64_t>(r < R ? r : 0) * K + c * kChunk;
-    });
+    uint16_t* dst = Es + b * RB * 32 * kLdc;
+    if constexpr (kSwz) {
+#pragma unroll
+      for (int j = 0; j < kEDma; ++j) {
+        const int slot = (4 * j + wave) * 64 + lane;
+        const int rho = slot >> 4, q = (slot & 15) ^ (rho & 7);
+        const int r = row_of_lds(rho);
+        __builtin_amdgcn_global_load_lds(
+            E + static_cast<int64_t>(r < R ? r : 0) * K + c * kChunk + 8 * q,
+            (lds_void_t)(dst + 8 * ((4 * j + wave) * 64)), 16, 0, 0);
+      }
+    } else {
+      dma_rows(dst, RB * 32, kChunk / 8, kLdc / 8, wave, 4, lane, [&](int rho) {
+        const int r = row_of_lds(rho);
+        return E + static_cast<int64_t>(r < R ? r : 0) * K + c * kChunk;
+      });
+    }
+  };
+  // MFMA A fragment of weight block b at chunk column col (a multiple of 8) for this lane's row
+  auto efrag = [&](const uint16_t* eb, int b, int col) {
+    const int q = kSwz ? ((col >> 3) ^ (lane & 7)) : (col >> 3);
+    return *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + 8 * q);
   };
 
   // this lane's rotation factors for every pair index it touches: i = 16*o + 8*h + e
@@ -97,7 +122,6 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   }
 
   const uint16_t* xrow = X + (valid ? row : 0) * K;
-  uint4 xc[8], xn[8];
   // rows past the end read row 0 (always in bounds); their codes are never stored
   auto load_x = [&](int c, uint4* dst) {
 #pragma unroll
@@ -115,10 +139,12 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) accm[i][e] = 0.f;
 
+  if constexpr (DEPTH == 1) {
+  uint4 xc[8], xn[8];
   stage_weights(0, 0);
   load_x(0, xc);
   wait_vmem();
-  __syncthreads();
+  lds_barrier();
 
   for (int c = 0; c < nchunks; ++c) {
     const int buf = c & 1;
@@ -154,12 +180,12 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       const int colu = chunk_col<DH>(s, h, derope), colv = chunk_col<DH>(s + 1, h, derope);
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colu);
+        const bf16x8 ae = efrag(eb, b, colu);
         acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bu, acc[b], 0, 0, 0);
       }
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colv);
+        const bf16x8 ae = efrag(eb, b, colv);
         acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
       }
       if constexpr (MU) {
@@ -170,8 +196,8 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
         for (int i = 0; i < kMuBlocks; ++i) {
           const int b = wave + 4 * i;
           if (b < RB) {
-            const bf16x8 au = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colu);
-            const bf16x8 av = *reinterpret_cast<const bf16x8*>(eb + b * 32 * kLdc + colv);
+            const bf16x8 au = efrag(eb, b, colu);
+            const bf16x8 av = efrag(eb, b, colv);
             accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(au, mu_u, accm[i], 0, 0, 0);
             accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, mu_v, accm[i], 0, 0, 0);
           }
@@ -179,11 +205,91 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       }
     }
     wait_vmem();
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int s = 0; s < 8; ++s) xc[s] = xn[s];
   }
 
+  } else {
+  // inputs two chunks ahead in a ring of three register sets; the chunk loop is unrolled by three
+  // so every set keeps its registers (no copies of registers whose loads are in flight)
+  constexpr int kWait8 = 8 | (0x7 << 4) | (0xF << 8);  // at most the 8 input loads of chunk c + 2
+  uint4 x0[8], x1[8], x2[8];
+  stage_weights(0, 0);
+  load_x(0, x0);
+  load_x(nchunks > 1 ? 1 : 0, x1);
+  __builtin_amdgcn_s_waitcnt(kWait8);
+  lds_barrier();
+  auto step = [&](int c, uint4 (&xcur)[8], uint4 (&xfar)[8]) {
+    const int buf = c & 1;
+    // weights of chunk c + 1 and inputs of chunk c + 2 (past the end: in-bounds re-loads that are
+    // never used, so every chunk issues the same loads)
+    stage_weights(c + 1 < nchunks ? c + 1 : c, buf ^ 1);
+    load_x(c + 2 < nchunks ? c + 2 : c, xfar);
+    // B operands, one (first half, second half) pair of k-steps at a time: deRoPE in fp32 and one
+    // bf16 rounding (keys), or the loaded values themselves, then the MFMAs of both steps.
+    const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
+#pragma unroll
+    for (int s = 0; s < 8; s += 2) {
+      bf16x8 bu, bv;
+      if constexpr (DEROPE) {
+        float u[8], v[8];
+        unpack8(xcur[s], u);
+        unpack8(xcur[s + 1], v);
+        constexpr int spH = DH / 16;
+        const int o = (s % spH) >> 1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float cc = cs_c[o][e], sn = cs_s[o][e];
+          const float a = u[e], b = v[e];
+          u[e] = a * cc + b * sn;
+          v[e] = b * cc - a * sn;
+        }
+        bu = __builtin_bit_cast(bf16x8, pack8(u));
+        bv = __builtin_bit_cast(bf16x8, pack8(v));
+      } else {
+        bu = __builtin_bit_cast(bf16x8, xcur[s]);
+        bv = __builtin_bit_cast(bf16x8, xcur[s + 1]);
+      }
+      const int colu = chunk_col<DH>(s, h, derope), colv = chunk_col<DH>(s + 1, h, derope);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        const bf16x8 ae = efrag(eb, b, colu);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bu, acc[b], 0, 0, 0);
+      }
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        const bf16x8 ae = efrag(eb, b, colv);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
+      }
+      if constexpr (MU) {
+        // E mu for this wave's offset blocks: mu (same columns as the inputs) in every B column
+        const bf16x8 mu_u = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colu);
+        const bf16x8 mu_v = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colv);
+#pragma unroll
+        for (int i = 0; i < kMuBlocks; ++i) {
+          const int b = wave + 4 * i;
+          if (b < RB) {
+            const bf16x8 au = efrag(eb, b, colu);
+            const bf16x8 av = efrag(eb, b, colv);
+            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(au, mu_u, accm[i], 0, 0, 0);
+            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, mu_v, accm[i], 0, 0, 0);
+          }
+        }
+      }
+    }
+    // chunk c + 1's weights and inputs have landed once only chunk c + 2's 8 input loads are
+    // pending; the barrier makes that true for every wave and retires this chunk's LDS reads
+    __builtin_amdgcn_s_waitcnt(kWait8);
+    lds_barrier();
+  };
+  for (int c = 0; c < nchunks; c += 3) {
+    step(c, x0, x2);
+    if (c + 1 < nchunks) step(c + 1, x1, x0);
+    if (c + 2 < nchunks) step(c + 2, x2, x1);
+  }
+  wait_vmem();
+  }
   if constexpr (MU) {
     // every B column of the offset product is the same: lanes 0 and 32 publish their 16 values
 #pragma unroll
@@ -218,14 +324,26 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 
 template <int RB, bool DEROPE, bool MU>
 hipError_t launch_rb(int head_dim, const GemmParams& p, size_t lds, hipStream_t stream) {
-  if (head_dim == 128)
-    hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU>), dim3(p.total_tiles),
-                       dim3(kThreads), lds, stream, p);
-  else
-    hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU>), dim3(p.total_tiles),
-                       dim3(kThreads), lds, stream, p);
+  // long rows (many chunks per unit, few units) prefetch two chunks ahead
+  const bool deep = !DEROPE && !MU && p.jobs[0].k >= 2048;
+  if (head_dim == 128) {
+    if (deep)
+      hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 2>), dim3(p.total_tiles),
+                         dim3(kThreads), lds, stream, p);
+    else
+      hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 1>), dim3(p.total_tiles),
+                         dim3(kThreads), lds, stream, p);
+  } else {
+    if (deep)
+      hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 2>), dim3(p.total_tiles),
+                         dim3(kThreads), lds, stream, p);
+    else
+      hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 1>), dim3(p.total_tiles),
+                         dim3(kThreads), lds, stream, p);
+  }
   return hipGetLastError();
 }
+
 
 template <int RB>
 hipError_t launch_kind(bool derope, bool mu, int head_dim, const GemmParams& p, size_t lds,
@@ -246,7 +364,7 @@ int encode_code_blocks(int max_rank) {
 }
 
 size_t encode_bf16_lds_bytes(int code_blocks, int k, bool mu) {
-  return static_cast<size_t>(2) * code_blocks * 32 * kLdc * 2 +
+  return static_cast<size_t>(2) * code_blocks * 32 * kLdcPad * 2 +
          (mu ? static_cast<size_t>(k) * 2 + static_cast<size_t>(code_blocks) * 32 * 4 : 0);
 }
 

@@ -170,7 +170,7 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
 #pragma unroll
   for (int st = 0; st < kStages - 1; ++st) stage(clamp(st), st);
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
-  __builtin_amdgcn_s_barrier();
+  lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
   const uint16_t* hrow = smem + kBN * kLDK + (wt * 128 + lr) * kLDK;
   bf16x8 a0[4], b0[4], a1[4], b1[4];
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
     // its reads of stage kc are complete once no LDS access is pending; the barrier makes both
     // true for every wave.  (A plain s_barrier: a fenced one would wait for every copy in flight.)
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
-    __builtin_amdgcn_s_barrier();
+    lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
     // The last slice's MFMAs, with the next stage's slice-0 reads between them.
     mma(a1, b1);
