@@ -58,6 +58,9 @@ __device__ __forceinline__ void decode_unit(const GemmParams& p, const LdsBatch&
   for (int tile = 0; tile < c.n_tiles; ++tile) {
     // keep the compiler from hoisting loop-invariant LDS reads into registers across tiles
     asm volatile("" ::: "memory");
+    // start every tile with the other waves of the workgroup, so that their stores go to
+    // neighbouring rows at the same time (lone waves drifting apart cost DRAM locality)
+    if (tile > 0) wave_lockstep();
     const int64_t row = c.row_first + static_cast<int64_t>(tile) * kTT + wave * 32 + (lane & 31);
     if (!FULL && c.row_first + static_cast<int64_t>(tile) * kTT >= c.M) break;  // uniform
 

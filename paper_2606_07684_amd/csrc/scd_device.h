@@ -141,5 +141,11 @@ __device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // compiler from moving memory accesses across the barrier.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// Workgroup barrier with no wait at all: it only brings the waves to the same point of their
+// instruction streams (loads and stores in flight stay in flight).  Store-bound loops use it to
+// keep the waves of a workgroup writing neighbouring addresses at the same time, which HBM
+// serves better than the scattered stream of waves that drifted apart.
+__device__ inline void wave_lockstep() { asm volatile("s_barrier" ::: "memory"); }
+
 }  // namespace dev
 }  // namespace scd
