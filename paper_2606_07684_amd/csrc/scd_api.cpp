@@ -432,9 +432,7 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
        })) {
     const int nhg = scd::decode_channel_groups(grp[0].k, w);
     scd::GemmParams gp = base;
-    // four tiles per workgroup when every layer-branch still spans two such units
-    gp.tiles_per_unit = T * g >= 8 * scd::kDecodeTileRows ? 4 : 1;
-    JobPacker jp(gp, gp.tiles_per_unit * scd::kDecodeTileRows, 128 * nhg);
+    JobPacker jp(gp, scd::decode_tile_rows(nhg), 128 * nhg);
     for (const auto& j : grp) jp.add(j);
     for (const auto& lp : jp.build()) {
       const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream);

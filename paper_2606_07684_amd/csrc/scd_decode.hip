@@ -24,25 +24,26 @@ namespace {
 
 using namespace dev;
 
-constexpr int kThreads = 256;
-constexpr int kTT = kDecodeTileRows;  // rows per tile (4 waves x 32)
+// Waves per workgroup: 4 for chunks of 128 or 256 channels (two workgroups per CU), 8 for chunks of
+// 512 channels (one workgroup per CU; its basis chunk fills most of the LDS).  A tile is 32 rows
+// per wave.
+constexpr int waves_for(int nhg) { return nhg == 4 ? 8 : 4; }
 constexpr int kDRows = kRopeMinRows;  // in-half offsets d = 0..15
 
-// Per-workgroup context of the decode kernel.
+// The layer-branch a workgroup is working on.
 struct DecodeCtx {
   const uint16_t* Z;     // codes [M, K]
   uint16_t* C;           // output rows [M, N]
   int64_t M;
   int N, n0;             // row width, first channel of the chunk
-  int64_t row_first;     // first row of the unit
-  int n_tiles;           // tiles of the unit
 };
 
-// KCH = rank / 32, NHG = channel groups of 128, DH = head_dim, ROPE = key jobs, FULL = every
-// tile of the unit is complete (only the last unit of a layer-branch can be partial).
-template <int KCH, int NHG, int DH, bool ROPE, bool FULL>
-__device__ __forceinline__ void decode_unit(const GemmParams& p, const LdsBatch& lb,
-                                            const DecodeCtx& c, const uint16_t* Fs,
+// One tile: the TT rows from row t0 of the current layer-branch, channels [n0, n0 + 128 NHG).
+// KCH = rank / 32, NHG = channel groups of 128, DH = head_dim, ROPE = key jobs, FULL = all TT
+// rows exist (only the last tile of a layer-branch can be partial).
+template <int KCH, int NHG, int DH, bool ROPE, bool FULL, int TT = 32 * waves_for(NHG)>
+__device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch& lb,
+                                            const DecodeCtx& c, int64_t t0, const uint16_t* Fs,
                                             const uint16_t* mus, const float2* dtab, int lane,
                                             int wave) {
   constexpr int K = 32 * KCH;
@@ -54,15 +55,8 @@ __device__ __forceinline__ void decode_unit(const GemmParams& p, const LdsBatch&
   const int hl = 16 * h;
   const int d = lane & 15;
 
-#pragma unroll 1
-  for (int tile = 0; tile < c.n_tiles; ++tile) {
-    // keep the compiler from hoisting loop-invariant LDS reads into registers across tiles
-    asm volatile("" ::: "memory");
-    // start every tile with the other waves of the workgroup, so that their stores go to
-    // neighbouring rows at the same time (lone waves drifting apart cost DRAM locality)
-    if (tile > 0) wave_lockstep();
-    const int64_t row = c.row_first + static_cast<int64_t>(tile) * kTT + wave * 32 + (lane & 31);
-    if (!FULL && c.row_first + static_cast<int64_t>(tile) * kTT >= c.M) break;  // uniform
+  {
+    const int64_t row = t0 + wave * 32 + (lane & 31);
 
     // codes: lane half h holds k = 16i + 8h + (0..7); rows past the end read row 0 (in bounds,
     // never stored)
@@ -149,8 +143,17 @@ __device__ __forceinline__ void decode_unit(const GemmParams& p, const LdsBatch&
   }
 }
 
+// Work decomposition: every launch covers one branch (keys or values) of every layer of one rank.
+// The row tiles of all its layer-branches form one list (layer-major).  Workgroup u works on
+// channel chunk u % n_nc of a contiguous, balanced share of that list (all its chunk siblings
+// take the same share, on the same XCD), so a launch sized to the machine runs as one round
+// with every workgroup busy to the end.  A workgroup stages a layer-branch's basis chunk once,
+// when its share enters that layer-branch.
 template <int KCH, int NHG, int DH, bool ROPE>
-__global__ __launch_bounds__(kThreads, 2) void reuse_decode_bf16_kernel(GemmParams p) {
+__global__ __launch_bounds__(64 * waves_for(NHG), 2) void reuse_decode_bf16_kernel(GemmParams p) {
+  constexpr int kWaves = waves_for(NHG);
+  constexpr int kThreads = 64 * kWaves;
+  constexpr int kTT = 32 * kWaves;
   constexpr int CN = 128 * NHG;
   constexpr int K = 32 * KCH;
   constexpr int LDK = K + 8;
@@ -166,34 +169,18 @@ __global__ __launch_bounds__(kThreads, 2) void reuse_decode_bf16_kernel(GemmPara
   const int lane = tid & 63;
   const int wave = tid >> 6;
 
-  // unit -> (job, row group, channel chunk); channel chunk fastest
-  const int unit = xcd_remap(blockIdx.x, gridDim.x);
-  const GemmJob job = p.jobs[job_of(p, unit)];
-  const int n_nc = job.n / CN;
-  const int local = unit - job.tile_begin;
-  const int nc = local % n_nc, tg = local / n_nc;
-  const int tiles_per_unit = p.tiles_per_unit;
+  // workgroup -> (share of the row-tile list, channel chunk); chunk fastest
+  const int u = xcd_remap(blockIdx.x, gridDim.x);
+  const int N = p.jobs[0].n;  // every job of a launch has the basis width
+  const int n_nc = N / CN;
+  const int n_share = gridDim.x / n_nc;
+  const int share = u / n_nc, nc = u % n_nc;
+  const int64_t M = p.m;
+  const int64_t tiles_per_job = (M + kTT - 1) / kTT;
+  const int64_t n_tiles = tiles_per_job * p.n_jobs;
+  const int64_t first = n_tiles * share / n_share, last = n_tiles * (share + 1) / n_share;
 
-  DecodeCtx c;
-  c.Z = static_cast<const uint16_t*>(job.a);
-  c.C = static_cast<uint16_t*>(job.c);
-  c.M = p.m;
-  c.N = job.n;
-  c.n0 = nc * CN;
-  c.row_first = static_cast<int64_t>(tg) * tiles_per_unit * kTT;
-  c.n_tiles = tiles_per_unit;
-  const uint16_t* F = static_cast<const uint16_t*>(job.b);
-  const uint16_t* mu = static_cast<const uint16_t*>(job.vec);
-  const bool add_mu = (job.flags & kVecOut) != 0 && mu != nullptr;
-
-  // basis chunk -> LDS (asynchronous); offsets, in-half RoPE factors and the batch -> LDS
-  dma_rows(Fs, CN, K / 8, LDK / 8, wave, 4, lane,
-           [&](int rho) { return F + static_cast<int64_t>(c.n0 + row_of_lds(rho)) * K; });
-  if (tid < CN / 8) {
-    const uint4 v = add_mu ? *reinterpret_cast<const uint4*>(mu + c.n0 + 8 * tid)
-                           : make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4*>(mus + 8 * tid) = v;
-  }
+  // in-half RoPE factors and the batch -> LDS (once)
   if (ROPE) {
     for (int i = tid; i < kDRows * HALF; i += kThreads) {
       const int r = i / HALF, k = i % HALF;
@@ -201,36 +188,107 @@ __global__ __launch_bounds__(kThreads, 2) void reuse_decode_bf16_kernel(GemmPara
     }
   }
   stage_batch(p, lbatch, tid, kThreads);
-  wait_vmem();
-  __syncthreads();
 
-  if (c.row_first + static_cast<int64_t>(tiles_per_unit) * kTT <= c.M)
-    decode_unit<KCH, NHG, DH, ROPE, true>(p, lbatch, c, Fs, mus, dtab, lane, wave);
-  else
-    decode_unit<KCH, NHG, DH, ROPE, false>(p, lbatch, c, Fs, mus, dtab, lane, wave);
+  DecodeCtx c;
+  c.M = M;
+  c.N = N;
+  c.n0 = nc * CN;
+  int cur = -1;
+#pragma unroll 1
+  for (int64_t gt = first; gt < last; ++gt) {
+    // keep the compiler from hoisting the loop-invariant basis reads into registers across tiles
+    asm volatile("" ::: "memory");
+    const int j = static_cast<int>(gt / tiles_per_job);
+    const int64_t t0 = (gt - static_cast<int64_t>(j) * tiles_per_job) * kTT;
+    if (j != cur) {
+      // entering a layer-branch: its basis chunk (rows permuted so each MFMA accumulator lane
+      // ends with 16 consecutive channels of one row) and offsets -> LDS
+      if (cur >= 0) lds_barrier();  // every wave is done reading the previous basis
+      const GemmJob& job = p.jobs[j];
+      c.Z = static_cast<const uint16_t*>(job.a);
+      c.C = static_cast<uint16_t*>(job.c);
+      const uint16_t* F = static_cast<const uint16_t*>(job.b);
+      const uint16_t* mu = static_cast<const uint16_t*>(job.vec);
+      const bool add_mu = (job.flags & kVecOut) != 0 && mu != nullptr;
+      dma_rows(Fs, CN, K / 8, LDK / 8, wave, kWaves, lane,
+               [&](int rho) { return F + static_cast<int64_t>(c.n0 + row_of_lds(rho)) * K; });
+      if (tid < CN / 8) {
+        const uint4 v = add_mu ? *reinterpret_cast<const uint4*>(mu + c.n0 + 8 * tid)
+                               : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(mus + 8 * tid) = v;
+      }
+      wait_vmem();
+      __syncthreads();
+      cur = j;
+    } else {
+      // start every tile with the other waves of the workgroup, so that their stores go to
+      // neighbouring rows at the same time (lone waves drifting apart cost DRAM locality)
+      wave_lockstep();
+    }
+    // one bounds-checked body for full and partial tiles (a second copy of the loop body costs
+    // registers)
+    decode_tile<KCH, NHG, DH, ROPE, false>(p, lbatch, c, t0, Fs, mus, dtab, lane, wave);
+  }
 }
 
 template <int NHG, int DH, bool ROPE>
-hipError_t launch_kch(int kch, const GemmParams& p, size_t lds, hipStream_t stream) {
-  const dim3 grid(p.total_tiles), block(kThreads);
+hipError_t launch_kch(int kch, const GemmParams& p, int grid_size, size_t lds,
+                      hipStream_t stream) {
+  const dim3 grid(grid_size), block(64 * waves_for(NHG));
   switch (kch) {
 #define SCD_DECODE_CASE(KC)                                                                   \
   case KC:                                                                                    \
     hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), grid, block, lds, stream, \
                        p);                                                                    \
-    break;
+    return hipGetLastError();
     SCD_DECODE_CASE(1) SCD_DECODE_CASE(2) SCD_DECODE_CASE(3) SCD_DECODE_CASE(4)
-    SCD_DECODE_CASE(5) SCD_DECODE_CASE(6) SCD_DECODE_CASE(7) SCD_DECODE_CASE(8)
 #undef SCD_DECODE_CASE
-    default: return hipErrorInvalidValue;
+    default:
+      break;
   }
-  return hipGetLastError();
+  // ranks above 128 use one channel group per workgroup (decode_channel_groups)
+  if constexpr (NHG == 1) {
+    switch (kch) {
+#define SCD_DECODE_CASE(KC)                                                                   \
+  case KC:                                                                                    \
+    hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), grid, block, lds, stream, \
+                       p);                                                                    \
+    return hipGetLastError();
+      SCD_DECODE_CASE(5) SCD_DECODE_CASE(6) SCD_DECODE_CASE(7) SCD_DECODE_CASE(8)
+#undef SCD_DECODE_CASE
+      default:
+        break;
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 int decode_channel_groups(int rank, int basis_width) {
-  return (rank <= 128 && basis_width % 256 == 0) ? 2 : 1;
+  if (rank > 128) return 1;
+  return basis_width % 512 == 0 ? 4 : (basis_width % 256 == 0 ? 2 : 1);
+}
+
+int decode_tile_rows(int nhg) { return 32 * waves_for(nhg); }
+
+// Compute units of the current device (queried once per device).
+static hipError_t compute_units(int* out) {
+  static int cache[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && cache[dev] > 0) {
+    *out = cache[dev];
+    return hipSuccess;
+  }
+  int n = 0;
+  e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (n < 1) n = 1;
+  if (dev >= 0 && dev < 64) cache[dev] = n;
+  *out = n;
+  return hipSuccess;
 }
 
 size_t decode_bf16_lds_bytes(int nhg, int rank, int head_dim) {
@@ -246,17 +304,39 @@ hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream) 
   for (int i = 1; i < p.n_jobs; ++i)
     if (p.jobs[i].k != rank || ((p.jobs[i].flags & kRopeOut) != 0) != rope)
       return hipErrorInvalidValue;
-  if (rank % 32 != 0 || rank < 32 || rank > 256 || p.n_seqs > kMaxLdsSeqs ||
-      p.tiles_per_unit < 1)
+  const int cn = 128 * nhg;
+  if (rank % 32 != 0 || rank < 32 || rank > 256 || p.n_seqs > kMaxLdsSeqs || p.n_jobs < 1 ||
+      p.jobs[0].n % cn != 0)
     return hipErrorInvalidValue;
+  for (int i = 1; i < p.n_jobs; ++i)
+    if (p.jobs[i].n != p.jobs[0].n) return hipErrorInvalidValue;
   const size_t lds = decode_bf16_lds_bytes(nhg, rank, p.head_dim);
   const int kch = rank / 32;
+  // one round of workgroups: as many as the compute units hold at once (LDS and the two waves per
+  // SIMD the kernel is built for), in whole sets of channel-chunk siblings, at most one set per
+  // row tile
+  int cus = 0;
+  const hipError_t e = compute_units(&cus);
+  if (e != hipSuccess) return e;
+  const int waves = waves_for(nhg);
+  const size_t lds_per_wg = lds + sizeof(LdsBatch);
+  int per_cu = static_cast<int>((160 * 1024) / lds_per_wg);
+  per_cu = per_cu < 8 / waves ? per_cu : 8 / waves;
+  per_cu = per_cu < 1 ? 1 : per_cu;
+  const int n_nc = p.jobs[0].n / cn;
+  const int64_t tile_rows = 32 * waves;
+  const int64_t row_tiles = (p.m + tile_rows - 1) / tile_rows * p.n_jobs;
+  int64_t shares = static_cast<int64_t>(cus) * per_cu / n_nc;
+  shares = shares < 1 ? 1 : (shares > row_tiles ? row_tiles : shares);
+  const int grid_size = static_cast<int>(shares * n_nc);
 #define SCD_DECODE_DISPATCH(NHG, DH)                                                    \
   if (nhg == NHG && p.head_dim == DH)                                                   \
-    return rope ? launch_kch<NHG, DH, true>(kch, p, lds, stream)                        \
-                : launch_kch<NHG, DH, false>(kch, p, lds, stream);
+    return rope ? launch_kch<NHG, DH, true>(kch, p, grid_size, lds, stream)             \
+                : launch_kch<NHG, DH, false>(kch, p, grid_size, lds, stream);
+  SCD_DECODE_DISPATCH(4, 128)
   SCD_DECODE_DISPATCH(2, 128)
   SCD_DECODE_DISPATCH(1, 128)
+  SCD_DECODE_DISPATCH(4, 64)
   SCD_DECODE_DISPATCH(2, 64)
   SCD_DECODE_DISPATCH(1, 64)
 #undef SCD_DECODE_DISPATCH

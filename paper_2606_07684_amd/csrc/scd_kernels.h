@@ -39,7 +39,7 @@ struct GemmParams {
   int32_t g;            // rows per token (row r belongs to token r / g)
   int32_t head_dim;
   int32_t n_seqs;
-  int32_t tiles_per_unit;     // row tiles one workgroup processes (bf16 decode)
+  int32_t reserved;
   const int32_t* cu_seqlens;  // [n_seqs + 1] or null (one request)
   const int32_t* pos0;        // [n_seqs] or null
   const float2* rope;         // [max_pos][head_dim / 2] (cos, sin)
@@ -64,11 +64,11 @@ constexpr int kPatchBM = 256;
 constexpr int kPatchBN = 256;
 hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
 
-// Reuse decode on the bf16 path: a unit is (channel chunk of 128 * nhg, tiles_per_unit tiles of
-// 128 rows); basis_width % (128 * nhg) == 0, one rank (% 32 == 0, <= 256) and one branch per
-// launch, head_dim 64 or 128.
-constexpr int kDecodeTileRows = 128;
+// Reuse decode on the bf16 path: workgroups own a channel chunk of 128 * nhg and a share of the
+// launch's row tiles (decode_tile_rows(nhg) rows each); basis_width % (128 * nhg) == 0, one rank
+// (% 32 == 0, <= 256) and one branch per launch, head_dim 64 or 128.
 int decode_channel_groups(int rank, int basis_width);
+int decode_tile_rows(int nhg);  // rows per tile of the kernel instance for nhg channel groups
 hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream);
 
 // Largest batch (requests) the bf16 decode kernel stages in LDS.
