@@ -3,20 +3,29 @@
 // written straight into the consumer's KV cache.  The step is bound by HBM writes: every
 // reconstructed element is written once and the codes are only r/w of that traffic.
 //
-// Work unit: NHG groups of 128 channels (CN = 128 * NHG) of one layer-branch x a group of
-// tiles of 128 rows.  The workgroup copies its basis chunk (CN rows of W_dec, permuted so each
-// MFMA accumulator lane ends with 16 consecutive channels of one row) into padded LDS rows with
-// direct global->LDS loads.  Each of its 4 waves owns 32 rows of a tile: it loads their codes
-// once, then for every 128-channel group runs v_mfma_f32_32x32x16_bf16 (basis as A, codes as
-// B), adds the offset, rotates the keys and stores 16-byte vectors.
+// Work decomposition: a launch covers one branch (keys or values) of every layer of one rank, as
+// one round of workgroups sized to the machine.  A workgroup owns a channel chunk of NHG x 128
+// channels (512 for ranks up to 128: one workgroup of 8 waves per CU, whose basis chunk fills most
+// of the LDS) and a contiguous, balanced share of the launch's row tiles, running across layers.
+// It copies a layer-branch's basis chunk (CN rows of W_dec, permuted so each MFMA accumulator lane
+// ends with 16 consecutive channels of one row) into padded LDS rows with direct global->LDS
+// loads when its share enters that layer-branch.  Each wave owns 32 rows of a tile: it loads
+// their codes once, then for every 128-channel group runs v_mfma_f32_32x32x16_bf16 (basis as A,
+// codes as B), adds the offset, rotates the keys and stores 16-byte vectors.  The waves start
+// every tile together, which keeps the workgroup's stores on neighbouring rows.
 //
-// Vector-memory instructions whose 64 lanes touch many cache lines are what limits this step, so
-// the RoPE factors are built to need few of them: a row at position p with in-half offset
-// d = (lane % 16) uses cos/sin((p - d) w) * cos/sin(d w).  The first factor is (nearly) the same
-// row for the 16 lanes of a half-wave, so its loads broadcast; the second comes from table rows
-// 0..15 staged once per workgroup in LDS.  Both factors are fp64-evaluated table entries; the
-// product in fp32 is within a few ulp of cos/sin(p w).  Codes and factors are reused for every
-// channel group.
+// Why this shape: the step writes ~8x what it reads, and HBM serves that write stream worst when
+// reads are interleaved with it and when concurrent stores scatter over many rows.  A 512-channel
+// chunk halves the code re-reads of a 256-channel one, the single round and the long shares
+// leave almost no per-workgroup set-up (basis copy, waits) on the critical path, and the lockstep
+// keeps the stores of a workgroup close together.
+//
+// RoPE factors are built to need few vector-memory instructions: a row at position p with
+// in-half offset d = (lane % 16) uses cos/sin((p - d) w) * cos/sin(d w).  The first factor is
+// (nearly) the same row for the 16 lanes of a half-wave, so its loads broadcast; the second comes
+// from table rows 0..15 staged once per workgroup in LDS.  Both factors are fp64-evaluated table
+// entries; the product in fp32 is within a few ulp of cos/sin(p w).  Codes and factors are reused
+// for every channel group.
 #include "scd_device.h"
 
 namespace scd {
