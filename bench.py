@@ -150,6 +150,28 @@ def cpu_baseline(wl, inp, budget_s=25.0):
     }
 
 
+def copy_ceiling(dev, gib=1.0, reps=10):
+    """Attainable HBM bandwidth on this GPU: a plain device-to-device copy of ``gib`` GiB (read +
+    write bytes over time), timed with HIP events on the current stream."""
+    import torch
+
+    n = int(gib * (1 << 30)) // 4
+    src = torch.empty(n, dtype=torch.float32, device=dev).uniform_()
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    end.record()
+    torch.cuda.synchronize()
+    gbps = 2 * n * 4 * reps / (start.elapsed_time(end) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -278,6 +300,28 @@ def main():
         "roofline_kernel": dom["kernel"],
         "rooflines": rooflines,
         "source_digest": digest,
+    }
+
+    # The combined readings of the decode-side target (Reuse decode + Patch at this workload):
+    #   reuse_hbm_frac:   Reuse algorithmic bytes / t_reuse / 8 TB/s
+    #   patch_mfma_frac:  Patch flops / t_patch / 2.5 PFLOP/s
+    #   roofline_time_frac: (t_HBM(Reuse) + t_MFMA(Patch)) / (t_reuse + t_patch), the fraction of the
+    #                     serial roofline time the two steps achieve together
+    #   literal_hbm_frac: (Reuse + Patch algorithmic bytes) / (t_reuse + t_patch) / 8 TB/s
+    # and the same decode and copy rates against a plain device copy timed in this run.
+    t_r, t_p = mean["reuse_decode"] * 1e-3, mean["patch_kv"] * 1e-3
+    b_r, b_p = alg["reuse_decode"][0], alg["patch_kv"][0]
+    f_p = alg["patch_kv"][1]
+    peak_flops = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12
+    copy_gbps = copy_ceiling(dev)
+    out["decode_readings"] = {
+        "reuse_hbm_frac": round(b_r / t_r / (HBM_PEAK_GBPS * 1e9), 4),
+        "patch_mfma_frac": round(f_p / t_p / peak_flops, 4),
+        "roofline_time_frac": round((b_r / (HBM_PEAK_GBPS * 1e9) + f_p / peak_flops) / (t_r + t_p),
+                                    4),
+        "literal_hbm_frac": round((b_r + b_p) / (t_r + t_p) / (HBM_PEAK_GBPS * 1e9), 4),
+        "copy_ceiling_GBps": round(copy_gbps, 1),
+        "reuse_frac_of_copy_ceiling": round(b_r / t_r / 1e9 / copy_gbps, 4),
     }
 
     if args.copy_probe_gib > 0:
