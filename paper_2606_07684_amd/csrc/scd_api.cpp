@@ -432,7 +432,7 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
        })) {
     const int nhg = scd::decode_channel_groups(grp[0].k, w);
     scd::GemmParams gp = base;
-    JobPacker jp(gp, scd::decode_tile_rows(nhg), 128 * nhg);
+    JobPacker jp(gp, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
     for (const auto& j : grp) jp.add(j);
     for (const auto& lp : jp.build()) {
       const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream);

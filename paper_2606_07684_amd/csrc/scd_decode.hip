@@ -33,10 +33,12 @@ namespace {
 
 using namespace dev;
 
-// Waves per workgroup: 4 for chunks of 128 or 256 channels (two workgroups per CU), 8 for chunks of
-// 512 channels (one workgroup per CU; its basis chunk fills most of the LDS).  A tile is 32 rows
-// per wave.
-constexpr int waves_for(int nhg) { return nhg == 4 ? 8 : 4; }
+// Waves per workgroup: 8 when the basis chunk (128 nhg channels x rank) takes more than half the
+// LDS, so one workgroup holds the CU (512 channels up to rank 128, 256 channels above); 4 when
+// two workgroups share a CU.  A tile is 32 rows per wave.
+constexpr int waves_for(int nhg, int kch) {
+  return 128 * nhg * (32 * kch + 8) * 2 > 80 * 1024 ? 8 : 4;
+}
 constexpr int kDRows = kRopeMinRows;  // in-half offsets d = 0..15
 
 // The layer-branch a workgroup is working on.
@@ -50,7 +52,7 @@ struct DecodeCtx {
 // One tile: the TT rows from row t0 of the current layer-branch, channels [n0, n0 + 128 NHG).
 // KCH = rank / 32, NHG = channel groups of 128, DH = head_dim, ROPE = key jobs, FULL = all TT
 // rows exist (only the last tile of a layer-branch can be partial).
-template <int KCH, int NHG, int DH, bool ROPE, bool FULL, int TT = 32 * waves_for(NHG)>
+template <int KCH, int NHG, int DH, bool ROPE, bool FULL, int TT = 32 * waves_for(NHG, KCH)>
 __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch& lb,
                                             const DecodeCtx& c, int64_t t0, const uint16_t* Fs,
                                             const uint16_t* mus, const float2* dtab, int lane,
@@ -159,8 +161,9 @@ __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch&
 // with every workgroup busy to the end.  A workgroup stages a layer-branch's basis chunk once,
 // when its share enters that layer-branch.
 template <int KCH, int NHG, int DH, bool ROPE>
-__global__ __launch_bounds__(64 * waves_for(NHG), 2) void reuse_decode_bf16_kernel(GemmParams p) {
-  constexpr int kWaves = waves_for(NHG);
+__global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16_kernel(
+    GemmParams p) {
+  constexpr int kWaves = waves_for(NHG, KCH);
   constexpr int kThreads = 64 * kWaves;
   constexpr int kTT = 32 * kWaves;
   constexpr int CN = 128 * NHG;
@@ -243,25 +246,24 @@ __global__ __launch_bounds__(64 * waves_for(NHG), 2) void reuse_decode_bf16_kern
 template <int NHG, int DH, bool ROPE>
 hipError_t launch_kch(int kch, const GemmParams& p, int grid_size, size_t lds,
                       hipStream_t stream) {
-  const dim3 grid(grid_size), block(64 * waves_for(NHG));
   switch (kch) {
 #define SCD_DECODE_CASE(KC)                                                                   \
   case KC:                                                                                    \
-    hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), grid, block, lds, stream, \
-                       p);                                                                    \
+    hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), dim3(grid_size),       \
+                       dim3(64 * waves_for(NHG, KC)), lds, stream, p);                        \
     return hipGetLastError();
     SCD_DECODE_CASE(1) SCD_DECODE_CASE(2) SCD_DECODE_CASE(3) SCD_DECODE_CASE(4)
 #undef SCD_DECODE_CASE
     default:
       break;
   }
-  // ranks above 128 use one channel group per workgroup (decode_channel_groups)
-  if constexpr (NHG == 1) {
+  // ranks above 128 use at most two channel groups per workgroup (decode_channel_groups)
+  if constexpr (NHG <= 2) {
     switch (kch) {
 #define SCD_DECODE_CASE(KC)                                                                   \
   case KC:                                                                                    \
-    hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), grid, block, lds, stream, \
-                       p);                                                                    \
+    hipLaunchKernelGGL((reuse_decode_bf16_kernel<KC, NHG, DH, ROPE>), dim3(grid_size),       \
+                       dim3(64 * waves_for(NHG, KC)), lds, stream, p);                        \
     return hipGetLastError();
       SCD_DECODE_CASE(5) SCD_DECODE_CASE(6) SCD_DECODE_CASE(7) SCD_DECODE_CASE(8)
 #undef SCD_DECODE_CASE
@@ -275,11 +277,11 @@ hipError_t launch_kch(int kch, const GemmParams& p, int grid_size, size_t lds,
 }  // namespace
 
 int decode_channel_groups(int rank, int basis_width) {
-  if (rank > 128) return 1;
+  if (rank > 128) return basis_width % 256 == 0 ? 2 : 1;
   return basis_width % 512 == 0 ? 4 : (basis_width % 256 == 0 ? 2 : 1);
 }
 
-int decode_tile_rows(int nhg) { return 32 * waves_for(nhg); }
+int decode_tile_rows(int nhg, int rank) { return 32 * waves_for(nhg, (rank + 31) / 32); }
 
 // Compute units of the current device (queried once per device).
 static hipError_t compute_units(int* out) {
@@ -327,7 +329,7 @@ hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream) 
   int cus = 0;
   const hipError_t e = compute_units(&cus);
   if (e != hipSuccess) return e;
-  const int waves = waves_for(nhg);
+  const int waves = waves_for(nhg, kch);
   const size_t lds_per_wg = lds + sizeof(LdsBatch);
   int per_cu = static_cast<int>((160 * 1024) / lds_per_wg);
   per_cu = per_cu < 8 / waves ? per_cu : 8 / waves;

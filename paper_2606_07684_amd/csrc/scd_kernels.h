@@ -68,7 +68,7 @@ hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
 // launch's row tiles (decode_tile_rows(nhg) rows each); basis_width % (128 * nhg) == 0, one rank
 // (% 32 == 0, <= 256) and one branch per launch, head_dim 64 or 128.
 int decode_channel_groups(int rank, int basis_width);
-int decode_tile_rows(int nhg);  // rows per tile of the kernel instance for nhg channel groups
+int decode_tile_rows(int nhg, int rank);  // rows per tile of the kernel instance
 hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream);
 
 // Largest batch (requests) the bf16 decode kernel stages in LDS.
