@@ -9,8 +9,9 @@ The Reuse decode consumes the codes the encode of the same step produced.
 
 Prints one JSON line.  ``value`` is reconstructed-KV GB/s over the whole step (KV bytes written by
 Reuse + Patch divided by the full step time, encode included), ``tokens_per_s`` the prefix tokens
-per second.  ``roofline`` is the dominant kernel's achieved fraction of its bound, timed with HIP
-events on the stream the kernels run on; ``cpu_baseline`` is the fp64 oracle timed on this host.
+per second, both from K uninstrumented steps.  ``roofline`` is the dominant kernel's achieved
+fraction of its bound, from a second pass of K steps with HIP events between the entry points on
+the stream the kernels run on; ``cpu_baseline`` is the fp64 oracle timed on this host.
 """
 from __future__ import annotations
 
@@ -238,14 +239,19 @@ def main():
     torch.cuda.synchronize()
     print("[bench] warmup done", file=sys.stderr, flush=True)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # the headline: K whole steps back to back, bracketed by synchronizations, no instrumentation
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(events[i])
+    for _ in range(args.steps):
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print("[bench] timed steps done", file=sys.stderr, flush=True)
+    # per-step breakdown: the same steps again, with HIP events between the entry points
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
 
     phase = {"encode": [], "reuse_decode": [], "patch_kv": []}
     for ev in events:
