@@ -165,6 +165,25 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
                           const void* const* b_k, const void* const* b_v,
                           void* const* k_cache, void* const* v_cache, hipStream_t stream);
 
+/* ---- Patch aligner (Section 4.4.2, Eq. aligner) --------------------------------------------------
+ * The consumer's aligner g_theta maps each Patch layer's code to a predicted normalised attention
+ * input, the input of scd_patch_kv:
+ *   act[l]   = SiLU(z_h[l] w1[l]^T + b1[l])           [T, hidden]
+ *   h_hat[l] = act[l] w2[l]^T + b2[l]                 [T, d_model]
+ * with z_h [T, rank_h[l]] (the transmitted code), w1 [hidden, rank_h[l]], w2 [d_model, hidden]
+ * (nn.Linear layout), b1 [hidden] and b2 [d_model] optional (NULL array or entry = none) and
+ * SiLU(x) = x / (1 + e^-x), evaluated in fp32 before the one rounding of each product.  The paper
+ * calls g_theta an MLP and fixes neither its depth, width nor activation: this is a two-layer MLP
+ * of width `hidden` (16 <= hidden, hidden % 16 == 0) with the backbone's SiLU.  act[l] holds layer
+ * l's hidden activations: caller-owned, one buffer per Patch layer, distinct (the call writes them
+ * all before it reads them); an act buffer that repeats returns SCD_ERR_SHAPE.  Reuse layers are
+ * not touched. */
+scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch, int32_t hidden,
+                             const void* const* z_h,
+                             const void* const* w1, const void* const* b1,
+                             const void* const* w2, const void* const* b2,
+                             void* const* act, void* const* h_hat, hipStream_t stream);
+
 /* ---- diagnostics ---------------------------------------------------------------------------- */
 const char* scd_status_string(scd_status_t status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */

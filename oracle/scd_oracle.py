@@ -188,6 +188,33 @@ def decode_v(z_v, w_dec, mu_dec, d):
 
 
 # --------------------------------------------------------------------------------------------
+# Patch aligner (Section 4.4.2, Eq. (aligner)): H_hat = g_theta(Z_H).  The paper calls g_theta
+# an MLP and fixes neither depth, width nor activation; the reading taken is two layers with the
+# backbone's SiLU between them: H_hat = W2 SiLU(W1 z + b1) + b2, weights stored [out, in].
+# --------------------------------------------------------------------------------------------
+def silu(x):
+    """``SiLU(x) = x * sigmoid(x) = x / (1 + e^-x)``, evaluated so that no term overflows."""
+    x = _f64(x)
+    # sigmoid(x) = 1 / (1 + e^-x) for x >= 0 and e^x / (1 + e^x) for x < 0 (same value)
+    e = np.exp(-np.abs(x))
+    sig = np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+    return x * sig
+
+
+def align(z_h, w1, b1, w2, b2):
+    """``H_hat = SiLU(Z_H @ W1^T + b1) @ W2^T + b2`` with ``W1 [h, r_H]``, ``W2 [d_model, h]``;
+    ``b1``/``b2`` may be ``None``.  Returns ``(H_hat, hidden activations)``."""
+    a = _f64(z_h) @ _f64(w1).T
+    if b1 is not None:
+        a = a + _f64(b1)[None, :]
+    a = silu(a)
+    y = a @ _f64(w2).T
+    if b2 is not None:
+        y = y + _f64(b2)[None, :]
+    return y, a
+
+
+# --------------------------------------------------------------------------------------------
 # a7: Patch KV regeneration (Section 4.4.2, Eq. (kv_from_patch); Appendix F.2 "Online Patch").
 # --------------------------------------------------------------------------------------------
 def patch_k(h_hat, w_k, b_k, pos, n_kv_heads, head_dim, theta):

@@ -28,6 +28,7 @@ __all__ = [
     "scd_rope_table", "scd_positions", "scd_schedule", "scd_payload_bytes",
     "scd_encode", "scd_reuse_decode", "scd_patch_kv", "scd_abi_version",
     "Prepared", "prepare_encode", "prepare_reuse_decode", "prepare_patch_kv",
+    "scd_patch_align", "prepare_patch_align",
 ]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -97,6 +98,8 @@ _SIGS = {
                                         ctypes.c_int64] + [_PP] * 8 + [_VP]),
     "scd_patch_kv": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.POINTER(_CBatch), _VP,
                                     ctypes.c_int64] + [_PP] * 7 + [_VP]),
+    "scd_patch_align": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.POINTER(_CBatch),
+                                       ctypes.c_int32] + [_PP] * 7 + [_VP]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -388,3 +391,30 @@ def prepare_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_ha
 def scd_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_hat, w_k, w_v,
                  b_k, b_v, k_cache, v_cache, stream=None) -> None:
     prepare_patch_kv(model, batch, rope, h_hat, w_k, w_v, b_k, b_v, k_cache, v_cache)(stream)
+
+
+def prepare_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2, b2, act,
+                        h_hat) -> Prepared:
+    """The Patch aligner (Eq. aligner): act = SiLU(z_h w1^T + b1), h_hat = act w2^T + b2 for every
+    Patch layer; act is caller-owned scratch, one distinct [T, hidden] buffer per Patch layer."""
+    lib = load_library()
+    L, T, d = model.n_layers, batch.n_tokens, model.d_model
+    dt = model.torch_dtype
+    P = [l for l in range(L) if model.is_patch[l]]
+    args = [
+        _ptr_array(z_h, L, "z_h", {l: (T, model.rank_h[l]) for l in P}, dt),
+        _ptr_array(w1, L, "w1", {l: (hidden, model.rank_h[l]) for l in P}, dt),
+        _ptr_array(b1, L, "b1", {l: (hidden,) for l in P}, dt),
+        _ptr_array(w2, L, "w2", {l: (d, hidden) for l in P}, dt),
+        _ptr_array(b2, L, "b2", {l: (d,) for l in P}, dt),
+        _ptr_array(act, L, "act", {l: (T, hidden) for l in P}, dt),
+        _ptr_array(h_hat, L, "h_hat", {l: (T, d) for l in P}, dt),
+    ]
+    return Prepared(lib.scd_patch_align, (ctypes.byref(model._c), ctypes.byref(batch._c),
+                                          int(hidden), *[_as_pp(a) for a in args]),
+                    (model, batch, args))
+
+
+def scd_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2, b2, act, h_hat,
+                    stream=None) -> None:
+    prepare_patch_align(model, batch, hidden, z_h, w1, b1, w2, b2, act, h_hat)(stream)

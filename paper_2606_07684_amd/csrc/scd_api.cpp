@@ -208,7 +208,7 @@ int64_t kv_width(const scd_model_t* m) {
 
 extern "C" {
 
-int32_t scd_abi_version(void) { return 1; }
+int32_t scd_abi_version(void) { return 2; }
 
 const char* scd_status_string(scd_status_t s) {
   switch (s) {
@@ -484,6 +484,71 @@ scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
   for (const auto& p : jp.build()) {
     const hipError_t e = scd::launch_patch_bf16(p, stream);
     if (e != hipSuccess) return fail(SCD_ERR_HIP, "patch launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch, int32_t hidden,
+                             const void* const* z_h,
+                             const void* const* w1, const void* const* b1,
+                             const void* const* w2, const void* const* b2,
+                             void* const* act, void* const* h_hat, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  if (hidden < 16 || hidden % 16 != 0)
+    return fail(SCD_ERR_SHAPE, "aligner width %d must be a positive multiple of 16", hidden);
+  if (model->d_model % 16 != 0)
+    return fail(SCD_ERR_SHAPE, "d_model %d must be a multiple of 16 for the aligner",
+                model->d_model);
+  const int rh_max = model->d_model < 256 ? model->d_model : 256;
+  bool any = false;
+  bool fast = model->dtype == SCD_BF16 && hidden % 128 == 0 && model->d_model % 128 == 0;
+  std::vector<const void*> acts;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    any = true;
+    const void* tmp;
+    SCD_TRY(check_rank("rank_h", l, model->rank_h[l], rh_max));
+    SCD_TRY(need_tok_ptr(z_h, l, "z_h", batch->n_tokens));
+    SCD_TRY(need_ptr(w1, l, "w1"));
+    SCD_TRY(need_ptr(w2, l, "w2"));
+    SCD_TRY(opt_ptr(b1, l, "b1", &tmp));
+    SCD_TRY(opt_ptr(b2, l, "b2", &tmp));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(act), l, "act", batch->n_tokens));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(h_hat), l, "h_hat",
+                         batch->n_tokens));
+    if (batch->n_tokens > 0) {
+      for (const void* a : acts)
+        if (a == act[l])
+          return fail(SCD_ERR_SHAPE, "act[%d] repeats an earlier Patch layer's buffer", l);
+      acts.push_back(act[l]);
+    }
+    if (model->rank_h[l] % 64 != 0) fast = false;
+  }
+  if (!any || batch->n_tokens == 0) return ok();
+
+  const int64_t T = batch->n_tokens;
+  const int d = model->d_model;
+  scd::GemmParams base = base_params(model, batch, T, 1, nullptr, 0);
+  const int bm = fast ? scd::kPatchBM : scd::kGenericBM, bn = fast ? scd::kPatchBN : scd::kGenericBN;
+  // act = SiLU(z_h w1^T + b1) for every Patch layer, then h_hat = act w2^T + b2
+  JobPacker first(base, bm, bn), second(base, bm, bn);
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    first.add({z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
+               scd::kVecOut | scd::kSiluOut, 0});
+    second.add({act[l], w2[l], h_hat[l], b2 ? b2[l] : nullptr, d, hidden, scd::kVecOut, 0});
+  }
+  for (JobPacker* jp : {&first, &second}) {
+    if (!fast) {
+      SCD_TRY(run(scd::Op::kPatchAlign, jp->build(), model->dtype, stream));
+      continue;
+    }
+    for (const auto& p : jp->build()) {
+      const hipError_t e = scd::launch_align_bf16(p, stream);
+      if (e != hipSuccess)
+        return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
+    }
   }
   return ok();
 }

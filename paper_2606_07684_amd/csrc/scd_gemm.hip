@@ -111,6 +111,7 @@ struct ReuseDecode {};
 struct PatchKV {};
 struct EncodeKV {};
 struct EncodeH {};
+struct PatchAlign {};
 
 template <typename OP, bool BF16, int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
@@ -152,6 +153,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
   const bool rope_out = (job.flags & kRopeOut) != 0;
   const bool vec_in = (job.flags & kVecIn) != 0 && job.vec != nullptr;
   const bool vec_out = (job.flags & kVecOut) != 0 && job.vec != nullptr;
+  const bool silu_out = (job.flags & kSiluOut) != 0;
   const int dh = p.head_dim, half = dh / 2;
   const int K = job.k, N = job.n;
   const int64_t M = p.m;
@@ -395,6 +397,10 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_nt_kernel(GemmParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) u[e] += EL::load1(job.vec, gc0 + e);
       }
+      if (silu_out) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) u[e] = u[e] / (1.f + expf(-u[e]));
+      }
       uint4 o0[NV];
       EL::pack(u, o0);
       uint4* d0 = reinterpret_cast<uint4*>(C + gm * N + gc0);
@@ -456,6 +462,7 @@ hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream
     case Op::kPatchKV: return launch_op<PatchKV>(bf16, p, stream);
     case Op::kEncodeKV: return launch_op<EncodeKV>(bf16, p, stream);
     case Op::kEncodeH: return launch_op<EncodeH>(bf16, p, stream);
+    case Op::kPatchAlign: return launch_op<PatchAlign>(bf16, p, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -15,6 +15,7 @@ enum JobFlags : int32_t {
   kDeropeIn = 2,  // inverse-rotate input column pairs of A before the contraction
   kVecOut = 4,    // vec[n] is added to every output row before RoPE (decoder offset, bias)
   kVecIn = 8,     // vec[k] is subtracted from every row of A after deRoPE (encoder offset)
+  kSiluOut = 16,  // SiLU x / (1 + e^-x) on every output after vec (aligner hidden layer)
 };
 
 // One dense product C[M, n] = prologue(A)[M, k] * B[n, k]^T (+ bias[n]) followed by the epilogue
@@ -53,7 +54,7 @@ constexpr int kGenericBN = 128;
 
 // The codec step a launch performs; each step is its own kernel symbol so profiles attribute time
 // per step.
-enum class Op : int { kReuseDecode = 0, kPatchKV = 1, kEncodeKV = 2, kEncodeH = 3 };
+enum class Op : int { kReuseDecode = 0, kPatchKV = 1, kEncodeKV = 2, kEncodeH = 3, kPatchAlign = 4 };
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream);
@@ -63,6 +64,9 @@ hipError_t launch_gemm(Op op, bool bf16, const GemmParams& p, hipStream_t stream
 constexpr int kPatchBM = 256;
 constexpr int kPatchBN = 256;
 hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
+// The aligner's two products on the same kernel (its own symbol): C = act(A B^T + vec), with
+// act = SiLU on jobs flagged kSiluOut; no RoPE.
+hipError_t launch_align_bf16(const GemmParams& p, hipStream_t stream);
 
 // Reuse decode on the bf16 path: workgroups own a channel chunk of 128 * nhg and a share of the
 // launch's row tiles (decode_tile_rows(nhg) rows each); basis_width % (128 * nhg) == 0, one rank

@@ -83,8 +83,10 @@ __device__ __forceinline__ void interleave_reads_dma() {
   __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
 }
 
-__global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
+// The product C = A B^T of one launch (both operands row-major with the contraction contiguous,
+// 256 x 256 tiles), with the epilogue the job flags select.  Two kernels run it: the Patch KV
+// regeneration and the aligner in front of it, so profiles attribute each step to its own symbol.
+__device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* smem) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -222,6 +224,7 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
   // Epilogue.  Lane l holds, for block (s, u), token t0 + wt*128 + 32u + l%32 and channels
   // n0 + wn*128 + 32s + 16*(l/32) + r, r = 0..15.
   const bool rope = (job.flags & kRopeOut) != 0;
+  const bool silu = (job.flags & kSiluOut) != 0;
   const bool add_vec = (job.flags & kVecOut) != 0 && job.vec != nullptr;
   const uint16_t* bias = static_cast<const uint16_t*>(job.vec);
   uint16_t* C = static_cast<uint16_t*>(job.c);
@@ -273,6 +276,13 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
       a[r] += acc[S][u][r];
       b[r] += acc[SP][u][r];
     }
+    if (silu) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        a[r] = a[r] / (1.f + __expf(-a[r]));
+        b[r] = b[r] / (1.f + __expf(-b[r]));
+      }
+    }
     if (rope) {
       const int i0 = (32 * S + hl) & (half - 1);  // pair index of channel r = 0
 #pragma unroll
@@ -303,11 +313,27 @@ __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p
   }
 }
 
+__global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
+  patch_gemm_bf16(p, smem);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void patch_align_bf16_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
+  patch_gemm_bf16(p, smem);
+}
+
 }  // namespace
 
 hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream) {
   if (p.total_tiles <= 0) return hipSuccess;
   hipLaunchKernelGGL(patch_kv_bf16_kernel, dim3(p.total_tiles), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_align_bf16(const GemmParams& p, hipStream_t stream) {
+  if (p.total_tiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(patch_align_bf16_kernel, dim3(p.total_tiles), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 

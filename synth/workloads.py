@@ -38,6 +38,7 @@ class Workload:
     with_bias: bool = False           # projection bias on the Patch branch (Qwen2-style)
     with_mu: bool = True
     ranks_v: Optional[Tuple[int, ...]] = None  # per-layer r_V when it differs from r_K
+    aligner_hidden: Optional[int] = None  # width of the Patch aligner's hidden layer (None: d_model)
 
     def rank(self, layer: int, branch: str) -> int:
         """Rank of one layer's branch ('k', 'v' or 'h')."""
@@ -82,6 +83,10 @@ class Workload:
         """One past the largest RoPE position any token of the batch takes."""
         p0 = self.pos0 or (0,) * self.n_seqs
         return int(max(a + n for a, n in zip(p0, self.seq_lens)))
+
+    @property
+    def hidden_width(self) -> int:
+        return self.aligner_hidden or self.d_model
 
     @property
     def torch_dtype(self):
@@ -143,8 +148,12 @@ SMALL_FULL_RANK = Workload("small_full_rank_bf16", 2, 256, 2, 128, (300, 33), (2
 # More requests than the bf16 decode stages in LDS (256): the generic kernel takes the batch.
 SMALL_MANY_REQUESTS = Workload("small_many_requests_bf16", 2, 128, 2, 64, _ragged_lengths(5, 300, 0, 3),
                                (32, 32), (1,), 1e4, "bf16")
+# Patch aligner on the bf16 GEMM kernel: ragged token count (two partial 256-row tiles), code ranks
+# 64 and 192, hidden width 384 (one and a half 256-column tiles).
+SMALL_ALIGN = Workload("small_align_bf16", 3, 512, 2, 128, (300, 77, 650), (64, 128, 192), (0, 2),
+                       5e5, "bf16", aligner_hidden=384)
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
-                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS)
+                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN)
 
 
 # --------------------------------------------------------------------------------------------
@@ -262,6 +271,23 @@ def proj_bias(wl: Workload, layer: int, device="cpu"):
     bk = _randn(wl, layer, "b_k", (wl.kv_width,), "cpu") * np.sqrt(0.1)
     bv = _randn(wl, layer, "b_v", (wl.kv_width,), "cpu") * np.sqrt(0.1)
     return _cast(bk, wl, device), _cast(bv, wl, device)
+
+
+def aligner_weights(wl: Workload, layer: int, device="cpu"):
+    """Patch aligner of one layer, ``(W1 [h, r_H], b1 [h], W2 [d_model, h], b2 [d_model])``:
+    ``W1 ~ N(0, 1/r_H)``, ``W2 ~ N(0, 1/h)``, biases ``N(0, 0.01)`` (random initialisation of the
+    two-layer MLP; no trained aligner is available)."""
+    r, h, d = wl.rank(layer, "h"), wl.hidden_width, wl.d_model
+    w1 = _randn(wl, layer, "align_w1", (h, r), device) / np.sqrt(r)
+    b1 = _randn(wl, layer, "align_b1", (h,), "cpu") * 0.1
+    w2 = _randn(wl, layer, "align_w2", (d, h), device) / np.sqrt(h)
+    b2 = _randn(wl, layer, "align_b2", (d,), "cpu") * 0.1
+    return _cast(w1, wl, device), _cast(b1, wl, device), _cast(w2, wl, device), _cast(b2, wl, device)
+
+
+def patch_codes(wl: Workload, layer: int, device="cpu") -> torch.Tensor:
+    """Patch-layer codes ``Z_H [T, r_H]`` ~ N(0, 1), the aligner's input."""
+    return _cast(_randn(wl, layer, "z_h", (wl.n_tokens, wl.rank(layer, "h")), device), wl, device)
 
 
 def cu_seqlens(wl: Workload, device="cpu") -> torch.Tensor:

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), f"libscd.so does not export {n}"
     assert set(names) == set(scd.EXPORTED_SYMBOLS)
-    assert scd.scd_abi_version() == 1
+    assert scd.scd_abi_version() == 2
 
 
 def test_status_strings(lib):
@@ -169,6 +169,33 @@ def test_encode_and_patch_validation(lib):
     need = lib.scd_rope_table_bytes(ctypes.byref(m._c), 100)
     assert need == 100 * 32 * 8
     assert lib.scd_rope_table(ctypes.byref(m._c), 100, FAKE, need - 1, None) == WS
+
+
+def test_aligner_validation(lib):
+    m = _model()  # layer 1 is the Patch layer (rank_h 32, d_model 256)
+    b = _batch()
+    L = m.n_layers
+    p, keep = _ptrs(L)
+
+    def align(model=m, batch=b, hidden=64, z=p, w1=p, b1=None, w2=p, b2=None, act=p, out=p):
+        return lib.scd_patch_align(ctypes.byref(model._c), ctypes.byref(batch._c), hidden, z, w1,
+                                   b1, w2, b2, act, out, None)
+
+    assert align(hidden=0) == SHAPE
+    assert align(hidden=40) == SHAPE
+    assert "multiple of 16" in lib.scd_last_error().decode()
+    q, keepq = _ptrs(L, skip=(1,))
+    assert align(w2=q) == NULL and "w2[1]" in lib.scd_last_error().decode()
+    assert align(z=q, batch=_batch(n_tokens=0)) == OK  # no tokens: token buffers may be absent
+    r, keepr = _ptrs(L, value=FAKE + 8)
+    assert align(b1=r) == ALIGN
+    assert align(model=_model(rank_h=[32, 24, 32])) == SCHED
+    # act entries must be distinct across Patch layers
+    m2 = _model(is_patch=[1, 1, 0])
+    assert align(model=m2) == SHAPE and "act[1]" in lib.scd_last_error().decode()
+    acts = (ctypes.c_void_p * L)(FAKE, FAKE + 4096, FAKE)
+    assert align(model=m2, act=ctypes.cast(acts, ctypes.POINTER(ctypes.c_void_p)),
+                 batch=_batch(n_tokens=0)) == OK
 
 
 @pytest.mark.parametrize("wl", [*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS],

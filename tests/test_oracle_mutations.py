@@ -17,6 +17,8 @@ _encode_v = O.encode_v
 _decode_k = O.decode_k
 _decode_v = O.decode_v
 _patch_k = O.patch_k
+_align = O.align
+_silu = O.silu
 
 
 def rope_wrong_sign(x, pos, n, dh, theta, inverse=False):
@@ -95,6 +97,30 @@ def patch_k_bias_after_rope(h, w, b, pos, n, dh, theta):
     return y if b is None else y + np.asarray(b, F64)[None, :]
 
 
+def align_w1_transposed(z, w1, b1, w2, b2):
+    # contracts z with W1 rather than W1^T (only square-compatible shapes survive)
+    return _align(z, np.asarray(w1, F64).T, b1, w2, b2)
+
+
+def align_silu_after_output(z, w1, b1, w2, b2):
+    a = np.asarray(z, F64) @ np.asarray(w1, F64).T
+    if b1 is not None:
+        a = a + np.asarray(b1, F64)[None, :]
+    y = a @ np.asarray(w2, F64).T
+    if b2 is not None:
+        y = y + np.asarray(b2, F64)[None, :]
+    return O.silu(y), a
+
+
+def align_hidden_bias_dropped(z, w1, b1, w2, b2):
+    return _align(z, w1, None, w2, b2)
+
+
+def silu_sign_flipped(x):
+    x = np.asarray(x, F64)
+    return x / (1.0 + np.exp(x))
+
+
 def _schedule_swapped(is_patch):
     flags = [bool(v) for v in is_patch]
     return [l for l, f in enumerate(flags) if f], [l for l, f in enumerate(flags) if not f]
@@ -116,6 +142,10 @@ MUTATIONS = [
     ("patch_k", patch_k_no_bias),
     ("patch_k", patch_k_bias_after_rope),
     ("schedule", _schedule_swapped),
+    ("align", align_w1_transposed),
+    ("align", align_silu_after_output),
+    ("align", align_hidden_bias_dropped),
+    ("silu", silu_sign_flipped),
 ]
 
 PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]

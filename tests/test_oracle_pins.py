@@ -411,3 +411,68 @@ def test_whole_model_routing_and_assembly():
         else:
             assert pk[l] is None and rk[l] is not None
             np.testing.assert_allclose(cv[l], z[l] @ f[l].T)
+
+
+# ------------------------------------------------------------------------------------------
+# Patch aligner (Section 4.4.2, Eq. aligner): H_hat = W2 SiLU(W1 z + b1) + b2 (the MLP reading)
+# ------------------------------------------------------------------------------------------
+def test_silu_closed_forms():
+    # sigmoid(1) = 1 / (1 + 1/e); SiLU(x) = x (1 + tanh(x / 2)) / 2 (an independent formulation)
+    # (well conditioned for |x| <= 8; 1 + tanh(x/2) cancels further out)
+    xs = np.array([-7.5, -3.5, -1.0, -1e-3, 0.0, 1e-3, 0.5, 1.0, 2.0, 7.25])
+    want = np.array([x * (1.0 + math.tanh(x / 2.0)) / 2.0 for x in xs])
+    np.testing.assert_allclose(O.silu(xs), want, rtol=1e-13, atol=1e-300)
+    # far out: SiLU(x) = x e^x (1 - e^x + ...) for x -> -inf and x - x e^-x (1 - ...) for x -> inf
+    for x in (-30.0, -45.0):
+        assert abs(O.silu(np.array([x]))[0] - x * math.exp(x)) <= 1e-12 * abs(x * math.exp(x))
+    for x in (30.0, 45.0):
+        assert abs(O.silu(np.array([x]))[0] - (x - x * math.exp(-x))) <= 1e-15 * x
+    assert abs(O.silu(np.array([1.0]))[0] - 1.0 / (1.0 + math.exp(-1.0))) < 1e-15
+    # SiLU(x) - SiLU(-x) = x; the derivative at 0 is 1/2; no overflow far out
+    x = np.linspace(-40.0, 40.0, 161)
+    np.testing.assert_allclose(O.silu(x) - O.silu(-x), x, atol=1e-12)
+    h = 1e-6
+    assert abs((O.silu(np.array([h]))[0] - O.silu(np.array([-h]))[0]) / (2 * h) - 0.5) < 1e-9
+    far = O.silu(np.array([-800.0, 800.0]))
+    assert np.all(np.isfinite(far)) and far[0] == 0.0 and far[1] == 800.0
+
+
+def test_align_brute_force():
+    rng = np.random.default_rng(41)
+    t, r, hid, d = 3, 4, 5, 6
+    z = rng.standard_normal((t, r))
+    w1, b1 = rng.standard_normal((hid, r)), rng.standard_normal(hid)
+    w2, b2 = rng.standard_normal((d, hid)), rng.standard_normal(d)
+    y, act = O.align(z, w1, b1, w2, b2)
+    for i in range(t):
+        a = []
+        for j in range(hid):
+            s = b1[j]
+            for k in range(r):
+                s += z[i, k] * w1[j, k]
+            a.append(s / (1.0 + math.exp(-s)))
+            assert abs(act[i, j] - a[j]) < 1e-12
+        for c in range(d):
+            s = b2[c]
+            for j in range(hid):
+                s += a[j] * w2[c, j]
+            assert abs(y[i, c] - s) < 1e-12
+    # absent biases are zero biases
+    y0, _ = O.align(z, w1, None, w2, None)
+    y1, _ = O.align(z, w1, np.zeros(hid), w2, np.zeros(d))
+    np.testing.assert_array_equal(y0, y1)
+
+
+def test_align_linear_limit_and_zero_output_layer():
+    # with W1 = I and a large positive shift SiLU is the identity to within 60 e^-60, so the
+    # aligner is the affine map W2 (z + c) + b2
+    rng = np.random.default_rng(43)
+    t, r, d, c = 7, 8, 5, 60.0
+    z = rng.standard_normal((t, r))
+    w2, b2 = rng.standard_normal((d, r)), rng.standard_normal(d)
+    y, _ = O.align(z, np.eye(r), np.full(r, c), w2, b2)
+    np.testing.assert_allclose(y, (z + c) @ w2.T + b2, rtol=1e-12, atol=1e-9)
+    # a zero output layer leaves only its bias
+    w1 = rng.standard_normal((6, r))
+    y, _ = O.align(z, w1, rng.standard_normal(6), np.zeros((d, 6)), b2)
+    np.testing.assert_array_equal(y, np.tile(b2, (t, 1)))
