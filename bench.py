@@ -151,6 +151,50 @@ def cpu_baseline(wl, inp, budget_s=25.0):
     }
 
 
+def time_aligner(wl, dev, steps, warmup, stream):
+    """``scd_patch_align`` over every Patch layer (hidden width = the workload's), HIP events on
+    the stream it runs on; algorithmic flops 2T(r_H h + h d) and bytes of every operand read and
+    every result written once (the activations are written and read back once)."""
+    import torch
+
+    import paper_2606_07684_amd as scd
+    from synth import workloads as W
+
+    L, T, h, d = wl.n_layers, wl.n_tokens, wl.hidden_width, wl.d_model
+    z_h, w1, b1, w2, b2, act, hh = ([None] * L for _ in range(7))
+    flops = nbytes = 0
+    for l in range(L):
+        if not wl.is_patch[l]:
+            continue
+        r = wl.rank(l, "h")
+        z_h[l] = W.patch_codes(wl, l, dev)
+        w1[l], b1[l], w2[l], b2[l] = W.aligner_weights(wl, l, dev)
+        act[l] = torch.empty((T, h), dtype=wl.torch_dtype, device=dev)
+        hh[l] = torch.empty((T, d), dtype=wl.torch_dtype, device=dev)
+        flops += 2 * T * (r * h + h * d)
+        nbytes += (T * r + h * r + h + 2 * T * h + d * h + d + T * d) * wl.elem_bytes
+    model = scd.Model(n_layers=L, d_model=d, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                      rope_theta=wl.rope_theta, dtype=wl.dtype, is_patch=wl.is_patch,
+                      rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks, basis_width=wl.w)
+    cu = W.cu_seqlens(wl, dev) if wl.n_seqs > 1 or wl.pos0 is not None else None
+    batch = scd.Batch(n_tokens=T, cu_seqlens=cu, pos0=W.pos0(wl, dev))
+    run = scd.prepare_patch_align(model, batch, h, z_h, w1, b1, w2, b2, act, hh)
+    for _ in range(warmup):
+        run(stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(steps):
+        run(stream)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    ach = flops / (ms * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFLOPS[wl.dtype]
+    return {"kernel": "patch_align_bf16_kernel", "hidden": h, "ms_per_call": round(ms, 4),
+            "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(ach / peak, 4), "alg_flops": flops, "alg_bytes": nbytes}
+
+
 def copy_ceiling(dev, gib=1.0, reps=10):
     """Attainable HBM bandwidth on this GPU: a plain device-to-device copy of ``gib`` GiB (read +
     write bytes over time), timed with HIP events on the current stream."""
@@ -307,6 +351,11 @@ def main():
         "rooflines": rooflines,
         "source_digest": digest,
     }
+
+    # The Patch aligner (Eq. aligner, the row after the hot path): timed on its own over the same
+    # step count, reported beside the step and not part of ``value``.
+    if any(wl.is_patch):
+        out["aligner"] = time_aligner(wl, dev, args.steps, args.warmup, stream)
 
     # The combined readings of the decode-side target (Reuse decode + Patch at this workload):
     #   reuse_hbm_frac:   Reuse algorithmic bytes / t_reuse / 8 TB/s
