@@ -27,8 +27,9 @@ import bench
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PHASES = {"encode_bf16_kernel": "encode", "reuse_decode": "reuse_decode",
-          "patch_kv": "patch_kv", "EncodeKV": "encode", "EncodeH": "encode",
-          "ReuseDecode": "reuse_decode", "PatchKV": "patch_kv"}
+          "patch_kv": "patch_kv", "patch_align": "aligner", "EncodeKV": "encode",
+          "EncodeH": "encode", "ReuseDecode": "reuse_decode", "PatchKV": "patch_kv",
+          "PatchAlign": "aligner"}
 
 
 def phase_of(name: str):
@@ -64,6 +65,17 @@ def kernel_table(trace_dir: str, warmup_launches: int):
         groups.setdefault(key, []).append(dur)
     out = []
     for (name, grid), d in groups.items():
+        if phase_of(name) == "aligner":
+            # one call is two launches of the same kernel (the two products of the MLP), which may
+            # share a grid: split them by their order within the call
+            d = d[2 * warmup_launches:] or d
+            for i, part in enumerate(("first product", "second product")):
+                di = d[i::2]
+                if di:
+                    out.append({"kernel": f"{short(name)} ({part})", "phase": "aligner",
+                                "grid": grid, "launches": len(di), "mean_us": statistics.mean(di),
+                                "min_us": min(di), "max_us": max(di)})
+            continue
         d = d[warmup_launches:] or d
         out.append({"kernel": short(name), "phase": phase_of(name), "grid": grid, "launches": len(d),
                     "mean_us": statistics.mean(d), "min_us": min(d), "max_us": max(d)})
@@ -114,7 +126,7 @@ def main():
 
     from synth import workloads as W
     wl = {w.name: w for w in (*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS)}[args.workload]
-    alg = bench.algorithmic(wl)
+    alg = dict(bench.algorithmic(wl))
     digest = bench.source_digest()
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
 
@@ -137,7 +149,12 @@ def main():
         if args.bench_log:
             for line in open(args.bench_log):  # the first JSON line is the traced run's
                 if line.startswith("{"):
-                    events = json.loads(line).get("phase_ms", {})
+                    rec = json.loads(line)
+                    events = rec.get("phase_ms", {})
+                    if "aligner" in rec:  # timed beside the step, with its own figures
+                        al = rec["aligner"]
+                        alg["aligner"] = (al["alg_bytes"], al["alg_flops"])
+                        events["aligner"] = al["ms_per_call"]
                     break
         lines += ["", "Per entry-point call (sum of its launches) and the algorithmic roofline; "
                   "\"bench events\" is bench.py's own HIP-event time of the same call in the "
@@ -145,9 +162,11 @@ def main():
                   "| step | us per call | bench events us | algorithmic | achieved | fraction of peak |",
                   "|---|---|---|---|---|---|"]
         for ph, us in per_phase.items():
+            if ph not in alg:
+                continue
             ev = f"{events[ph] * 1e3:.1f}" if ph in events else "-"
             b, f = alg[ph]
-            bound = bench.KERNELS[ph][1]
+            bound = bench.KERNELS[ph][1] if ph in bench.KERNELS else "mfma"
             if bound == "hbm":
                 ach = b / (us * 1e-6) / 1e9
                 lines.append(f"| {ph} | {us:.1f} | {ev} | {b / 1e9:.4f} GB | {ach:.0f} GB/s | "
