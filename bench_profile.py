@@ -51,7 +51,7 @@ def one_csv(folder: str, suffix: str) -> str:
     return found[0]
 
 
-def kernel_table(trace_dir: str, warmup_launches: int):
+def kernel_table(trace_dir: str, warmup_launches: int, aligner_calls: int = 0):
     """Per (kernel, grid) group of codec kernels: launches, mean/min/max microseconds, with the first
     ``warmup_launches`` launches of each group dropped."""
     rows = list(csv.DictReader(open(one_csv(trace_dir, "kernel_trace.csv"))))
@@ -65,9 +65,9 @@ def kernel_table(trace_dir: str, warmup_launches: int):
         groups.setdefault(key, []).append(dur)
     out = []
     for (name, grid), d in groups.items():
-        if phase_of(name) == "aligner":
-            # one call is two launches of the same kernel (the two products of the MLP), which may
-            # share a grid: split them by their order within the call
+        if phase_of(name) == "aligner" and aligner_calls and len(d) == 2 * aligner_calls:
+            # both products of the MLP ran on this kernel (two launches per call, possibly with
+            # the same grid): split them by their order within the call
             d = d[2 * warmup_launches:] or d
             for i, part in enumerate(("first product", "second product")):
                 di = d[i::2]
@@ -131,7 +131,14 @@ def main():
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
 
     if args.trace:
-        tab = kernel_table(args.trace, args.warmup_launches)
+        aligner_calls = 0
+        if args.bench_log:
+            for line in open(args.bench_log):
+                if line.startswith("{"):
+                    rec = json.loads(line)
+                    aligner_calls = rec["steps"] + rec["warmup"] if "aligner" in rec else 0
+                    break
+        tab = kernel_table(args.trace, args.warmup_launches, aligner_calls)
         lines = [f"# Codec kernels, {wl.name} (T={wl.n_tokens}, L={wl.n_layers}, d={wl.d_model}, "
                  f"{wl.n_kv_heads}x{wl.head_dim}, r={sorted(set(wl.ranks))}, Patch layers "
                  f"{list(wl.patch_layers)})", "",

@@ -532,14 +532,37 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
   scd::GemmParams base = base_params(model, batch, T, 1, nullptr, 0);
   const int bm = fast ? scd::kPatchBM : scd::kGenericBM, bn = fast ? scd::kPatchBN : scd::kGenericBN;
   // act = SiLU(z_h w1^T + b1) for every Patch layer, then h_hat = act w2^T + b2
+  std::vector<scd::GemmJob> first_jobs;
   JobPacker first(base, bm, bn), second(base, bm, bn);
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
-    first.add({z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
-               scd::kVecOut | scd::kSiluOut, 0});
+    const scd::GemmJob j1{z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
+                          scd::kVecOut | scd::kSiluOut, 0};
+    first_jobs.push_back(j1);
+    first.add(j1);
     second.add({act[l], w2[l], h_hat[l], b2 ? b2[l] : nullptr, d, hidden, scd::kVecOut, 0});
   }
+  // The first product is a short contraction (K = r_H) whose time is writing act: the shape of a
+  // Reuse decode (code x basis + offset), so the bf16 decode kernel takes it when it can.
+  bool decode_first = model->dtype == SCD_BF16 && hidden % 128 == 0 &&
+                      (model->head_dim == 64 || model->head_dim == 128) &&
+                      batch->n_seqs <= scd::kMaxLdsSeqs;
+  for (const auto& j : first_jobs)
+    if (j.k % 32 != 0 || j.k > 128) decode_first = false;
+  if (decode_first) {
+    for (const auto& grp : group_by(first_jobs, [](const scd::GemmJob& j) { return j.k; })) {
+      const int nhg = scd::decode_channel_groups(grp[0].k, hidden);
+      JobPacker jp(base, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
+      for (const auto& j : grp) jp.add(j);
+      for (const auto& lp : jp.build()) {
+        const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream, true);
+        if (e != hipSuccess)
+          return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
+      }
+    }
+  }
   for (JobPacker* jp : {&first, &second}) {
+    if (jp == &first && decode_first) continue;
     if (!fast) {
       SCD_TRY(run(scd::Op::kPatchAlign, jp->build(), model->dtype, stream));
       continue;

@@ -47,6 +47,7 @@ struct DecodeCtx {
   uint16_t* C;           // output rows [M, N]
   int64_t M;
   int N, n0;             // row width, first channel of the chunk
+  bool silu;             // SiLU after the offset (the aligner's first product; never with RoPE)
 };
 
 // One tile: the TT rows from row t0 of the current layer-branch, channels [n0, n0 + 128 NHG).
@@ -133,6 +134,15 @@ __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch&
             a[r] += acc[S][r];
             b[r] += acc[S + PS][r];
           }
+          if constexpr (!ROPE) {
+            if (c.silu) {
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                a[r] = a[r] / (1.f + __expf(-a[r]));
+                b[r] = b[r] / (1.f + __expf(-b[r]));
+              }
+            }
+          }
           if constexpr (ROPE) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -161,8 +171,8 @@ __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch&
 // with every workgroup busy to the end.  A workgroup stages a layer-branch's basis chunk once,
 // when its share enters that layer-branch.
 template <int KCH, int NHG, int DH, bool ROPE>
-__global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16_kernel(
-    GemmParams p) {
+__device__ __forceinline__ void decode_body(const GemmParams& p, uint16_t* lds,
+                                            LdsBatch& lbatch) {
   constexpr int kWaves = waves_for(NHG, KCH);
   constexpr int kThreads = 64 * kWaves;
   constexpr int kTT = 32 * kWaves;
@@ -171,8 +181,6 @@ __global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16
   constexpr int LDK = K + 8;
   constexpr int HALF = DH / 2;
   constexpr int DSTRIDE = HALF + 2;
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  __shared__ LdsBatch lbatch;
   uint16_t* Fs = lds;                                                   // [CN][LDK]
   uint16_t* mus = Fs + CN * LDK;                                        // [CN]
   float2* dtab = reinterpret_cast<float2*>(mus + CN);                   // [kDRows][DSTRIDE]
@@ -222,6 +230,7 @@ __global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16
       const uint16_t* F = static_cast<const uint16_t*>(job.b);
       const uint16_t* mu = static_cast<const uint16_t*>(job.vec);
       const bool add_mu = (job.flags & kVecOut) != 0 && mu != nullptr;
+      c.silu = (job.flags & kSiluOut) != 0;
       dma_rows(Fs, CN, K / 8, LDK / 8, wave, kWaves, lane,
                [&](int rho) { return F + static_cast<int64_t>(c.n0 + row_of_lds(rho)) * K; });
       if (tid < CN / 8) {
@@ -241,6 +250,42 @@ __global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16
     // registers)
     decode_tile<KCH, NHG, DH, ROPE, false>(p, lbatch, c, t0, Fs, mus, dtab, lane, wave);
   }
+}
+
+template <int KCH, int NHG, int DH, bool ROPE>
+__global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void reuse_decode_bf16_kernel(
+    GemmParams p) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  __shared__ LdsBatch lbatch;
+  decode_body<KCH, NHG, DH, ROPE>(p, lds, lbatch);
+}
+
+// The aligner's first product (act = SiLU(z_h w1^T + b1)) on the same body: a short contraction
+// whose time is writing its output, like the Reuse decode; its own symbol so that profiles keep
+// the two steps apart.
+template <int KCH, int NHG, int DH>
+__global__ __launch_bounds__(64 * waves_for(NHG, KCH), 2) void patch_align_act_bf16_kernel(
+    GemmParams p) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  __shared__ LdsBatch lbatch;
+  decode_body<KCH, NHG, DH, false>(p, lds, lbatch);
+}
+
+template <int NHG, int DH>
+hipError_t launch_align_kch(int kch, const GemmParams& p, int grid_size, size_t lds,
+                            hipStream_t stream) {
+  switch (kch) {
+#define SCD_ALIGN_CASE(KC)                                                                     \
+  case KC:                                                                                     \
+    hipLaunchKernelGGL((patch_align_act_bf16_kernel<KC, NHG, DH>), dim3(grid_size),           \
+                       dim3(64 * waves_for(NHG, KC)), lds, stream, p);                        \
+    return hipGetLastError();
+    SCD_ALIGN_CASE(1) SCD_ALIGN_CASE(2) SCD_ALIGN_CASE(3) SCD_ALIGN_CASE(4)
+#undef SCD_ALIGN_CASE
+    default:
+      break;
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int NHG, int DH, bool ROPE>
@@ -307,7 +352,7 @@ size_t decode_bf16_lds_bytes(int nhg, int rank, int head_dim) {
   return cn * (rank + 8) * 2 + cn * 2 + static_cast<size_t>(kDRows) * (head_dim / 2 + 2) * 8;
 }
 
-hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream) {
+hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream, bool align) {
   if (p.total_tiles <= 0) return hipSuccess;
   // every job of a launch has the same rank and branch
   const int rank = p.jobs[0].k;
@@ -340,10 +385,12 @@ hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream) 
   int64_t shares = static_cast<int64_t>(cus) * per_cu / n_nc;
   shares = shares < 1 ? 1 : (shares > row_tiles ? row_tiles : shares);
   const int grid_size = static_cast<int>(shares * n_nc);
+  if (align && (rope || kch > 4)) return hipErrorInvalidValue;
 #define SCD_DECODE_DISPATCH(NHG, DH)                                                    \
   if (nhg == NHG && p.head_dim == DH)                                                   \
-    return rope ? launch_kch<NHG, DH, true>(kch, p, grid_size, lds, stream)             \
-                : launch_kch<NHG, DH, false>(kch, p, grid_size, lds, stream);
+    return align  ? launch_align_kch<NHG, DH>(kch, p, grid_size, lds, stream)           \
+           : rope ? launch_kch<NHG, DH, true>(kch, p, grid_size, lds, stream)           \
+                  : launch_kch<NHG, DH, false>(kch, p, grid_size, lds, stream);
   SCD_DECODE_DISPATCH(4, 128)
   SCD_DECODE_DISPATCH(2, 128)
   SCD_DECODE_DISPATCH(1, 128)

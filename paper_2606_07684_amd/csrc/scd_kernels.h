@@ -73,7 +73,9 @@ hipError_t launch_align_bf16(const GemmParams& p, hipStream_t stream);
 // (% 32 == 0, <= 256) and one branch per launch, head_dim 64 or 128.
 int decode_channel_groups(int rank, int basis_width);
 int decode_tile_rows(int nhg, int rank);  // rows per tile of the kernel instance
-hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream);
+// align: run the aligner's first product (jobs flagged kSiluOut, rank <= 128, no RoPE) under its
+// own kernel symbol.
+hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream, bool align = false);
 
 // Largest batch (requests) the bf16 decode kernel stages in LDS.
 constexpr int kMaxLdsSeqs = 256;
