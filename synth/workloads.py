@@ -152,8 +152,13 @@ SMALL_MANY_REQUESTS = Workload("small_many_requests_bf16", 2, 128, 2, 64, _ragge
 # 64 and 192, hidden width 384 (one and a half 256-column tiles).
 SMALL_ALIGN = Workload("small_align_bf16", 3, 512, 2, 128, (300, 77, 650), (64, 128, 192), (0, 2),
                        5e5, "bf16", aligner_hidden=384)
+# Many short Reuse layers: more row tiles than the decode's one round of workgroups, so shares run
+# across layer boundaries (the basis is restaged mid-share) and every layer ends in a partial tile;
+# ranks 128 (512-channel chunks) and 256 (256-channel chunks).
+SMALL_MANY_LAYERS = Workload("small_many_layers_bf16", 72, 256, 8, 128, (300, 340),
+                             (128,) * 48 + (256,) * 24, (), 5e5, "bf16")
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
-                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN)
+                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS)
 
 
 # --------------------------------------------------------------------------------------------
