@@ -195,6 +195,70 @@ def time_aligner(wl, dev, steps, warmup, stream):
             "frac": round(ach / peak, 4), "alg_flops": flops, "alg_bytes": nbytes}
 
 
+def time_receive(wl, dev, steps, warmup, stream, model, batch, rope, inp, z_k, z_v, z_h,
+                 k_cache, v_cache):
+    """The consumer's receipt of the packed payload from pinned host memory (PCIe-inclusive;
+    reported beside the step, never as ``value``): the plain host-to-device copy of the whole
+    payload, the copy followed by the one-call decode, and ``scd_reuse_decode_streamed`` (copy by
+    layer groups on a side stream, each group decoded as it lands) for several group sizes.  HIP
+    events on ``stream``, which every variant ends on."""
+    import torch
+
+    import paper_2606_07684_amd as scd
+
+    L, T = wl.n_layers, wl.n_tokens
+    total, _ = scd.scd_payload_bytes(model, T)
+    staged = torch.empty(total, dtype=torch.uint8, device=dev)
+    pz_k, pz_v, pz_h = scd.scd_payload_views(model, T, staged)
+    for l in range(L):  # this step's codes, packed
+        for dst, src in ((pz_k, z_k), (pz_v, z_v), (pz_h, z_h)):
+            if dst[l] is not None:
+                dst[l].copy_(src[l])
+    host = torch.empty(total, dtype=torch.uint8, pin_memory=True)
+    host.copy_(staged)
+    dst = torch.empty_like(staged)
+    copy_stream = torch.cuda.Stream(device=dev)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    def copy_only():
+        with torch.cuda.stream(stream):
+            dst.copy_(host, non_blocking=True)
+
+    def receipt(group, side):
+        return scd.prepare_reuse_decode_streamed(model, batch, rope, host, dst, group,
+                                                 inp.w_dec_k, inp.w_dec_v, inp.mu_k, inp.mu_v,
+                                                 k_cache, v_cache), (copy_stream if side else stream)
+
+    copy_ms = timed(copy_only)
+    serial, cs = receipt(L, False)
+    serial_ms = timed(lambda: serial(cs, stream))
+    by_group = {}
+    for group in sorted({1, 2, 4, 8, 16, scd.DEFAULT_LAYERS_PER_GROUP}):
+        if group > L:
+            continue
+        run, cs = receipt(group, True)
+        by_group[group] = timed(lambda: run(cs, stream))
+    default = by_group[min(scd.DEFAULT_LAYERS_PER_GROUP, L)] if by_group else serial_ms
+    reuse_kv = sum(2 * T * wl.kv_width * wl.elem_bytes for l in range(L) if not wl.is_patch[l])
+    del staged, host, dst
+    return {"source": "pinned host memory", "payload_bytes": total,
+            "layers_per_group": scd.DEFAULT_LAYERS_PER_GROUP,
+            "copy_ms": round(copy_ms, 4), "h2d_GBps": round(total / (copy_ms * 1e-3) / 1e9, 2),
+            "copy_then_decode_ms": round(serial_ms, 4), "streamed_ms": round(default, 4),
+            "streamed_ms_by_group": {str(k): round(v, 4) for k, v in by_group.items()},
+            "reuse_kv_GBps_pcie_inclusive": round(reuse_kv / (default * 1e-3) / 1e9, 2)}
+
+
 def copy_ceiling(dev, gib=1.0, reps=10):
     """Attainable HBM bandwidth on this GPU: a plain device-to-device copy of ``gib`` GiB (read +
     write bytes over time), timed with HIP events on the current stream."""
@@ -224,6 +288,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-receive", action="store_true",
+                    help="skip the receipt timing (its decode launches share the step's kernel "
+                         "and grid, so kernel traces of the step leave it out)")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run a plain copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -356,6 +423,11 @@ def main():
     # step count, reported beside the step and not part of ``value``.
     if any(wl.is_patch):
         out["aligner"] = time_aligner(wl, dev, args.steps, args.warmup, stream)
+
+    # The consumer's receipt from host memory (PCIe-inclusive), beside the step.
+    if not args.no_receive:
+        out["receive"] = time_receive(wl, dev, args.steps, args.warmup, stream, model, batch, rope,
+                                      inp, z_k, z_v, z_h, k_cache, v_cache)
 
     # The combined readings of the decode-side target (Reuse decode + Patch at this workload):
     #   reuse_hbm_frac:   Reuse algorithmic bytes / t_reuse / 8 TB/s

@@ -184,6 +184,40 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
                              const void* const* w2, const void* const* b2,
                              void* const* act, void* const* h_hat, hipStream_t stream);
 
+/* ---- packed payload and streamed receipt (Algorithm 1's transmitted set; Section 4.5) ---------
+ * The codes Algorithm 1 sends travel as one contiguous buffer in the layout scd_payload_bytes
+ * describes: layers in order, a Reuse layer's K codes [T*g, rank_k] then its V codes
+ * [T*g, rank_v], a Patch layer's code [T, rank_h], no padding.
+ *
+ * scd_payload_views (host only, touches no memory) fills z_k, z_v, z_h [n_layers] with the
+ * addresses of each layer's codes inside `payload` (any 16-byte aligned buffer of
+ * scd_payload_bytes bytes), NULL for the branches a layer does not have.  The arrays can be passed
+ * as they are to scd_encode (which then writes the packed payload), scd_reuse_decode and
+ * scd_patch_align.
+ *
+ * scd_reuse_decode_streamed is the consumer's receipt: it copies the whole payload from
+ * payload_src (pinned host memory, or device memory of this or a peer device; any address
+ * hipMemcpyDefault accepts; pageable host memory works but serialises the copies) to payload_dst
+ * (device, 16-byte aligned, scd_payload_bytes bytes, not overlapping payload_src) in groups of
+ * layers_per_group layers on copy_stream, and enqueues the Reuse decode of each group (as
+ * scd_reuse_decode, reading the codes from payload_dst) on `stream` behind that group's copy, so
+ * the decode of one group overlaps the copy of the next.  The copies start after the work already
+ * queued on `stream`; on return `stream` is ordered after every copy, so work queued on it next
+ * (the aligner and scd_patch_kv on the Patch layers' codes) sees the whole payload.  copy_stream
+ * may equal `stream` (no overlap).  With no tokens the payload is empty and both payload
+ * pointers may be NULL.  The other arguments are scd_reuse_decode's.  SCD_ERR_HIP can leave
+ * earlier groups enqueued; every other error means nothing was enqueued. */
+scd_status_t scd_payload_views(const scd_model_t* model, int64_t n_tokens, void* payload,
+                               void** z_k, void** z_v, void** z_h);
+scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch_t* batch,
+                                       const void* rope_table, int64_t max_position,
+                                       const void* payload_src, void* payload_dst,
+                                       int32_t layers_per_group,
+                                       const void* const* w_dec_k, const void* const* w_dec_v,
+                                       const void* const* mu_k, const void* const* mu_v,
+                                       void* const* k_cache, void* const* v_cache,
+                                       hipStream_t copy_stream, hipStream_t stream);
+
 /* ---- diagnostics ---------------------------------------------------------------------------- */
 const char* scd_status_string(scd_status_t status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */

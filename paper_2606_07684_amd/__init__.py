@@ -28,13 +28,19 @@ __all__ = [
     "scd_rope_table", "scd_positions", "scd_schedule", "scd_payload_bytes",
     "scd_encode", "scd_reuse_decode", "scd_patch_kv", "scd_abi_version",
     "Prepared", "prepare_encode", "prepare_reuse_decode", "prepare_patch_kv",
-    "scd_patch_align", "prepare_patch_align",
+    "scd_patch_align", "prepare_patch_align", "scd_payload_views",
+    "scd_reuse_decode_streamed", "prepare_reuse_decode_streamed", "PreparedStreamed",
+    "DEFAULT_LAYERS_PER_GROUP",
 ]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
 
 SCD_F32, SCD_BF16 = 0, 1
+# Layers per copy of the streamed receipt.  Each group boundary costs the copy stream a few tens
+# of microseconds (the event between two copies), and the last group's decode is not overlapped;
+# at 32 layers of 8K tokens, 8 layers per group balances the two.
+DEFAULT_LAYERS_PER_GROUP = 8
 _STATUS_NAMES = {0: "SCD_OK", 1: "SCD_ERR_NULL", 2: "SCD_ERR_SHAPE", 3: "SCD_ERR_SCHEDULE",
                  4: "SCD_ERR_ALIGN", 5: "SCD_ERR_UNSUPPORTED", 6: "SCD_ERR_WORKSPACE",
                  7: "SCD_ERR_HIP"}
@@ -100,6 +106,12 @@ _SIGS = {
                                     ctypes.c_int64] + [_PP] * 7 + [_VP]),
     "scd_patch_align": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.POINTER(_CBatch),
                                        ctypes.c_int32] + [_PP] * 7 + [_VP]),
+    "scd_payload_views": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int64, _VP,
+                                         _PP, _PP, _PP]),
+    "scd_reuse_decode_streamed": (ctypes.c_int, [ctypes.POINTER(_CModel),
+                                                 ctypes.POINTER(_CBatch), _VP, ctypes.c_int64,
+                                                 _VP, _VP, ctypes.c_int32] + [_PP] * 6
+                                  + [_VP, _VP]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -178,6 +190,10 @@ class Model:
     @property
     def torch_dtype(self):
         return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
 
 
 @dataclasses.dataclass
@@ -418,3 +434,87 @@ def prepare_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2
 def scd_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2, b2, act, h_hat,
                     stream=None) -> None:
     prepare_patch_align(model, batch, hidden, z_h, w1, b1, w2, b2, act, h_hat)(stream)
+
+
+def _payload_buffer(t, name: str, nbytes: int, need_cuda: bool) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.uint8 or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous uint8 tensor")
+    if need_cuda and not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA tensor")
+    if t.numel() < nbytes:
+        raise ValueError(f"{name} holds {t.numel()} bytes, the payload needs {nbytes}")
+    return t
+
+
+def scd_payload_views(model: Model, n_tokens: int, payload: torch.Tensor):
+    """Per-layer code tensors inside one packed payload buffer (uint8, scd_payload_bytes bytes):
+    returns (z_k, z_v, z_h), lists of n_layers entries, None where a layer has no such branch.
+    The addresses come from the library; the views only wrap them."""
+    lib = load_library()
+    L, T, g = model.n_layers, int(n_tokens), model.g
+    total, _ = scd_payload_bytes(model, T)
+    _payload_buffer(payload, "payload", total, need_cuda=False)
+    arrs = [(ctypes.c_void_p * L)() for _ in range(3)]
+    _check(lib.scd_payload_views(ctypes.byref(model._c), T, payload.data_ptr(),
+                                 *[_as_pp(a) for a in arrs]))
+    base, dt, eb = payload.data_ptr(), model.torch_dtype, model.elem_bytes
+    shapes = (lambda l: (T * g, model.rank_k[l]), lambda l: (T * g, model.rank_v[l]),
+              lambda l: (T, model.rank_h[l]))
+    views = []
+    for arr, shape in zip(arrs, shapes):
+        out = []
+        for l in range(L):
+            if not arr[l]:
+                out.append(None)
+                continue
+            rows, cols = shape(l)
+            off = arr[l] - base
+            out.append(payload[off:off + rows * cols * eb].view(dt).view(rows, cols))
+        views.append(out)
+    return tuple(views)
+
+
+def prepare_reuse_decode_streamed(model: Model, batch: Batch, rope: Optional[RopeTable],
+                                  payload_src: torch.Tensor, payload_dst: torch.Tensor,
+                                  layers_per_group: int, w_dec_k, w_dec_v, mu_k, mu_v, k_cache,
+                                  v_cache) -> "PreparedStreamed":
+    """Receipt of a packed payload: copy it from payload_src (pinned host or device memory) to
+    payload_dst (device) in groups of layers_per_group layers on the copy stream, decoding each
+    group's Reuse layers on the compute stream as soon as it has landed."""
+    lib = load_library()
+    L, T, D, w = model.n_layers, batch.n_tokens, model.kv_width, model.basis_width
+    dt = model.torch_dtype
+    total, _ = scd_payload_bytes(model, T)
+    _payload_buffer(payload_src, "payload_src", total, need_cuda=False)
+    _payload_buffer(payload_dst, "payload_dst", total, need_cuda=True)
+    R = [l for l in range(L) if not model.is_patch[l]]
+    args = [
+        _ptr_array(w_dec_k, L, "w_dec_k", {l: (w, model.rank_k[l]) for l in R}, dt),
+        _ptr_array(w_dec_v, L, "w_dec_v", {l: (w, model.rank_v[l]) for l in R}, dt),
+        _ptr_array(mu_k, L, "mu_k", {l: (w,) for l in R}, dt),
+        _ptr_array(mu_v, L, "mu_v", {l: (w,) for l in R}, dt),
+        _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in R}, dt),
+        _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in R}, dt),
+    ]
+    tab, maxp = _rope_args(rope)
+    return PreparedStreamed(lib.scd_reuse_decode_streamed,
+                            (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
+                             payload_src.data_ptr(), payload_dst.data_ptr(),
+                             int(layers_per_group), *[_as_pp(a) for a in args]),
+                            (model, batch, rope, payload_src, payload_dst, args))
+
+
+class PreparedStreamed(Prepared):
+    """A prepared streamed receipt: called with (copy_stream, stream)."""
+
+    def __call__(self, copy_stream=None, stream=None) -> None:
+        _check(self._fn(*self._args, _stream(copy_stream), _stream(stream)))
+
+
+def scd_reuse_decode_streamed(model: Model, batch: Batch, rope: Optional[RopeTable],
+                              payload_src, payload_dst, layers_per_group: int, w_dec_k, w_dec_v,
+                              mu_k, mu_v, k_cache, v_cache, copy_stream=None,
+                              stream=None) -> None:
+    prepare_reuse_decode_streamed(model, batch, rope, payload_src, payload_dst,
+                                  layers_per_group, w_dec_k, w_dec_v, mu_k, mu_v, k_cache,
+                                  v_cache)(copy_stream, stream)

@@ -1,8 +1,9 @@
 // Host side of the SCD codec's C ABI: argument validation, routing, job tables and launches.
 //
 // Every entry point validates all of its arguments before the first launch, so a non-OK status
-// means nothing ran.  No entry point allocates, synchronises or keeps state beyond the
-// thread-local text of the last error.
+// other than SCD_ERR_HIP means nothing ran.  No entry point allocates device memory, synchronises
+// or keeps state beyond the thread-local text of the last error; the streamed decode creates (and
+// releases) the events that order its copies and launches.
 #include "../../include/scd.h"
 
 #include <cstdarg>
@@ -208,7 +209,7 @@ int64_t kv_width(const scd_model_t* m) {
 
 extern "C" {
 
-int32_t scd_abi_version(void) { return 2; }
+int32_t scd_abi_version(void) { return 3; }
 
 const char* scd_status_string(scd_status_t s) {
   switch (s) {
@@ -377,16 +378,18 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
   return run(scd::Op::kEncodeH, hp.build(), model->dtype, stream);
 }
 
-scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
-                              const void* rope_table, int64_t max_position,
-                              const void* const* z_k, const void* const* z_v,
-                              const void* const* w_dec_k, const void* const* w_dec_v,
-                              const void* const* mu_k, const void* const* mu_v,
-                              void* const* k_cache, void* const* v_cache, hipStream_t stream) {
+namespace {
+
+// Validation half of the Reuse decode; *any is set when the model has a Reuse layer.
+scd_status_t check_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
+                                const void* rope_table, int64_t max_position,
+                                const void* const* z_k, const void* const* z_v,
+                                const void* const* w_dec_k, const void* const* w_dec_v,
+                                const void* const* mu_k, const void* const* mu_v,
+                                void* const* k_cache, void* const* v_cache, bool* any_out) {
   SCD_TRY(check_model(model));
   SCD_TRY(check_batch(batch));
   const int w = model->basis_width;
-  const int g = static_cast<int>(kv_width(model) / w);
   const int rk_max = w < 256 ? w : 256;
   bool any = false;
   for (int l = 0; l < model->n_layers; ++l) {
@@ -405,8 +408,20 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
     SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache", batch->n_tokens));
   }
   if (any && batch->n_tokens > 0) SCD_TRY(check_rope(rope_table, max_position));
-  if (!any || batch->n_tokens == 0) return ok();
+  *any_out = any;
+  return SCD_OK;
+}
 
+// Launch half of the Reuse decode, on arguments check_reuse_decode accepted.
+scd_status_t enqueue_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
+                                  const void* rope_table, int64_t max_position,
+                                  const void* const* z_k, const void* const* z_v,
+                                  const void* const* w_dec_k, const void* const* w_dec_v,
+                                  const void* const* mu_k, const void* const* mu_v,
+                                  void* const* k_cache, void* const* v_cache,
+                                  hipStream_t stream) {
+  const int w = model->basis_width;
+  const int g = static_cast<int>(kv_width(model) / w);
   const int64_t T = batch->n_tokens;
   bool fast = model->dtype == SCD_BF16 && (model->head_dim == 64 || model->head_dim == 128) &&
               w % 128 == 0 && batch->n_seqs <= scd::kMaxLdsSeqs;
@@ -439,6 +454,151 @@ scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch
       if (e != hipSuccess)
         return fail(SCD_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
     }
+  }
+  return SCD_OK;
+}
+
+}  // namespace
+
+scd_status_t scd_reuse_decode(const scd_model_t* model, const scd_batch_t* batch,
+                              const void* rope_table, int64_t max_position,
+                              const void* const* z_k, const void* const* z_v,
+                              const void* const* w_dec_k, const void* const* w_dec_v,
+                              const void* const* mu_k, const void* const* mu_v,
+                              void* const* k_cache, void* const* v_cache, hipStream_t stream) {
+  bool any = false;
+  SCD_TRY(check_reuse_decode(model, batch, rope_table, max_position, z_k, z_v, w_dec_k, w_dec_v,
+                             mu_k, mu_v, k_cache, v_cache, &any));
+  if (!any || batch->n_tokens == 0) return ok();
+  SCD_TRY(enqueue_reuse_decode(model, batch, rope_table, max_position, z_k, z_v, w_dec_k,
+                               w_dec_v, mu_k, mu_v, k_cache, v_cache, stream));
+  return ok();
+}
+
+scd_status_t scd_payload_views(const scd_model_t* model, int64_t n_tokens, void* payload,
+                               void** z_k, void** z_v, void** z_h) {
+  SCD_TRY(check_model(model));
+  if (n_tokens < 0) return fail(SCD_ERR_SHAPE, "n_tokens must be >= 0");
+  if (payload == nullptr) return fail(SCD_ERR_NULL, "payload is NULL");
+  if (!aligned16(payload)) return fail(SCD_ERR_ALIGN, "payload is not 16-byte aligned");
+  if (z_k == nullptr || z_v == nullptr || z_h == nullptr)
+    return fail(SCD_ERR_NULL, "view arrays must not be NULL");
+  const int w = model->basis_width;
+  const int rk_max = w < 256 ? w : 256;
+  const int rh_max = model->d_model < 256 ? model->d_model : 256;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) {
+      SCD_TRY(check_rank("rank_h", l, model->rank_h[l], rh_max));
+    } else {
+      SCD_TRY(check_rank("rank_k", l, model->rank_k[l], rk_max));
+      SCD_TRY(check_rank("rank_v", l, model->rank_v[l], rk_max));
+    }
+  }
+  // Ranks are multiples of 16, so every view below inherits the base's 16-byte alignment.
+  const int64_t g = kv_width(model) / w;
+  const int64_t eb = model->dtype == SCD_BF16 ? 2 : 4;
+  char* base = static_cast<char*>(payload);
+  int64_t off = 0;
+  for (int l = 0; l < model->n_layers; ++l) {
+    z_k[l] = z_v[l] = z_h[l] = nullptr;
+    if (model->is_patch[l]) {
+      z_h[l] = base + off;
+      off += n_tokens * model->rank_h[l] * eb;
+    } else {
+      z_k[l] = base + off;
+      off += n_tokens * g * model->rank_k[l] * eb;
+      z_v[l] = base + off;
+      off += n_tokens * g * model->rank_v[l] * eb;
+    }
+  }
+  return ok();
+}
+
+namespace {
+
+// Owns the events of one streamed call; destroying a recorded event is safe (HIP releases it once
+// the recorded work completes).
+struct EventSet {
+  std::vector<hipEvent_t> ev;
+  ~EventSet() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
+  hipError_t add(hipEvent_t* out) {
+    const hipError_t e = hipEventCreateWithFlags(out, hipEventDisableTiming);
+    if (e == hipSuccess) ev.push_back(*out);
+    return e;
+  }
+};
+
+}  // namespace
+
+scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch_t* batch,
+                                       const void* rope_table, int64_t max_position,
+                                       const void* payload_src, void* payload_dst,
+                                       int32_t layers_per_group,
+                                       const void* const* w_dec_k, const void* const* w_dec_v,
+                                       const void* const* mu_k, const void* const* mu_v,
+                                       void* const* k_cache, void* const* v_cache,
+                                       hipStream_t copy_stream, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  if (layers_per_group < 1)
+    return fail(SCD_ERR_SHAPE, "layers_per_group must be >= 1 (got %d)", layers_per_group);
+  const int L = model->n_layers;
+  const int64_t T = batch->n_tokens;
+  std::vector<int64_t> offs(L + 1);
+  const size_t total = scd_payload_bytes(model, T, offs.data());
+  std::vector<void*> zk(L, nullptr), zv(L, nullptr), zh(L, nullptr);
+  if (total > 0) {  // an empty payload (no tokens) may come with NULL buffers
+    if (payload_src == nullptr) return fail(SCD_ERR_NULL, "payload_src is NULL");
+    if (payload_dst == nullptr) return fail(SCD_ERR_NULL, "payload_dst is NULL");
+    SCD_TRY(scd_payload_views(model, T, payload_dst, zk.data(), zv.data(), zh.data()));
+  }
+  bool any = false;
+  SCD_TRY(check_reuse_decode(model, batch, rope_table, max_position, zk.data(), zv.data(),
+                             w_dec_k, w_dec_v, mu_k, mu_v, k_cache, v_cache, &any));
+  if (total == 0) return ok();
+
+  auto hip_fail = [](const char* what, hipError_t e) {
+    return fail(SCD_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
+  };
+  EventSet events;
+  hipEvent_t ready;  // work already queued on stream (producer of payload_src, readers of dst)
+  hipError_t e = events.add(&ready);
+  if (e != hipSuccess) return hip_fail("event creation", e);
+  if ((e = hipEventRecord(ready, stream)) != hipSuccess) return hip_fail("event record", e);
+  if ((e = hipStreamWaitEvent(copy_stream, ready, 0)) != hipSuccess)
+    return hip_fail("stream wait", e);
+
+  const char* src = static_cast<const char*>(payload_src);
+  char* dst = static_cast<char*>(payload_dst);
+  for (int l0 = 0; l0 < L; l0 += layers_per_group) {
+    const int l1 = l0 + layers_per_group < L ? l0 + layers_per_group : L;
+    const int64_t bytes = offs[l1] - offs[l0];
+    if (bytes == 0) continue;
+    if ((e = hipMemcpyAsync(dst + offs[l0], src + offs[l0], static_cast<size_t>(bytes),
+                            hipMemcpyDefault, copy_stream)) != hipSuccess)
+      return hip_fail("payload copy", e);
+    hipEvent_t landed;
+    if ((e = events.add(&landed)) != hipSuccess) return hip_fail("event creation", e);
+    if ((e = hipEventRecord(landed, copy_stream)) != hipSuccess) return hip_fail("event record", e);
+    if ((e = hipStreamWaitEvent(stream, landed, 0)) != hipSuccess)
+      return hip_fail("stream wait", e);
+    if (!any || T == 0) continue;
+    // the group's layers as a model of their own: routing and rank arrays start at l0
+    scd_model_t sub = *model;
+    sub.n_layers = l1 - l0;
+    sub.is_patch += l0;
+    sub.rank_k += l0;
+    sub.rank_v += l0;
+    sub.rank_h += l0;
+    bool sub_any = false;
+    for (int l = l0; l < l1; ++l) sub_any = sub_any || !model->is_patch[l];
+    if (!sub_any) continue;
+    SCD_TRY(enqueue_reuse_decode(&sub, batch, rope_table, max_position, zk.data() + l0,
+                                 zv.data() + l0, w_dec_k + l0, w_dec_v + l0,
+                                 mu_k ? mu_k + l0 : nullptr, mu_v ? mu_v + l0 : nullptr,
+                                 k_cache + l0, v_cache + l0, stream));
   }
   return ok();
 }

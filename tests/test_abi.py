@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), f"libscd.so does not export {n}"
     assert set(names) == set(scd.EXPORTED_SYMBOLS)
-    assert scd.scd_abi_version() == 2
+    assert scd.scd_abi_version() == 3
 
 
 def test_status_strings(lib):
@@ -220,3 +220,84 @@ def test_workload_shapes_are_the_stated_ones():
     assert W.LLAMA3_70B.patch_layers == tuple(range(0, 80, 10))
     assert W.QWEN2_7B.n_tokens == 32768 and W.QWEN2_7B.kv_width == 512
     assert W.TINY_F32.kv_width == 256 and W.TINY_F32.is_patch == (0, 0, 1, 0)
+
+
+def _wl_model(wl):
+    return scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
+                     head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
+                     is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
+                     basis_width=wl.w)
+
+
+@pytest.mark.parametrize("wl", [*W.CONFIGS, *W.TEST_WORKLOADS], ids=lambda w: w.name)
+def test_payload_views_tile_the_packed_buffer(wl):
+    """The per-layer views the library hands out start at the oracle's layer offsets, keep K
+    before V, and cover the packed buffer exactly once: no gap, no overlap, nothing past the end."""
+    import torch
+    m = _wl_model(wl)
+    T = wl.n_tokens
+    total, offs = O.payload_bytes(wl.is_patch, T, wl.n_kv_heads, wl.head_dim, wl.w, wl.ranks,
+                                  wl.rank_v, wl.ranks, wl.elem_bytes)
+    buf = torch.empty(total + 64, dtype=torch.uint8)
+    base = buf.data_ptr()
+    assert base % 16 == 0
+    z_k, z_v, z_h = scd.scd_payload_views(m, T, buf)
+    spans = []
+    for l, p in enumerate(wl.is_patch):
+        if p:
+            assert z_k[l] is None and z_v[l] is None
+            assert z_h[l].data_ptr() - base == offs[l]
+            assert tuple(z_h[l].shape) == (T, wl.ranks[l])
+            spans.append(z_h[l])
+        else:
+            assert z_h[l] is None
+            assert z_k[l].data_ptr() - base == offs[l]
+            assert z_v[l].data_ptr() > z_k[l].data_ptr()
+            spans += [z_k[l], z_v[l]]
+    pos = base
+    for t in spans:
+        assert t.data_ptr() == pos and t.data_ptr() % 16 == 0
+        assert t.dtype == m.torch_dtype and t.is_contiguous()
+        pos += t.numel() * t.element_size()
+    assert pos == base + total
+
+
+def test_payload_views_and_streamed_decode_validation(lib):
+    m = _model()
+    b = _batch()
+    L = m.n_layers
+    views = [(ctypes.c_void_p * L)() for _ in range(3)]
+    vp = [ctypes.cast(v, ctypes.POINTER(ctypes.c_void_p)) for v in views]
+    assert lib.scd_payload_views(ctypes.byref(m._c), 10, FAKE, *vp) == OK
+    assert views[0][1] is None and views[2][1] == FAKE + 10 * 64 * 2
+    assert lib.scd_payload_views(ctypes.byref(m._c), 10, FAKE + 8, *vp) == ALIGN
+    assert lib.scd_payload_views(ctypes.byref(m._c), 10, None, *vp) == NULL
+    assert lib.scd_payload_views(ctypes.byref(m._c), -1, FAKE, *vp) == SHAPE
+    assert lib.scd_payload_views(ctypes.byref(m._c), 10, FAKE, vp[0], None, vp[2]) == NULL
+    assert lib.scd_payload_views(ctypes.byref(_model(rank_h=[32, 24, 32])._c), 10, FAKE,
+                                 *vp) == SCHED
+
+    def streamed(model=m, batch=b, src=FAKE, dst=FAKE, group=2, **over):
+        keep, args = [], []
+        for name in ("w_dec_k", "w_dec_v", "mu_k", "mu_v", "k_cache", "v_cache"):
+            if name in over:
+                args.append(over[name])
+            else:
+                p, a = _ptrs(model.n_layers)
+                keep.append(a)
+                args.append(p)
+        st = lib.scd_reuse_decode_streamed(ctypes.byref(model._c), ctypes.byref(batch._c), FAKE,
+                                           100, src, dst, group, *args, None, None)
+        return st, lib.scd_last_error().decode()
+
+    assert streamed(group=0)[0] == SHAPE
+    assert streamed(src=None)[0] == NULL
+    assert streamed(dst=None)[0] == NULL
+    assert streamed(dst=FAKE + 8)[0] == ALIGN
+    q, keepq = _ptrs(L, skip=(2,))
+    st, msg = streamed(w_dec_v=q)
+    assert st == NULL and "w_dec_v[2]" in msg
+    assert streamed(model=_model(rank_k=[32, 32, 40]))[0] == SCHED
+    # no tokens: an empty payload, nothing to copy or decode, no HIP call
+    assert streamed(batch=_batch(n_tokens=0))[0] == OK
+    assert streamed(batch=_batch(n_tokens=0), src=None, dst=None)[0] == OK
