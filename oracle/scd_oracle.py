@@ -296,3 +296,68 @@ def assemble(is_patch, reuse_kv, patch_kv):
         out_k.append(pk[l] if p else rk[l])
         out_v.append(pv[l] if p else rv[l])
     return out_k, out_v
+
+
+# --------------------------------------------------------------------------------------------
+# Offline Reuse fit (Section 4.3.1 "Joint Subspace Learning"; Appendix F.1 "Reuse: Layer-wise
+# Stack-SVD with Ridge Regression").  For one layer and branch the producer's and consumer's
+# calibration tensors of the same prefixes are flattened into rows A, B [N, w] (keys de-rotated
+# first), a truncated SVD of the joint matrix X = [A B] finds the shared rank-r latent space, and
+# ridge regressions fit the producer encoder (A -> Z) and the consumer decoder (Z -> B).
+# Readings taken where the paper is open:
+#   * latents Z = X V_r (= U_r S_r): the decoders carry the orthonormal right singular vectors and
+#     the codes carry the scale;
+#   * the decoder is a ridge fit as well, with the same lambda (lambda = 0 gives the SVD factor);
+#   * optional centring: A and B lose their column means first; the means become the encoder's
+#     and decoder's offsets (the codec subtracts the encoder offset and adds the decoder offset);
+#   * each singular vector's sign is fixed so that its entry of largest magnitude is positive
+#     (the first such entry on ties).
+# --------------------------------------------------------------------------------------------
+def fit_rows(x, pos, n_kv_heads, head_dim, theta, basis_width, derope):
+    """Calibration rows ``[N, w]`` of one model's cache ``x [T, D]``: de-rotated for keys."""
+    if derope:
+        x = rope(x, pos, n_kv_heads, head_dim, theta, inverse=True)
+    return to_rows(x, basis_width)
+
+
+def fit_gram(a, b, pos, n_kv_heads, head_dim, theta, basis_width, derope):
+    """``G = X^T X`` and ``s = 1^T X`` of the joint rows ``X = [A B]`` (no centring)."""
+    x = np.concatenate([fit_rows(a, pos, n_kv_heads, head_dim, theta, basis_width, derope),
+                        fit_rows(b, pos, n_kv_heads, head_dim, theta, basis_width, derope)], axis=1)
+    return x.T @ x, x.sum(axis=0)
+
+
+def sign_fix(v):
+    """Flip each column of ``v`` so that its entry of largest magnitude is positive."""
+    v = _f64(v).copy()
+    idx = np.argmax(np.abs(v), axis=0)
+    sgn = np.sign(v[idx, np.arange(v.shape[1])])
+    sgn[sgn == 0] = 1.0
+    return v * sgn[None, :]
+
+
+def fit_reuse(a, b, pos, n_kv_heads, head_dim, theta, basis_width, derope, rank, lam,
+              center=True):
+    """Fit one layer's Reuse translator from paired caches ``a`` (producer) and ``b`` (consumer).
+
+    Steps in the paper's order: de-rotate keys; flatten to rows A, B; (centre); truncated SVD of
+    X = [A B] keeping ``rank`` right singular vectors V_r; latents Z = X V_r; ridge encoder
+    ``E = argmin ||A E - Z||^2 + lam ||E||^2`` and ridge decoder
+    ``F = argmin ||Z F - B||^2 + lam ||F||^2``.  Returned in the codec's storage:
+    ``(W_enc [r, w] = E^T, W_dec [w, r] = F^T, mu_enc [w], mu_dec [w])`` (offsets None unless
+    ``center``).
+    """
+    A = fit_rows(a, pos, n_kv_heads, head_dim, theta, basis_width, derope)
+    B = fit_rows(b, pos, n_kv_heads, head_dim, theta, basis_width, derope)
+    mu_a = mu_b = None
+    if center:
+        mu_a, mu_b = A.mean(axis=0), B.mean(axis=0)
+        A, B = A - mu_a[None, :], B - mu_b[None, :]
+    X = np.concatenate([A, B], axis=1)
+    _, _, vt = np.linalg.svd(X, full_matrices=False)
+    vr = sign_fix(vt[:rank].T)
+    Z = X @ vr
+    w = A.shape[1]
+    E = np.linalg.solve(A.T @ A + lam * np.eye(w), A.T @ Z)
+    F = np.linalg.solve(Z.T @ Z + lam * np.eye(rank), Z.T @ B)
+    return E.T, F.T, mu_a, mu_b

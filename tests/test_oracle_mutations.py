@@ -19,6 +19,8 @@ _decode_v = O.decode_v
 _patch_k = O.patch_k
 _align = O.align
 _silu = O.silu
+_fit_rows = O.fit_rows
+_sign_fix = O.sign_fix
 
 
 def rope_wrong_sign(x, pos, n, dh, theta, inverse=False):
@@ -121,6 +123,49 @@ def silu_sign_flipped(x):
     return x / (1.0 + np.exp(x))
 
 
+def fit_rows_no_derope(x, pos, n, dh, theta, w, derope):
+    return _fit_rows(x, pos, n, dh, theta, w, False)
+
+
+def sign_fix_negative(v):
+    return -_sign_fix(v)
+
+
+def _fit_variant(a, b, pos, n, dh, theta, w, derope, rank, lam, center=True, *, subtract=True,
+                 scaled=True, dec_ridge=True, enc_from_b=False):
+    A = O.fit_rows(a, pos, n, dh, theta, w, derope)
+    B = O.fit_rows(b, pos, n, dh, theta, w, derope)
+    mu_a = mu_b = None
+    if center:
+        mu_a, mu_b = A.mean(axis=0), B.mean(axis=0)
+        if subtract:
+            A, B = A - mu_a[None, :], B - mu_b[None, :]
+    X = np.concatenate([A, B], axis=1)
+    _, s, vt = np.linalg.svd(X, full_matrices=False)
+    vr = O.sign_fix(vt[:rank].T)
+    Z = X @ vr if scaled else (X @ vr) / s[None, :rank]
+    src = B if enc_from_b else A
+    E = np.linalg.solve(src.T @ src + lam * np.eye(src.shape[1]), src.T @ Z)
+    F = np.linalg.solve(Z.T @ Z + (lam if dec_ridge else 0.0) * np.eye(rank), Z.T @ B)
+    return E.T, F.T, mu_a, mu_b
+
+
+def fit_not_centred(*a, **k):
+    return _fit_variant(*a, **k, subtract=False)
+
+
+def fit_unscaled_latents(*a, **k):
+    return _fit_variant(*a, **k, scaled=False)
+
+
+def fit_decoder_without_ridge(*a, **k):
+    return _fit_variant(*a, **k, dec_ridge=False)
+
+
+def fit_encoder_on_consumer(*a, **k):
+    return _fit_variant(*a, **k, enc_from_b=True)
+
+
 def _schedule_swapped(is_patch):
     flags = [bool(v) for v in is_patch]
     return [l for l, f in enumerate(flags) if f], [l for l, f in enumerate(flags) if not f]
@@ -146,6 +191,12 @@ MUTATIONS = [
     ("align", align_silu_after_output),
     ("align", align_hidden_bias_dropped),
     ("silu", silu_sign_flipped),
+    ("fit_rows", fit_rows_no_derope),
+    ("sign_fix", sign_fix_negative),
+    ("fit_reuse", fit_not_centred),
+    ("fit_reuse", fit_unscaled_latents),
+    ("fit_reuse", fit_decoder_without_ridge),
+    ("fit_reuse", fit_encoder_on_consumer),
 ]
 
 PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]

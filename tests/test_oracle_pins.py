@@ -476,3 +476,158 @@ def test_align_linear_limit_and_zero_output_layer():
     w1 = rng.standard_normal((6, r))
     y, _ = O.align(z, w1, rng.standard_normal(6), np.zeros((d, 6)), b2)
     np.testing.assert_array_equal(y, np.tile(b2, (t, 1)))
+
+
+# ------------------------------------------------------------------------------------------
+# Offline Reuse fit (Section 4.3.1; Appendix F.1)
+# ------------------------------------------------------------------------------------------
+def _sign_fix_test(v):
+    """Test-side sign convention: each column's largest-magnitude entry positive."""
+    v = np.array(v, dtype=np.float64)
+    for j in range(v.shape[1]):
+        i = int(np.argmax(np.abs(v[:, j])))
+        if v[i, j] < 0:
+            v[:, j] = -v[:, j]
+    return v
+
+
+def _exact_svd_pair(rng, n, w, sig):
+    """Joint rows X = U diag(sig) W^T with U [n, 2w] orthonormal and W [2w, 2w] orthogonal."""
+    u = rand_orthonormal(rng, n, 2 * w)
+    wm = rand_orthonormal(rng, 2 * w, 2 * w)
+    x = (u * sig[None, :]) @ wm.T
+    return x[:, :w], x[:, w:], wm
+
+
+def test_fit_gram_brute_force():
+    rng = np.random.default_rng(41)
+    T, H, dh, th = 7, 2, 4, 100.0
+    w = dh  # head-shared: two rows per token
+    a = rng.standard_normal((T, H * dh))
+    b = rng.standard_normal((T, H * dh))
+    pos = np.array([3, 4, 5, 0, 1, 2, 9])
+    G, s = O.fit_gram(a, b, pos, H, dh, th, w, derope=True)
+    ar = rope_complex(a, pos, H, dh, th, sign=-1.0)
+    br = rope_complex(b, pos, H, dh, th, sign=-1.0)
+    rows = []
+    for t in range(T):
+        for h in range(H):
+            rows.append(list(ar[t, h * dh:(h + 1) * dh]) + list(br[t, h * dh:(h + 1) * dh]))
+    n2 = 2 * w
+    G_ref = np.zeros((n2, n2))
+    s_ref = np.zeros(n2)
+    for row in rows:
+        for i in range(n2):
+            s_ref[i] += row[i]
+            for j in range(n2):
+                G_ref[i, j] += row[i] * row[j]
+    np.testing.assert_allclose(G, G_ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(s, s_ref, rtol=1e-12, atol=1e-12)
+
+
+def test_fit_matches_library_svd_and_ridge():
+    # The SVD of the joint rows (LAPACK gesvd, not the oracle's call) and scikit-learn's Ridge
+    # fix the encoder and decoder: W_enc = Ridge(A -> Z), W_dec = Ridge(Z -> B), Z = X V_r.
+    from sklearn.linear_model import Ridge
+    rng = np.random.default_rng(42)
+    N, w, r, lam = 60, 6, 3, 0.7
+    A = rng.standard_normal((N, w)) @ rng.standard_normal((w, w))
+    B = A @ rng.standard_normal((w, w)) + 0.1 * rng.standard_normal((N, w))
+    w_enc, w_dec, mu_a, mu_b = O.fit_reuse(A, B, None, 1, w, 1e4, w, False, r, lam, center=False)
+    assert mu_a is None and mu_b is None
+    X = np.concatenate([A, B], axis=1)
+    _, _, vt = scipy.linalg.svd(X, full_matrices=False, lapack_driver="gesvd")
+    vr = _sign_fix_test(vt[:r].T)
+    Z = X @ vr
+    enc = Ridge(alpha=lam, fit_intercept=False, solver="svd").fit(A, Z).coef_
+    dec = Ridge(alpha=lam, fit_intercept=False, solver="svd").fit(Z, B).coef_
+    assert w_enc.shape == (r, w) and w_dec.shape == (w, r)
+    np.testing.assert_allclose(w_enc, enc, rtol=1e-9, atol=1e-10)
+    np.testing.assert_allclose(w_dec, dec, rtol=1e-9, atol=1e-10)
+
+
+def test_fit_decoder_closed_form_on_exact_svd():
+    # X = U diag(sig) W^T by construction: the decoder is the consumer half of W's first r
+    # columns (sign-fixed), shrunk by sig^2 / (sig^2 + lam) under the ridge penalty.
+    rng = np.random.default_rng(43)
+    N, w, r = 40, 5, 3
+    sig = np.array([9.0, 6.0, 4.0, 1.0, 0.5, 0.3, 0.2, 0.1, 0.05, 0.02])
+    A, B, wm = _exact_svd_pair(rng, N, w, sig)
+    vr = _sign_fix_test(wm[:, :r])
+    for lam in (0.0, 3.0):
+        _, w_dec, _, _ = O.fit_reuse(A, B, None, 1, w, 1e4, w, False, r, lam, center=False)
+        shrink = sig[:r] ** 2 / (sig[:r] ** 2 + lam)
+        np.testing.assert_allclose(w_dec, vr[w:, :] * shrink[None, :], rtol=1e-9, atol=1e-11)
+
+
+def test_fit_exact_rank_pair_translates_new_samples():
+    # Producer and consumer rows driven by one rank-r latent (plus offsets): the fitted
+    # translator maps fresh producer rows of the same form onto the consumer's exactly
+    # (up to the tiny ridge term).
+    rng = np.random.default_rng(44)
+    N, w, r = 300, 8, 3
+    qa = rng.standard_normal((r, w))
+    qb = rng.standard_normal((r, w))
+    ma, mb = rng.standard_normal(w), rng.standard_normal(w)
+    C = rng.standard_normal((N, r))
+    A, B = C @ qa + ma, C @ qb + mb
+    w_enc, w_dec, mu_a, mu_b = O.fit_reuse(A, B, None, 1, w, 1e4, w, False, r, 1e-9)
+    np.testing.assert_allclose(mu_a, ma + C.mean(0) @ qa, rtol=1e-12, atol=1e-12)
+    C2 = rng.standard_normal((50, r))
+    A2, B2 = C2 @ qa + ma, C2 @ qb + mb
+    z = O.encode_v(A2, w_enc, mu_a)
+    np.testing.assert_allclose(O.decode_v(z, w_dec, mu_b, w), B2, rtol=1e-6, atol=1e-6)
+
+
+def test_fit_self_pair_full_rank_is_identity():
+    rng = np.random.default_rng(45)
+    N, w = 80, 6
+    A = rng.standard_normal((N, w)) @ rng.standard_normal((w, w)) + 2.0
+    w_enc, w_dec, mu_a, mu_b = O.fit_reuse(A, A, None, 1, w, 1e4, w, False, w, 0.0)
+    np.testing.assert_allclose(w_dec @ w_enc, np.eye(w), rtol=1e-9, atol=1e-9)
+    np.testing.assert_allclose(mu_a, mu_b, rtol=0, atol=0)
+
+
+def test_fit_centering_is_translation_invariant():
+    rng = np.random.default_rng(46)
+    N, w, r, lam = 70, 6, 4, 0.5
+    A = rng.standard_normal((N, w)) * np.arange(1, w + 1)
+    B = A @ rng.standard_normal((w, w)) + 0.2 * rng.standard_normal((N, w))
+    ca, cb = 5.0 * rng.standard_normal(w), -3.0 * rng.standard_normal(w)
+    e0, d0, ma0, mb0 = O.fit_reuse(A, B, None, 1, w, 1e4, w, False, r, lam)
+    e1, d1, ma1, mb1 = O.fit_reuse(A + ca, B + cb, None, 1, w, 1e4, w, False, r, lam)
+    np.testing.assert_allclose(e1, e0, rtol=1e-8, atol=1e-9)
+    np.testing.assert_allclose(d1, d0, rtol=1e-8, atol=1e-9)
+    np.testing.assert_allclose(ma1, ma0 + ca, rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(mb1, mb0 + cb, rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(ma0, A.mean(0), rtol=1e-12, atol=1e-12)
+
+
+def test_fit_keys_are_fitted_in_content_space():
+    # Keys are fitted after deRoPE: rotating the content by each token's position (complex
+    # multiplication, test side) and fitting with deRoPE gives the content's own fit.
+    rng = np.random.default_rng(47)
+    T, H, dh, th, r = 50, 2, 8, 500.0, 4
+    w = dh
+    ca = rng.standard_normal((T, H * dh))
+    cb = ca @ np.kron(np.eye(H), rng.standard_normal((dh, dh))) + 0.1 * rng.standard_normal((T, H * dh))
+    pos = np.arange(T) * 3 + 1
+    ka = rope_complex(ca, pos, H, dh, th)
+    kb = rope_complex(cb, pos, H, dh, th)
+    fk = O.fit_reuse(ka, kb, pos, H, dh, th, w, True, r, 0.1)
+    fc = O.fit_reuse(ca, cb, None, H, dh, th, w, False, r, 0.1)
+    for got, want in zip(fk, fc):
+        np.testing.assert_allclose(got, want, rtol=1e-8, atol=1e-9)
+
+
+def test_fit_sign_convention():
+    # At lambda = 0 the decoder is the consumer half of V_r, whose full columns have their
+    # largest-magnitude entry positive (LAPACK gesvd and a test-side sign rule).
+    rng = np.random.default_rng(48)
+    N, w, r = 50, 5, 3
+    A = rng.standard_normal((N, w))
+    B = 3.0 * rng.standard_normal((N, w))
+    _, w_dec, _, _ = O.fit_reuse(A, B, None, 1, w, 1e4, w, False, r, 0.0, center=False)
+    X = np.concatenate([A, B], axis=1)
+    _, _, vt = scipy.linalg.svd(X, full_matrices=False, lapack_driver="gesvd")
+    np.testing.assert_allclose(w_dec, _sign_fix_test(vt[:r].T)[w:], rtol=1e-9, atol=1e-11)
