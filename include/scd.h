@@ -218,6 +218,49 @@ scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch
                                        void* const* k_cache, void* const* v_cache,
                                        hipStream_t copy_stream, hipStream_t stream);
 
+/* ---- Offline Reuse fit (Section 4.3.1 "Joint Subspace Learning"; Appendix F.1) ---------------
+ * Fits one branch's Reuse translators for every Reuse layer from paired calibration caches: the
+ * producer's a_in[l] and the consumer's b_in[l], both [T, H, d_h] over the same packed batch of
+ * prefixes (positions as everywhere else).  With rows A, B [N, w] (N = T*g; keys de-rotated first)
+ * and X = [A B]:
+ *   centring (optional):  mu_enc = mean of A's rows, mu_dec = mean of B's rows; A, B lose them;
+ *   truncated SVD:        V_r = the top-r right singular vectors of X (r = rank_k or rank_v of
+ *                         the layer), each with its largest-magnitude entry positive; Z = X V_r;
+ *   ridge encoder:        E = argmin ||A E - Z||^2 + lambda ||E||^2   -> w_enc [r, w] = E^T;
+ *   ridge decoder:        F = argmin ||Z F - B||^2 + lambda ||F||^2   -> w_dec [w, r] = F^T.
+ * The outputs are exactly the w_enc / mu_enc the encoder takes and the w_dec / mu_dec the Reuse
+ * decoder takes (the paper leaves the latent scale, the decoder's fit and the centring open: Z
+ * carries the singular values, the decoder is a ridge fit with the same lambda, and centring is a
+ * flag).
+ *
+ * The fit runs in two calls, stream-ordered:
+ *  - scd_fit_gram accumulates, per Reuse layer, gram[l] = X^T X (fp32 [2w, 2w], symmetric) and
+ *    colsum[l] = 1^T X (fp32 [2w]) on the matrix cores (bf16: keys de-rotated and rounded to bf16
+ *    once, fp32 accumulation; fp32: fp32 products).  Rows are split into slices whose partial sums
+ *    go to `workspace` and are added in a fixed order, so the result is deterministic.  branch 0 =
+ *    keys (de-rotated; rope_table required), 1 = values.  Needs basis_width % 64 == 0 and at least
+ *    one token.
+ *  - scd_fit_solve takes those sums for N = n_rows rows (n_tokens * g) and solves the fit in fp64,
+ *    one workgroup per layer (cyclic Jacobi eigendecomposition of the centred Gram, Cholesky ridge
+ *    solves), writing w_enc, w_dec and, when center = 1, mu_enc and mu_dec in the model's dtype
+ *    (rounded once).  Needs basis_width <= 256 and 16 <= rank <= basis_width, rank % 16 == 0,
+ *    lambda >= 0.  lambda = 0 with a singular A^T A (fewer independent rows than w) leaves NaN in
+ *    the layer's outputs.
+ * `workspace` (device, 16-byte aligned, caller-owned, contents undefined on entry and exit) must
+ * hold scd_fit_workspace_bytes(model, n_tokens) bytes; one buffer serves both calls.  Layers run
+ * 64 per launch; the calls never synchronise.  Patch layers are not touched. */
+size_t scd_fit_workspace_bytes(const scd_model_t* model, int64_t n_tokens);
+scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
+                          const void* rope_table, int64_t max_position, int32_t branch,
+                          const void* const* a_in, const void* const* b_in,
+                          float* const* gram, float* const* colsum, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                           double ridge_lambda, int32_t center, const float* const* gram,
+                           const float* const* colsum, void* const* w_enc, void* const* w_dec,
+                           void* const* mu_enc, void* const* mu_dec, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
 /* ---- diagnostics ---------------------------------------------------------------------------- */
 const char* scd_status_string(scd_status_t status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */

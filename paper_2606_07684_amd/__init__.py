@@ -112,6 +112,13 @@ _SIGS = {
                                                  ctypes.POINTER(_CBatch), _VP, ctypes.c_int64,
                                                  _VP, _VP, ctypes.c_int32] + [_PP] * 6
                                   + [_VP, _VP]),
+    "scd_fit_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(_CModel), ctypes.c_int64]),
+    "scd_fit_gram": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.POINTER(_CBatch), _VP,
+                                    ctypes.c_int64, ctypes.c_int32] + [_PP] * 4
+                     + [_VP, ctypes.c_size_t, _VP]),
+    "scd_fit_solve": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32, ctypes.c_int64,
+                                     ctypes.c_double, ctypes.c_int32] + [_PP] * 6
+                      + [_VP, ctypes.c_size_t, _VP]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -518,3 +525,103 @@ def scd_reuse_decode_streamed(model: Model, batch: Batch, rope: Optional[RopeTab
     prepare_reuse_decode_streamed(model, batch, rope, payload_src, payload_dst,
                                   layers_per_group, w_dec_k, w_dec_v, mu_k, mu_v, k_cache,
                                   v_cache)(copy_stream, stream)
+
+
+# ------------------------------------------------------------------------------------------------
+# Offline Reuse fit
+# ------------------------------------------------------------------------------------------------
+FIT_KEYS, FIT_VALUES = 0, 1
+
+
+def scd_fit_workspace_bytes(model: Model, n_tokens: int) -> int:
+    return int(load_library().scd_fit_workspace_bytes(ctypes.byref(model._c), int(n_tokens)))
+
+
+def _workspace_arg(workspace: torch.Tensor):
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda:
+        raise ValueError("workspace must be a CUDA tensor")
+    if not workspace.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def prepare_fit_gram(model: Model, batch: Batch, rope: Optional[RopeTable], branch: int, a_in,
+                     b_in, gram, colsum, workspace: torch.Tensor) -> Prepared:
+    lib = load_library()
+    L, T, D, w = model.n_layers, batch.n_tokens, model.kv_width, model.basis_width
+    dt = model.torch_dtype
+    R = [l for l in range(L) if not model.is_patch[l]]
+    args = [
+        _ptr_array(a_in, L, "a_in", {l: (T, D) for l in R}, dt),
+        _ptr_array(b_in, L, "b_in", {l: (T, D) for l in R}, dt),
+        _ptr_array(gram, L, "gram", {l: (2 * w, 2 * w) for l in R}, torch.float32),
+        _ptr_array(colsum, L, "colsum", {l: (2 * w,) for l in R}, torch.float32),
+    ]
+    ws, nbytes = _workspace_arg(workspace)
+    tab, maxp = _rope_args(rope)
+    return Prepared(lib.scd_fit_gram, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
+                                       int(branch), *[_as_pp(a) for a in args], ws, nbytes),
+                    (model, batch, rope, args, workspace))
+
+
+def scd_fit_gram(model: Model, batch: Batch, rope: Optional[RopeTable], branch: int, a_in, b_in,
+                 gram, colsum, workspace: torch.Tensor, stream=None) -> None:
+    prepare_fit_gram(model, batch, rope, branch, a_in, b_in, gram, colsum, workspace)(stream)
+
+
+def prepare_fit_solve(model: Model, branch: int, n_rows: int, ridge_lambda: float, center: bool,
+                      gram, colsum, w_enc, w_dec, mu_enc, mu_dec,
+                      workspace: torch.Tensor) -> Prepared:
+    lib = load_library()
+    L, w = model.n_layers, model.basis_width
+    dt = model.torch_dtype
+    R = [l for l in range(L) if not model.is_patch[l]]
+    ranks = model.rank_k if branch == FIT_KEYS else model.rank_v
+    args = [
+        _ptr_array(gram, L, "gram", {l: (2 * w, 2 * w) for l in R}, torch.float32),
+        _ptr_array(colsum, L, "colsum", {l: (2 * w,) for l in R}, torch.float32),
+        _ptr_array(w_enc, L, "w_enc", {l: (ranks[l], w) for l in R}, dt),
+        _ptr_array(w_dec, L, "w_dec", {l: (w, ranks[l]) for l in R}, dt),
+        _ptr_array(mu_enc, L, "mu_enc", {l: (w,) for l in R}, dt),
+        _ptr_array(mu_dec, L, "mu_dec", {l: (w,) for l in R}, dt),
+    ]
+    ws, nbytes = _workspace_arg(workspace)
+    return Prepared(lib.scd_fit_solve, (ctypes.byref(model._c), int(branch), int(n_rows),
+                                        float(ridge_lambda), 1 if center else 0,
+                                        *[_as_pp(a) for a in args], ws, nbytes),
+                    (model, args, workspace))
+
+
+def scd_fit_solve(model: Model, branch: int, n_rows: int, ridge_lambda: float, center: bool,
+                  gram, colsum, w_enc, w_dec, mu_enc, mu_dec, workspace: torch.Tensor,
+                  stream=None) -> None:
+    prepare_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc, w_dec,
+                      mu_enc, mu_dec, workspace)(stream)
+
+
+def fit_reuse(model: Model, batch: Batch, rope: Optional[RopeTable], branch: int, a_in, b_in,
+              ridge_lambda: float, center: bool = True, stream=None):
+    """Both fit calls with freshly allocated outputs: returns per-layer lists
+    ``(w_enc, w_dec, mu_enc, mu_dec, gram, colsum)`` (None for Patch layers; the offsets are None
+    without centring)."""
+    L, w = model.n_layers, model.basis_width
+    R = [l for l in range(L) if not model.is_patch[l]]
+    dev = next(t.device for t in a_in if t is not None)
+    dt = model.torch_dtype
+    ranks = model.rank_k if branch == FIT_KEYS else model.rank_v
+    ws = torch.empty(max(scd_fit_workspace_bytes(model, batch.n_tokens), 16), dtype=torch.uint8,
+                     device=dev)
+    gram, colsum, w_enc, w_dec, mu_enc, mu_dec = ([None] * L for _ in range(6))
+    for l in R:
+        gram[l] = torch.empty((2 * w, 2 * w), dtype=torch.float32, device=dev)
+        colsum[l] = torch.empty((2 * w,), dtype=torch.float32, device=dev)
+        w_enc[l] = torch.empty((ranks[l], w), dtype=dt, device=dev)
+        w_dec[l] = torch.empty((w, ranks[l]), dtype=dt, device=dev)
+        if center:
+            mu_enc[l] = torch.empty((w,), dtype=dt, device=dev)
+            mu_dec[l] = torch.empty((w,), dtype=dt, device=dev)
+    scd_fit_gram(model, batch, rope, branch, a_in, b_in, gram, colsum, ws, stream)
+    scd_fit_solve(model, branch, batch.n_tokens * model.g, ridge_lambda, center, gram, colsum,
+                  w_enc, w_dec, mu_enc if center else None, mu_dec if center else None, ws, stream)
+    return w_enc, w_dec, mu_enc, mu_dec, gram, colsum
+

@@ -209,7 +209,7 @@ int64_t kv_width(const scd_model_t* m) {
 
 extern "C" {
 
-int32_t scd_abi_version(void) { return 3; }
+int32_t scd_abi_version(void) { return 4; }
 
 const char* scd_status_string(scd_status_t s) {
   switch (s) {
@@ -732,6 +732,187 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
       if (e != hipSuccess)
         return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
     }
+  }
+  return ok();
+}
+
+}  // extern "C"
+
+// ---- Offline Reuse fit ------------------------------------------------------------------------
+namespace {
+
+constexpr int kFitMaxSweeps = 40;
+
+// Slices of the row axis for a Gram launch of n_jobs jobs: about four workgroups per CU over the
+// whole launch, at least 512 rows per slice, slice lengths a multiple of the kernels' k-step.
+int64_t fit_slices(int n_jobs, int w, int64_t n_rows, int64_t* slice_rows) {
+  const int64_t units = static_cast<int64_t>(n_jobs) * scd::fit_upper_tiles(w);
+  int64_t ns = (1024 + units - 1) / units;
+  const int64_t max_ns = (n_rows + 511) / 512;
+  if (ns > max_ns) ns = max_ns;
+  if (ns < 1) ns = 1;
+  int64_t sr = (n_rows + ns - 1) / ns;
+  sr = (sr + scd::kFitRowStep - 1) / scd::kFitRowStep * scd::kFitRowStep;
+  ns = (n_rows + sr - 1) / sr;
+  if (ns < 1) ns = 1;
+  *slice_rows = sr;
+  return ns;
+}
+
+int count_reuse(const scd_model_t* m) {
+  int n = 0;
+  for (int l = 0; l < m->n_layers; ++l) n += m->is_patch[l] ? 0 : 1;
+  return n;
+}
+
+size_t fit_gram_ws(const scd_model_t* m, int64_t n_rows) {
+  const int R = count_reuse(m);
+  size_t best = 0;
+  for (int done = 0; done < R; done += scd::kMaxJobs) {
+    const int jobs = R - done < scd::kMaxJobs ? R - done : scd::kMaxJobs;
+    int64_t sr;
+    const int64_t ns = fit_slices(jobs, m->basis_width, n_rows, &sr);
+    const size_t b = static_cast<size_t>(jobs) * ns * scd::fit_upper_tiles(m->basis_width) *
+                     (scd::kFitTile * scd::kFitTile + scd::kFitTile) * sizeof(float);
+    if (b > best) best = b;
+  }
+  return best;
+}
+
+size_t fit_solve_ws(const scd_model_t* m) {
+  const int R = count_reuse(m);
+  const size_t jobs = R < scd::kMaxJobs ? R : scd::kMaxJobs;
+  const size_t n = 2 * static_cast<size_t>(m->basis_width);
+  return jobs * 3 * n * n * sizeof(double);
+}
+
+scd_status_t check_fit_model(const scd_model_t* model, int32_t branch) {
+  SCD_TRY(check_model(model));
+  if (branch != 0 && branch != 1)
+    return fail(SCD_ERR_SHAPE, "branch must be 0 (keys) or 1 (values), got %d", branch);
+  if (model->basis_width % 64 != 0)
+    return fail(SCD_ERR_UNSUPPORTED, "the fit needs basis_width %% 64 == 0 (got %d)",
+                model->basis_width);
+  return SCD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t scd_fit_workspace_bytes(const scd_model_t* model, int64_t n_tokens) {
+  if (check_model(model) != SCD_OK || n_tokens < 1) return 0;
+  const int64_t g = kv_width(model) / model->basis_width;
+  const size_t a = fit_gram_ws(model, n_tokens * g), b = fit_solve_ws(model);
+  return a > b ? a : b;
+}
+
+scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
+                          const void* rope_table, int64_t max_position, int32_t branch,
+                          const void* const* a_in, const void* const* b_in,
+                          float* const* gram, float* const* colsum, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  SCD_TRY(check_fit_model(model, branch));
+  SCD_TRY(check_batch(batch));
+  if (batch->n_tokens < 1) return fail(SCD_ERR_SHAPE, "the fit needs at least one token");
+  const int w = model->basis_width;
+  const int g = static_cast<int>(kv_width(model) / w);
+  const int64_t n_rows = batch->n_tokens * g;
+  std::vector<int> layers;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) continue;
+    layers.push_back(l);
+    SCD_TRY(need_ptr(a_in, l, "a_in"));
+    SCD_TRY(need_ptr(b_in, l, "b_in"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(gram), l, "gram"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(colsum), l, "colsum"));
+  }
+  if (layers.empty()) return ok();
+  if (branch == 0) SCD_TRY(check_rope(rope_table, max_position));
+  if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
+  const size_t need = fit_gram_ws(model, n_rows);
+  if (workspace_bytes < need)
+    return fail(SCD_ERR_SHAPE, "workspace_bytes %zu < %zu needed", workspace_bytes, need);
+
+  for (size_t done = 0; done < layers.size(); done += scd::kMaxJobs) {
+    scd::FitGramParams p{};
+    p.n_jobs = 0;
+    for (size_t i = done; i < layers.size() && i < done + scd::kMaxJobs; ++i) {
+      const int l = layers[i];
+      p.jobs[p.n_jobs++] = {a_in[l], b_in[l], gram[l], colsum[l]};
+    }
+    p.w = w;
+    p.n_rows = n_rows;
+    p.g = g;
+    p.head_dim = model->head_dim;
+    p.derope = branch == 0 ? 1 : 0;
+    p.n_slices = static_cast<int32_t>(fit_slices(p.n_jobs, w, n_rows, &p.slice_rows));
+    p.n_seqs = batch->n_seqs;
+    p.cu_seqlens = batch->cu_seqlens;
+    p.pos0 = batch->pos0;
+    p.rope = static_cast<const float2*>(rope_table);
+    p.max_pos = max_position;
+    p.partial = static_cast<float*>(workspace);
+    const hipError_t e = scd::launch_fit_gram(model->dtype == SCD_BF16, p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "fit Gram launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                           double ridge_lambda, int32_t center, const float* const* gram,
+                           const float* const* colsum, void* const* w_enc, void* const* w_dec,
+                           void* const* mu_enc, void* const* mu_dec, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  SCD_TRY(check_fit_model(model, branch));
+  const int w = model->basis_width;
+  if (w > scd::kFitMaxSolveWidth)
+    return fail(SCD_ERR_UNSUPPORTED, "the fit's solve takes basis_width <= %d (got %d)",
+                scd::kFitMaxSolveWidth, w);
+  if (n_rows < 1) return fail(SCD_ERR_SHAPE, "n_rows must be >= 1");
+  if (!(ridge_lambda >= 0.0) || ridge_lambda > 1e300)
+    return fail(SCD_ERR_SHAPE, "ridge_lambda must be finite and >= 0");
+  if (center != 0 && center != 1) return fail(SCD_ERR_SHAPE, "center must be 0 or 1");
+  const int32_t* ranks = branch == 0 ? model->rank_k : model->rank_v;
+  std::vector<int> layers;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (model->is_patch[l]) continue;
+    layers.push_back(l);
+    SCD_TRY(check_rank(branch == 0 ? "rank_k" : "rank_v", l, ranks[l], w));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(gram), l, "gram"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(colsum), l, "colsum"));
+    SCD_TRY(need_ptr(w_enc, l, "w_enc"));
+    SCD_TRY(need_ptr(w_dec, l, "w_dec"));
+    if (center) {
+      SCD_TRY(need_ptr(mu_enc, l, "mu_enc"));
+      SCD_TRY(need_ptr(mu_dec, l, "mu_dec"));
+    }
+  }
+  if (layers.empty()) return ok();
+  if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
+  const size_t need = fit_solve_ws(model);
+  if (workspace_bytes < need)
+    return fail(SCD_ERR_SHAPE, "workspace_bytes %zu < %zu needed", workspace_bytes, need);
+
+  for (size_t done = 0; done < layers.size(); done += scd::kMaxJobs) {
+    scd::FitSolveParams p{};
+    p.n_jobs = 0;
+    for (size_t i = done; i < layers.size() && i < done + scd::kMaxJobs; ++i) {
+      const int l = layers[i];
+      p.jobs[p.n_jobs++] = {gram[l], colsum[l], w_enc[l], w_dec[l],
+                            center ? mu_enc[l] : nullptr, center ? mu_dec[l] : nullptr, ranks[l], 0};
+    }
+    p.w = w;
+    p.n_rows = n_rows;
+    p.lambda = ridge_lambda;
+    p.center = center;
+    p.bf16 = model->dtype == SCD_BF16 ? 1 : 0;
+    p.max_sweeps = kFitMaxSweeps;
+    p.work = static_cast<double*>(workspace);
+    const hipError_t e = scd::launch_fit_solve(p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "fit solve launch failed: %s", hipGetErrorString(e));
   }
   return ok();
 }

@@ -1,0 +1,672 @@
+// Offline Reuse fit of the SCD codec (Section 4.3.1 "Joint Subspace Learning"; Appendix F.1
+// "Reuse: Layer-wise Stack-SVD with Ridge Regression").
+//
+// For one branch (keys or values) of every Reuse layer, the producer's and the consumer's caches of
+// the same calibration prefixes give rows A, B [N, w] (keys de-rotated first).  The fit needs only
+// the joint Gram G = X^T X of X = [A B] (2w x 2w) and the column sums 1^T X:
+//   * the truncated SVD of the (centred) X is the eigendecomposition of the (centred) G, whose top-r
+//     eigenvectors V_r give the latents Z = X V_r;
+//   * the ridge encoder E = (A^T A + lam I)^-1 A^T Z needs A^T A and A^T Z = G[0:w, :] V_r;
+//   * the ridge decoder F = (Z^T Z + lam I)^-1 Z^T B needs Z^T Z = V_r^T G V_r and
+//     Z^T B = (G[w:2w, :] V_r)^T.
+// The O(N w^2) part (the Gram) streams the caches once on the matrix cores; the O(w^3) part runs in
+// fp64 in one workgroup per layer (parallel cyclic Jacobi, then Cholesky solves).
+#include "scd_device.h"
+
+namespace scd {
+
+using namespace dev;
+
+namespace {
+
+constexpr int kTB = kFitTile;
+constexpr int kTileFloats = kTB * kTB + kTB;  // one partial tile: Gram block + column sums
+
+__device__ inline int fit_position(const FitGramParams& p, int64_t row) {
+  const int64_t t = row / p.g;
+  int b = 0;
+  int64_t local = t;
+  if (p.cu_seqlens != nullptr) {
+    int lo = 0, hi = p.n_seqs - 1;  // largest b with cu[b] <= t
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (p.cu_seqlens[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+    local = t - p.cu_seqlens[b];
+  }
+  int64_t pos = local + (p.pos0 != nullptr ? p.pos0[b] : 0);
+  pos = pos < 0 ? 0 : (pos >= p.max_pos ? p.max_pos - 1 : pos);
+  return static_cast<int>(pos);
+}
+
+// Upper tiles (ti <= tj) of the nt x nt tile grid, numbered row by row.
+__device__ inline void tile_of(int tile, int nt, int& ti, int& tj) {
+  int rem = tile;
+  ti = 0;
+  while (rem >= nt - ti) {
+    rem -= nt - ti;
+    ++ti;
+  }
+  tj = ti + rem;
+}
+__device__ inline int upper_index(int ti, int tj, int nt) {
+  return ti * nt - ti * (ti - 1) / 2 + (tj - ti);
+}
+
+// First column (inside a 128-column block) of chunk pair cp: VEC columns of one head's first half;
+// their RoPE partners sit d_h/2 further on.  A block holds 128 / d_h heads of d_h / (2 VEC) pairs.
+template <int DH, int VEC>
+__device__ inline int pair_col(int cp) {
+  constexpr int PER_HEAD = DH / 2 / VEC;
+  return (cp / PER_HEAD) * DH + (cp % PER_HEAD) * VEC;
+}
+
+struct BlockSrc {
+  const char* base;  // producer or consumer cache
+  int col;           // column inside the w-wide row
+};
+
+// Source of the chunk pair starting at joint column jc (< 2w): columns [0, w) are the producer's,
+// [w, 2w) the consumer's.  A head never straddles the two (w is a multiple of d_h).
+__device__ inline BlockSrc block_src(const FitGramJob& j, int w, int jc, int eb) {
+  BlockSrc s;
+  s.base = static_cast<const char*>(jc < w ? j.a : j.b);
+  s.col = (jc < w ? jc : jc - w) * eb;
+  return s;
+}
+
+// ---------------------------------------------------------------------------------------------
+// bf16 Gram: one workgroup of 4 waves per (job, upper 128 x 128 tile, row slice).  Each k-step
+// stages 64 rows of the tile's two column blocks transposed in LDS ([column][row], so an MFMA
+// operand fragment is 8 consecutive rows of one column) and runs v_mfma_f32_32x32x16_bf16 with the
+// I block as A and the J block as B: C[m][n] = sum_rows X[row][I0+m] X[row][J0+n].  Keys are
+// de-rotated in registers and rounded to bf16 once before the product (as the encoder does).
+// Thread t stages row pair t % 32 and chunk pair t / 32 (8 columns + their RoPE partners); the
+// next k-step's rows are loaded while the current one's MFMAs run.
+// ---------------------------------------------------------------------------------------------
+template <int DH, bool DEROPE>
+__global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams p) {
+  constexpr int BK = kFitRowStep, S = BK + 8, HALF = DH / 2;
+  __shared__ __attribute__((aligned(16))) uint16_t xt[2][kTB * S];
+
+  const int nt = 2 * p.w / kTB, n_upper = nt * (nt + 1) / 2;
+  int unit = blockIdx.x;
+  const int slice = unit % p.n_slices;
+  unit /= p.n_slices;
+  const int tile = unit % n_upper;
+  const int job = unit / n_upper;
+  int ti, tj;
+  tile_of(tile, nt, ti, tj);
+  const bool diag = ti == tj;
+  const int nblk = diag ? 1 : 2;
+  const FitGramJob& jb = p.jobs[job];
+  const int64_t r0 = static_cast<int64_t>(slice) * p.slice_rows;
+  const int64_t r1 = r0 + p.slice_rows < p.n_rows ? r0 + p.slice_rows : p.n_rows;
+  const int64_t row_bytes = static_cast<int64_t>(p.w) * 2;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rp = tid & 31, cp = tid >> 5;
+  const int c = pair_col<DH, 8>(cp);
+  const int ri = c % DH;  // RoPE pair index of the first column (< d_h / 2)
+  BlockSrc src[2];
+  src[0] = block_src(jb, p.w, ti * kTB + c, 2);
+  src[1] = block_src(jb, p.w, tj * kTB + c, 2);
+
+  uint4 ld[2][2][2];  // [block][row of the pair][first half / partner]
+  float csum[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) csum[i] = 0.f;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  auto issue_loads = [&](int64_t k0) {
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+      const int64_t n = k0 + 2 * rp + rr;
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        if (b < nblk && n < r1) {
+          const char* rowp = src[b].base + n * row_bytes + src[b].col;
+          ld[b][rr][0] = *reinterpret_cast<const uint4*>(rowp);
+          ld[b][rr][1] = *reinterpret_cast<const uint4*>(rowp + HALF * 2);
+        } else {
+          ld[b][rr][0] = zero4;
+          ld[b][rr][1] = zero4;
+        }
+      }
+    }
+  };
+
+  const int wy = wave >> 1, wx = wave & 1;
+  const int h = lane >> 5;
+  const uint16_t* xa = xt[0] + (wy * 64 + (lane & 31)) * S + 8 * h;
+  const uint16_t* xb = xt[diag ? 0 : 1] + (wx * 64 + (lane & 31)) * S + 8 * h;
+
+  if (r0 < r1) issue_loads(r0);
+  for (int64_t k0 = r0; k0 < r1; k0 += BK) {
+    // de-rotate (keys) and round the staged rows; accumulate the diagonal tile's column sums
+    uint32_t pk[2][2][8];  // [block][first half / partner][column]: rows 2rp (low), 2rp+1 (high)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b >= nblk) break;
+      float f[2][2][8];
+#pragma unroll
+      for (int rr = 0; rr < 2; ++rr) {
+        unpack8(ld[b][rr][0], f[rr][0]);
+        unpack8(ld[b][rr][1], f[rr][1]);
+        if constexpr (DEROPE) {
+          const int64_t n = k0 + 2 * rp + rr;
+          if (n < r1) {
+            const float2* tab = p.rope + static_cast<int64_t>(fit_position(p, n)) * HALF + ri;
+#pragma unroll
+            for (int j = 0; j < 8; j += 2) {
+              const float4 cs = *reinterpret_cast<const float4*>(tab + j);
+              const float u0 = f[rr][0][j], v0 = f[rr][1][j];
+              const float u1 = f[rr][0][j + 1], v1 = f[rr][1][j + 1];
+              // inverse rotation by the position's angle
+              f[rr][0][j] = u0 * cs.x + v0 * cs.y;
+              f[rr][1][j] = v0 * cs.x - u0 * cs.y;
+              f[rr][0][j + 1] = u1 * cs.z + v1 * cs.w;
+              f[rr][1][j + 1] = v1 * cs.z - u1 * cs.w;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          pk[b][q][j] = pack_bf16x2(f[0][q][j], f[1][q][j]);
+          if (b == 0 && diag) csum[8 * q + j] += bf16_lo(pk[b][q][j]) + bf16_hi(pk[b][q][j]);
+        }
+    }
+    __syncthreads();  // every wave has finished reading the previous k-step's tiles
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b >= nblk) break;
+      uint32_t* dst = reinterpret_cast<uint32_t*>(xt[b]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        dst[((c + j) * S) / 2 + rp] = pk[b][0][j];
+        dst[((c + HALF + j) * S) / 2 + rp] = pk[b][1][j];
+      }
+    }
+    __syncthreads();
+    if (k0 + BK < r1) issue_loads(k0 + BK);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = *reinterpret_cast<const bf16x8*>(xa + i * 32 * S + ks * 16);
+        fb[i] = *reinterpret_cast<const bf16x8*>(xb + i * 32 * S + ks * 16);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  float* out = p.partial + ((static_cast<int64_t>(job) * p.n_slices + slice) * n_upper + tile) *
+                               static_cast<int64_t>(kTileFloats);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = wy * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const int n = wx * 64 + j * 32 + (lane & 31);
+        out[m * kTB + n] = acc[i][j][r];
+      }
+  if (diag) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) csum[i] += __shfl_xor(csum[i], o, 64);
+    if (rp == 0) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        out[kTB * kTB + c + j] = csum[j];
+        out[kTB * kTB + c + HALF + j] = csum[8 + j];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// fp32 Gram on the vector units (the fp32 path takes no reduced-precision products): 16-row
+// k-steps staged row-major in LDS, each thread accumulates an 8 x 8 block of the tile.  Thread t
+// stages row t % 16 and chunk pair t / 16 (4 columns + their RoPE partners).
+// ---------------------------------------------------------------------------------------------
+template <int DH, bool DEROPE>
+__global__ __launch_bounds__(256) void fit_gram_f32_kernel(const FitGramParams p) {
+  constexpr int BK = 16, LD = kTB + 4, HALF = DH / 2;
+  __shared__ __attribute__((aligned(16))) float xs[2][BK * LD];
+
+  const int nt = 2 * p.w / kTB, n_upper = nt * (nt + 1) / 2;
+  int unit = blockIdx.x;
+  const int slice = unit % p.n_slices;
+  unit /= p.n_slices;
+  const int tile = unit % n_upper;
+  const int job = unit / n_upper;
+  int ti, tj;
+  tile_of(tile, nt, ti, tj);
+  const bool diag = ti == tj;
+  const int nblk = diag ? 1 : 2;
+  const FitGramJob& jb = p.jobs[job];
+  const int64_t r0 = static_cast<int64_t>(slice) * p.slice_rows;
+  const int64_t r1 = r0 + p.slice_rows < p.n_rows ? r0 + p.slice_rows : p.n_rows;
+  const int64_t row_bytes = static_cast<int64_t>(p.w) * 4;
+
+  const int tid = threadIdx.x;
+  const int lr = tid & 15, cp = tid >> 4;
+  const int c = pair_col<DH, 4>(cp);
+  const int ri = c % DH;
+  BlockSrc src[2];
+  src[0] = block_src(jb, p.w, ti * kTB + c, 4);
+  src[1] = block_src(jb, p.w, tj * kTB + c, 4);
+  const int ty = tid >> 4, tx = tid & 15;
+
+  float acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+  float csum[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) csum[i] = 0.f;
+
+  for (int64_t k0 = r0; k0 < r1; k0 += BK) {
+    const int64_t n = k0 + lr;
+    float f[2][2][4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b >= nblk) break;
+      float4 u = make_float4(0.f, 0.f, 0.f, 0.f), v = u;
+      if (n < r1) {
+        const char* rowp = src[b].base + n * row_bytes + src[b].col;
+        u = *reinterpret_cast<const float4*>(rowp);
+        v = *reinterpret_cast<const float4*>(rowp + HALF * 4);
+      }
+      f[b][0][0] = u.x; f[b][0][1] = u.y; f[b][0][2] = u.z; f[b][0][3] = u.w;
+      f[b][1][0] = v.x; f[b][1][1] = v.y; f[b][1][2] = v.z; f[b][1][3] = v.w;
+      if constexpr (DEROPE) {
+        if (n < r1) {
+          const float2* tab = p.rope + static_cast<int64_t>(fit_position(p, n)) * HALF + ri;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float2 cs = tab[j];
+            const float a0 = f[b][0][j], b0 = f[b][1][j];
+            f[b][0][j] = a0 * cs.x + b0 * cs.y;
+            f[b][1][j] = b0 * cs.x - a0 * cs.y;
+          }
+        }
+      }
+      if (b == 0 && diag) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          csum[j] += f[0][0][j];
+          csum[4 + j] += f[0][1][j];
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b >= nblk) break;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xs[b][lr * LD + c + j] = f[b][0][j];
+        xs[b][lr * LD + c + HALF + j] = f[b][1][j];
+      }
+    }
+    __syncthreads();
+    const float* xi = xs[0];
+    const float* xj = xs[diag ? 0 : 1];
+#pragma unroll 4
+    for (int k = 0; k < BK; ++k) {
+      float av[8], bv[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        av[i] = xi[k * LD + ty + 16 * i];
+        bv[i] = xj[k * LD + tx + 16 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+  }
+
+  float* out = p.partial + ((static_cast<int64_t>(job) * p.n_slices + slice) * n_upper + tile) *
+                               static_cast<int64_t>(kTileFloats);
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[(ty + 16 * i) * kTB + tx + 16 * j] = acc[i][j];
+  if (diag) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) csum[i] += __shfl_xor(csum[i], o, 64);
+    if (lr == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        out[kTB * kTB + c + j] = csum[j];
+        out[kTB * kTB + c + HALF + j] = csum[4 + j];
+      }
+    }
+  }
+}
+
+// Sums each job's partial tiles over its slices in slice order (so the result does not depend on
+// scheduling) and writes the full symmetric Gram (element (i, j) and (j, i) both come from the
+// upper tile's (min, max) element) and the column sums.
+__global__ __launch_bounds__(256) void fit_gram_reduce_kernel(const FitGramParams p) {
+  const int n2 = 2 * p.w, nt = n2 / kTB, n_upper = nt * (nt + 1) / 2;
+  const int job = blockIdx.y;
+  const FitGramJob& jb = p.jobs[job];
+  const float* base = p.partial + static_cast<int64_t>(job) * p.n_slices * n_upper * kTileFloats;
+  const int64_t slice_stride = static_cast<int64_t>(n_upper) * kTileFloats;
+  const int64_t total = static_cast<int64_t>(n2) * n2 + n2;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += gridDim.x * 256) {
+    int64_t off;
+    if (e < static_cast<int64_t>(n2) * n2) {
+      int i = static_cast<int>(e / n2), j = static_cast<int>(e % n2);
+      if (i > j) {
+        const int t = i; i = j; j = t;
+      }
+      const int tile = upper_index(i / kTB, j / kTB, nt);
+      off = static_cast<int64_t>(tile) * kTileFloats + (i % kTB) * kTB + (j % kTB);
+    } else {
+      const int i = static_cast<int>(e - static_cast<int64_t>(n2) * n2);
+      const int tile = upper_index(i / kTB, i / kTB, nt);
+      off = static_cast<int64_t>(tile) * kTileFloats + kTB * kTB + (i % kTB);
+    }
+    float s = 0.f;
+    for (int sl = 0; sl < p.n_slices; ++sl) s += base[sl * slice_stride + off];
+    if (e < static_cast<int64_t>(n2) * n2) jb.gram[e] = s;
+    else jb.colsum[e - static_cast<int64_t>(n2) * n2] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// fp64 solve, one workgroup of 1024 threads per layer.
+// ---------------------------------------------------------------------------------------------
+constexpr int kSolveThreads = 1024;
+
+// Pair k of round `round` of the cyclic ("round-robin") ordering of n indices: the n/2 pairs of a
+// round are disjoint and the n - 1 rounds visit every pair once.
+__device__ inline void jacobi_pair(int round, int k, int n, int& lo, int& hi) {
+  const int m = n - 1;
+  int a, b;
+  if (k == 0) {
+    a = m;
+    b = round;
+  } else {
+    a = (round + k) % m;
+    b = (round - k + m) % m;
+  }
+  lo = a < b ? a : b;
+  hi = a < b ? b : a;
+}
+
+// In-place Cholesky factor (lower triangle) of the dim x dim matrix at a (row stride ld).  A
+// non-positive pivot leaves NaN, which then reaches every output of the solve.
+__device__ void cholesky(double* a, int dim, int ld, double* piv) {
+  const int tid = threadIdx.x;
+  for (int k = 0; k < dim; ++k) {
+    if (tid == 0) {
+      const double d = a[k * ld + k];
+      *piv = d > 0.0 ? sqrt(d) : __longlong_as_double(0x7ff8000000000000ll);
+      a[k * ld + k] = *piv;
+    }
+    __syncthreads();
+    const double pv = *piv;
+    for (int i = k + 1 + tid; i < dim; i += kSolveThreads) a[i * ld + k] /= pv;
+    __syncthreads();
+    const int rem = dim - k - 1;
+    for (int e = tid; e < rem * rem; e += kSolveThreads) {
+      const int i = k + 1 + e / rem, j = k + 1 + e % rem;
+      if (j <= i) a[i * ld + j] -= a[i * ld + k] * a[j * ld + k];
+    }
+    __syncthreads();
+  }
+}
+
+// Solves (L L^T) x = b for one right-hand side held at x[0], x[xs], ... (in place).
+__device__ void chol_solve(const double* l, int dim, int ld, double* x, int xs) {
+  for (int i = 0; i < dim; ++i) {
+    double s = x[i * xs];
+    for (int j = 0; j < i; ++j) s -= l[i * ld + j] * x[j * xs];
+    x[i * xs] = s / l[i * ld + i];
+  }
+  for (int i = dim - 1; i >= 0; --i) {
+    double s = x[i * xs];
+    for (int j = i + 1; j < dim; ++j) s -= l[j * ld + i] * x[j * xs];
+    x[i * xs] = s / l[i * ld + i];
+  }
+}
+
+__device__ inline void store_out(void* dst, int64_t i, double v, bool bf16) {
+  if (bf16) static_cast<__bf16*>(dst)[i] = static_cast<__bf16>(static_cast<float>(v));
+  else static_cast<float*>(dst)[i] = static_cast<float>(v);
+}
+
+__global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolveParams p) {
+  const int job = blockIdx.x;
+  const FitSolveJob& jb = p.jobs[job];
+  const int w = p.w, n = 2 * w, r = jb.rank, half = n / 2;
+  const int tid = threadIdx.x;
+  const bool bf16 = p.bf16 != 0;
+  double* gc = p.work + static_cast<int64_t>(job) * 3 * n * n;  // centred Gram (kept)
+  double* mj = gc + static_cast<int64_t>(n) * n;                 // Jacobi matrix, then V_r
+  double* vj = mj + static_cast<int64_t>(n) * n;                 // eigenvectors, then G V_r
+  const double rows = static_cast<double>(p.n_rows);
+
+  __shared__ double rot_c[kFitMaxSolveWidth], rot_s[kFitMaxSolveWidth];
+  __shared__ int sel[2 * kFitMaxSolveWidth];
+  __shared__ int changed;
+  __shared__ double piv, trace;
+
+  // centred Gram G - s s^T / N (the Gram of the rows minus their mean), V = I, offsets
+  for (int e = tid; e < n * n; e += kSolveThreads) {
+    const int i = e / n, j = e % n;
+    double g = jb.gram[e];
+    if (p.center) g -= static_cast<double>(jb.colsum[i]) * static_cast<double>(jb.colsum[j]) / rows;
+    gc[e] = g;
+    mj[e] = g;
+    vj[e] = i == j ? 1.0 : 0.0;
+  }
+  if (p.center) {
+    for (int i = tid; i < w; i += kSolveThreads) {
+      store_out(jb.mu_enc, i, static_cast<double>(jb.colsum[i]) / rows, bf16);
+      store_out(jb.mu_dec, i, static_cast<double>(jb.colsum[w + i]) / rows, bf16);
+    }
+  }
+  if (tid == 0) {
+    trace = 0.0;
+    changed = 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double t = 0.0;
+    for (int i = 0; i < n; ++i) t += fabs(gc[i * n + i]);
+    trace = t;
+  }
+  __syncthreads();
+  const double floor_abs = 1e-18 * trace;
+
+  // parallel cyclic Jacobi: every round applies n/2 disjoint rotations at once
+  for (int sweep = 0; sweep < p.max_sweeps; ++sweep) {
+    for (int round = 0; round < n - 1; ++round) {
+      for (int k = tid; k < half; k += kSolveThreads) {
+        int a, b;
+        jacobi_pair(round, k, n, a, b);
+        const double app = mj[a * n + a], aqq = mj[b * n + b], apq = mj[a * n + b];
+        double cr = 1.0, sr = 0.0;
+        if (fabs(apq) > floor_abs && fabs(apq) > 1e-15 * sqrt(fabs(app * aqq))) {
+          // zero the (a, b) entry of J^T M J with J = [[c, s], [-s, c]] on (a, b)
+          const double th = (aqq - app) / (2.0 * apq);
+          const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(th * th + 1.0));
+          cr = 1.0 / sqrt(t * t + 1.0);
+          sr = t * cr;
+          changed = 1;
+        }
+        rot_c[k] = cr;
+        rot_s[k] = sr;
+      }
+      __syncthreads();
+      for (int e = tid; e < half * half; e += kSolveThreads) {
+        const int P = e / half, Q = e % half;
+        int p0, q0, p1, q1;
+        jacobi_pair(round, P, n, p0, q0);
+        jacobi_pair(round, Q, n, p1, q1);
+        const double cP = rot_c[P], sP = rot_s[P], cQ = rot_c[Q], sQ = rot_s[Q];
+        const double m00 = mj[p0 * n + p1], m01 = mj[p0 * n + q1];
+        const double m10 = mj[q0 * n + p1], m11 = mj[q0 * n + q1];
+        const double r0a = cP * m00 - sP * m10, r0b = cP * m01 - sP * m11;
+        const double r1a = sP * m00 + cP * m10, r1b = sP * m01 + cP * m11;
+        mj[p0 * n + p1] = cQ * r0a - sQ * r0b;
+        mj[p0 * n + q1] = sQ * r0a + cQ * r0b;
+        mj[q0 * n + p1] = cQ * r1a - sQ * r1b;
+        mj[q0 * n + q1] = sQ * r1a + cQ * r1b;
+      }
+      for (int e = tid; e < n * half; e += kSolveThreads) {
+        const int i = e / half, Q = e % half;
+        int p1, q1;
+        jacobi_pair(round, Q, n, p1, q1);
+        const double cQ = rot_c[Q], sQ = rot_s[Q];
+        const double a = vj[i * n + p1], b = vj[i * n + q1];
+        vj[i * n + p1] = cQ * a - sQ * b;
+        vj[i * n + q1] = sQ * a + cQ * b;
+      }
+      __syncthreads();
+    }
+    const int any = changed;
+    __syncthreads();
+    if (!any) break;
+    if (tid == 0) changed = 0;
+    __syncthreads();
+  }
+
+  // the r largest eigenvalues (ties by index), in decreasing order
+  for (int i = tid; i < n; i += kSolveThreads) {
+    const double li = mj[i * n + i];
+    int cnt = 0;
+    for (int j = 0; j < n; ++j) {
+      const double lj = mj[j * n + j];
+      cnt += (lj > li || (lj == li && j < i)) ? 1 : 0;
+    }
+    if (cnt < r) sel[cnt] = i;
+  }
+  __syncthreads();
+  // V_r [n, r] (into the Jacobi matrix's storage), each column's largest-magnitude entry positive
+  double* vr = mj;
+  for (int k = tid; k < r; k += kSolveThreads) {
+    const int col = sel[k];
+    int imax = 0;
+    double best = -1.0;
+    for (int i = 0; i < n; ++i) {
+      const double a = fabs(vj[i * n + col]);
+      if (a > best) {
+        best = a;
+        imax = i;
+      }
+    }
+    const double sg = vj[imax * n + col] < 0.0 ? -1.0 : 1.0;
+    for (int i = 0; i < n; ++i) vr[i * r + k] = sg * vj[i * n + col];
+  }
+  __syncthreads();
+  // P = G_c V_r [n, r]: rows [0, w) are A^T Z, rows [w, 2w) are (Z^T B)^T
+  double* pm = vj;
+  for (int e = tid; e < n * r; e += kSolveThreads) {
+    const int i = e / r, k = e % r;
+    double s = 0.0;
+    for (int j = 0; j < n; ++j) s += gc[i * n + j] * vr[j * r + k];
+    pm[e] = s;
+  }
+  __syncthreads();
+  // Z^T Z + lam I = V_r^T P + lam I (r x r, in the centred Gram's lower-right block) and
+  // A^T A + lam I (its upper-left block)
+  double* c2 = gc + static_cast<int64_t>(w) * n + w;
+  for (int e = tid; e < r * r; e += kSolveThreads) {
+    const int k = e / r, l = e % r;
+    double s = 0.0;
+    for (int i = 0; i < n; ++i) s += vr[i * r + k] * pm[i * r + l];
+    c2[k * n + l] = s + (k == l ? p.lambda : 0.0);
+  }
+  for (int i = tid; i < w; i += kSolveThreads) gc[i * n + i] += p.lambda;
+  __syncthreads();
+  cholesky(gc, w, n, &piv);
+  cholesky(c2, r, n, &piv);
+  // encoder E = (A^T A + lam I)^-1 A^T Z: column k of P's first w rows, in place
+  for (int k = tid; k < r; k += kSolveThreads) chol_solve(gc, w, n, pm + k, r);
+  // decoder F = (Z^T Z + lam I)^-1 Z^T B: column j of F is row w + j of P, in place
+  for (int j = tid; j < w; j += kSolveThreads) chol_solve(c2, r, n, pm + static_cast<int64_t>(w + j) * r, 1);
+  __syncthreads();
+  // W_enc [r, w] = E^T and W_dec [w, r] = F^T, each rounded once
+  for (int e = tid; e < r * w; e += kSolveThreads) {
+    const int k = e / w, cc = e % w;
+    store_out(jb.w_enc, e, pm[cc * r + k], bf16);
+  }
+  for (int e = tid; e < w * r; e += kSolveThreads)
+    store_out(jb.w_dec, e, pm[static_cast<int64_t>(w) * r + e], bf16);
+}
+
+template <int DH>
+hipError_t launch_gram_dh(bool bf16, bool derope, const FitGramParams& p, dim3 grid,
+                          hipStream_t stream) {
+  if (bf16) {
+    if (derope) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, false>), grid, dim3(256), 0, stream, p);
+  } else {
+    if (derope) hipLaunchKernelGGL((fit_gram_f32_kernel<DH, true>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((fit_gram_f32_kernel<DH, false>), grid, dim3(256), 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t fit_upper_tiles(int w) {
+  const int64_t nt = 2 * static_cast<int64_t>(w) / kTB;
+  return nt * (nt + 1) / 2;
+}
+
+hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream) {
+  const int64_t units = static_cast<int64_t>(p.n_jobs) * fit_upper_tiles(p.w) * p.n_slices;
+  const dim3 grid(static_cast<unsigned>(units));
+  hipError_t e;
+  switch (p.head_dim) {
+    case 32: e = launch_gram_dh<32>(bf16, p.derope != 0, p, grid, stream); break;
+    case 64: e = launch_gram_dh<64>(bf16, p.derope != 0, p, grid, stream); break;
+    case 128: e = launch_gram_dh<128>(bf16, p.derope != 0, p, grid, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess) return e;
+  const int64_t n2 = 2 * static_cast<int64_t>(p.w);
+  const int64_t per_job = n2 * n2 + n2;
+  int64_t bx = (per_job + 255) / 256;
+  if (bx > 1024) bx = 1024;
+  hipLaunchKernelGGL(fit_gram_reduce_kernel, dim3(static_cast<unsigned>(bx), p.n_jobs), dim3(256),
+                     0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(fit_solve_kernel, dim3(p.n_jobs), dim3(kSolveThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace scd

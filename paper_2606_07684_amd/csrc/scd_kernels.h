@@ -86,6 +86,71 @@ constexpr int kRopeMinRows = 16;
 // head_dim 64 or 128 when a job de-rotates.
 constexpr int kEncodeRows = 128;
 hipError_t launch_encode_bf16(const GemmParams& p, hipStream_t stream);
+// ---- Offline Reuse fit (joint Gram of de-rotated producer/consumer rows, then a small fp64
+// solve).  The Gram of X = [A B] (N rows of 2w columns) is accumulated per 128 x 128 upper tile and
+// per slice of rows into a workspace of partial tiles, then summed over slices in a fixed order.
+constexpr int kFitTile = 128;   // Gram tile edge
+constexpr int kFitRowStep = 64; // rows per k-step of the Gram kernels; slices are multiples of it
+
+struct FitGramJob {
+  const void* a;   // producer cache [T, D] = rows [N, w]
+  const void* b;   // consumer cache
+  float* gram;     // [2w, 2w] out
+  float* colsum;   // [2w] out
+};
+
+struct FitGramParams {
+  FitGramJob jobs[kMaxJobs];
+  int32_t n_jobs;
+  int32_t w;           // basis width; the joint rows have 2w columns
+  int64_t n_rows;      // N = T * g
+  int32_t g;           // rows per token
+  int32_t head_dim;
+  int32_t derope;      // keys: inverse-rotate both caches' rows first
+  int32_t n_slices;
+  int64_t slice_rows;  // multiple of kFitRowStep
+  int32_t n_seqs;
+  int32_t reserved;
+  const int32_t* cu_seqlens;
+  const int32_t* pos0;
+  const float2* rope;
+  int64_t max_pos;
+  float* partial;      // [n_jobs][n_slices][n_upper][kFitTile^2 + kFitTile]
+};
+static_assert(sizeof(FitGramParams) <= 4096, "kernel argument block");
+
+struct FitSolveJob {
+  const float* gram;    // [2w, 2w]
+  const float* colsum;  // [2w]
+  void* w_enc;          // [r, w] out (model dtype)
+  void* w_dec;          // [w, r] out
+  void* mu_enc;         // [w] out, or null (no centring)
+  void* mu_dec;         // [w] out, or null
+  int32_t rank;
+  int32_t reserved;
+};
+
+struct FitSolveParams {
+  FitSolveJob jobs[kMaxJobs];
+  int32_t n_jobs;
+  int32_t w;
+  int64_t n_rows;
+  double lambda;
+  int32_t center;
+  int32_t bf16;
+  int32_t max_sweeps;
+  int32_t reserved;
+  double* work;  // [n_jobs][3][2w][2w] fp64
+};
+static_assert(sizeof(FitSolveParams) <= 4096, "kernel argument block");
+
+// Largest basis width the solve takes (its Jacobi matrix is 2w x 2w in one workgroup).
+constexpr int kFitMaxSolveWidth = 256;
+
+int64_t fit_upper_tiles(int w);  // upper 128 x 128 tiles of the 2w x 2w Gram
+hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream);
+hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream);
+
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,
                              hipStream_t stream);
 hipError_t launch_positions(int32_t* out, int64_t n_tokens, int32_t n_seqs,

@@ -157,6 +157,25 @@ SMALL_ALIGN = Workload("small_align_bf16", 3, 512, 2, 128, (300, 77, 650), (64, 
 # ranks 128 (512-channel chunks) and 256 (256-channel chunks).
 SMALL_MANY_LAYERS = Workload("small_many_layers_bf16", 72, 256, 8, 128, (300, 340),
                              (128,) * 48 + (256,) * 24, (), 5e5, "bf16")
+# Offline Reuse fit (paired producer/consumer calibration caches): ragged batch with start positions,
+# w = D = 128 (one 256 x 256 Gram of three upper tiles, several row slices with a ragged tail);
+# the head-shared basis (w = d_h = 128, g = 4); fp32 with w = 64 (a 128-column Gram that spans the
+# producer and consumer halves); d_h = 32; single-token requests (every position 0, so de-rotated
+# keys keep the shared latent's low rank and the key fit is well conditioned).
+FIT_SMALL_BF16 = Workload("fit_small_bf16", 3, 256, 2, 64, (300, 77, 650), (32, 32, 32), (1,), 1e4,
+                          "bf16", pos0=(0, 40, 7), ranks_v=(48, 48, 48))
+FIT_HEAD_SHARED = Workload("fit_head_shared_bf16", 2, 256, 4, 128, (129, 250), (16, 16), (), 5e5,
+                           "bf16", basis_width=128, ranks_v=(32, 32))
+FIT_F32 = Workload("fit_f32", 2, 128, 2, 64, (200, 61), (16, 16), (), 1e4, "f32", basis_width=64,
+                   ranks_v=(32, 32))
+FIT_DH32 = Workload("fit_dh32_bf16", 2, 128, 4, 32, (333,), (16, 32), (0,), 1e4, "bf16")
+FIT_POS0_KEYS = Workload("fit_single_tokens_bf16", 2, 128, 2, 64, (1,) * 700, (32, 32), (), 1e4,
+                         "bf16", ranks_v=(16, 16))
+FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KEYS)
+# Calibration at the Llama-3-8B shape with the head-shared basis: 8192 tokens x 8 heads = 65,536
+# rows of 128 channels per layer (the paper calibrates on 100-500 prefixes of ~600 tokens).
+FIT_LLAMA3_8B = LLAMA3_8B_HEAD_SHARED.replace(name="fit_llama3_8b_head_shared_bf16")
+
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
                   SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS)
 
@@ -293,6 +312,36 @@ def aligner_weights(wl: Workload, layer: int, device="cpu"):
 def patch_codes(wl: Workload, layer: int, device="cpu") -> torch.Tensor:
     """Patch-layer codes ``Z_H [T, r_H]`` ~ N(0, 1), the aligner's input."""
     return _cast(_randn(wl, layer, "z_h", (wl.n_tokens, wl.rank(layer, "h")), device), wl, device)
+
+
+def fit_spectrum(r: int) -> np.ndarray:
+    """Scales of the shared latent's r directions: evenly spaced from 2 down to 1."""
+    return np.linspace(2.0, 1.0, r)
+
+
+def fit_pair(wl: Workload, layer: int, branch: str, device="cpu", sample: str = "cal"):
+    """Paired calibration caches ``(A, B)`` [T, D] of one layer and branch: the producer's and the
+    consumer's cache over the same prefixes, driven by one shared latent.  Per row of w channels:
+    ``A = mu_A + C diag(s) Q_A^T + N(0, 0.01)`` and ``B = mu_B + C diag(s) Q_B^T + N(0, 0.01)``
+    with ``C ~ N(0, 1)`` [T*g, r] shared, ``s`` from :func:`fit_spectrum`, ``Q_A``, ``Q_B``
+    orthonormal [w, r] and offsets ``mu ~ N(0, 0.1)``.  Drawn directly in the cache layout.
+    ``sample`` names an independent draw of the latent and the noise over the same bases and
+    offsets (e.g. held-out rows of the same model pair)."""
+    r = wl.rank(layer, branch)
+    n = wl.n_tokens * wl.g
+    tag = "" if sample == "cal" else sample + "_"
+    c = _randn(wl, layer, f"fit_latent_{tag}{branch}", (n, r), device)
+    c = c * torch.tensor(fit_spectrum(r), dtype=torch.float32, device=device)[None, :]
+    out = []
+    for side in ("a", "b"):
+        g = np.random.default_rng(_seed(wl, layer, f"fit_basis_{side}_{branch}"))
+        q, rr = np.linalg.qr(g.standard_normal((wl.w, r)))
+        q = torch.from_numpy(q * np.sign(np.diag(rr))[None, :]).to(device=device,
+                                                                    dtype=torch.float32)
+        x = c @ q.T + _randn(wl, layer, f"fit_noise_{tag}{side}_{branch}", (n, wl.w), device) * 0.1
+        x = x + _randn(wl, layer, f"fit_mu_{side}_{branch}", (wl.w,), "cpu").to(device) * np.sqrt(0.1)
+        out.append(_cast(x.reshape(wl.n_tokens, wl.kv_width), wl, device))
+    return out[0], out[1]
 
 
 def cu_seqlens(wl: Workload, device="cpu") -> torch.Tensor:

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), f"libscd.so does not export {n}"
     assert set(names) == set(scd.EXPORTED_SYMBOLS)
-    assert scd.scd_abi_version() == 3
+    assert scd.scd_abi_version() == 4
 
 
 def test_status_strings(lib):
@@ -301,3 +301,88 @@ def test_payload_views_and_streamed_decode_validation(lib):
     # no tokens: an empty payload, nothing to copy or decode, no HIP call
     assert streamed(batch=_batch(n_tokens=0))[0] == OK
     assert streamed(batch=_batch(n_tokens=0), src=None, dst=None)[0] == OK
+
+
+def _fit_gram(lib, model, batch, branch=0, rope=FAKE, maxp=100, ws=FAKE, ws_bytes=1 << 40,
+              **over):
+    L = model.n_layers
+    keep, args = [], {}
+    for name in ("a_in", "b_in", "gram", "colsum"):
+        if name in over:
+            args[name] = over[name]
+        else:
+            p, a = _ptrs(L)
+            keep.append(a)
+            args[name] = p
+    st = lib.scd_fit_gram(ctypes.byref(model._c), ctypes.byref(batch._c), rope, maxp, branch,
+                          args["a_in"], args["b_in"], args["gram"], args["colsum"], ws, ws_bytes,
+                          None)
+    return st, lib.scd_last_error().decode()
+
+
+def _fit_solve(lib, model, branch=0, n_rows=100, lam=0.1, center=1, ws=FAKE, ws_bytes=1 << 40,
+               **over):
+    L = model.n_layers
+    keep, args = [], {}
+    for name in ("gram", "colsum", "w_enc", "w_dec", "mu_enc", "mu_dec"):
+        if name in over:
+            args[name] = over[name]
+        else:
+            p, a = _ptrs(L)
+            keep.append(a)
+            args[name] = p
+    st = lib.scd_fit_solve(ctypes.byref(model._c), branch, n_rows, lam, center, args["gram"],
+                           args["colsum"], args["w_enc"], args["w_dec"], args["mu_enc"],
+                           args["mu_dec"], ws, ws_bytes, None)
+    return st, lib.scd_last_error().decode()
+
+
+def test_fit_validation(lib):
+    m = _model()  # w = D = 128, two Reuse layers
+    b = _batch()
+    # branch, basis width, tokens
+    assert _fit_gram(lib, m, b, branch=2)[0] == SHAPE
+    assert _fit_gram(lib, _model(n_kv_heads=1, head_dim=32, rank_k=[16] * 3, rank_v=[16] * 3),
+                     b)[0] == UNSUP  # w = 32 is not a multiple of 64
+    assert _fit_gram(lib, m, _batch(n_tokens=0))[0] == SHAPE
+    # pointers, RoPE table (keys only), workspace
+    p, keep = _ptrs(3, skip=(2,))
+    st, msg = _fit_gram(lib, m, b, b_in=p)
+    assert st == NULL and "b_in[2]" in msg
+    assert _fit_gram(lib, m, b, rope=None)[0] == WS
+    assert _fit_gram(lib, m, b, ws=None)[0] == NULL
+    assert _fit_gram(lib, m, b, ws=FAKE + 8)[0] == ALIGN
+    st, msg = _fit_gram(lib, m, b, ws_bytes=1024)
+    assert st == SHAPE and "workspace" in msg
+    # solve
+    assert _fit_solve(lib, m, branch=-1)[0] == SHAPE
+    assert _fit_solve(lib, m, n_rows=0)[0] == SHAPE
+    assert _fit_solve(lib, m, lam=-1.0)[0] == SHAPE
+    assert _fit_solve(lib, m, lam=float("nan"))[0] == SHAPE
+    assert _fit_solve(lib, m, center=2)[0] == SHAPE
+    assert _fit_solve(lib, _model(rank_v=[32, 32, 24]), branch=1)[0] == SCHED
+    assert _fit_solve(lib, _model(rank_k=[144, 32, 32]))[0] == SCHED  # > basis width 128
+    wide = _model(n_kv_heads=6, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 384 > 256
+    assert _fit_solve(lib, wide)[0] == UNSUP
+    pm, keepm = _ptrs(3, skip=(0,))
+    st, msg = _fit_solve(lib, m, mu_dec=pm)
+    assert st == NULL and "mu_dec[0]" in msg
+    solve_need = 2 * 3 * 256 * 256 * 8  # two Reuse layers, w = 128
+    st, msg = _fit_solve(lib, m, ws_bytes=solve_need - 8)
+    assert st == SHAPE and "workspace" in msg
+
+
+def test_fit_workspace_bytes_cover_both_calls(lib):
+    # Gram partials: jobs x slices x upper tiles x (128^2 + 128) floats; solve: 3 (2w)^2 doubles
+    # per job.  One Reuse-only model, w = 128 (one 256 x 256 Gram = 3 upper tiles).
+    m = _model(is_patch=[0, 0, 0])
+    for T in (1, 100, 511, 512, 5000, 200000):
+        units = 3 * 3
+        ns = min(-(-1024 // units), max(1, -(-T // 512)))
+        sr = -(-T // ns)
+        sr = -(-sr // 64) * 64
+        ns = -(-T // sr)
+        gram = 3 * ns * 3 * (128 * 128 + 128) * 4
+        solve = 3 * 3 * 256 * 256 * 8
+        assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), T) == max(gram, solve)
+    assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), 0) == 0
