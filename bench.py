@@ -195,6 +195,79 @@ def time_aligner(wl, dev, steps, warmup, stream):
             "frac": round(ach / peak, 4), "alg_flops": flops, "alg_bytes": nbytes}
 
 
+def time_fit(dev, steps, warmup, stream):
+    """The offline Reuse fit at the Llama-3-8B shape with the head-shared basis (w = d_h = 128:
+    8192 tokens x 8 heads = 65,536 calibration rows per layer, 28 Reuse layers): ``scd_fit_gram``
+    and ``scd_fit_solve`` for keys and values, HIP events on the stream they run on.  The Gram is
+    HBM-bound (2w = 256 columns: about 128 flops per byte of the symmetric product); algorithmic
+    bytes read both caches once and write the Gram and column sums once.  The solve is the
+    O(w^3) fp64 step, one workgroup per layer, reported as time per call."""
+    import torch
+
+    import paper_2606_07684_amd as scd
+    from synth import workloads as W
+
+    wl = W.FIT_LLAMA3_8B
+    L, T, D, w, g = wl.n_layers, wl.n_tokens, wl.kv_width, wl.w, wl.g
+    R = [l for l in range(L) if not wl.is_patch[l]]
+    model = scd.Model(n_layers=L, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
+                      head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
+                      is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
+                      basis_width=w)
+    batch = scd.Batch(n_tokens=T)
+    rope = scd.scd_rope_table(model, wl.max_position)
+    ws = torch.empty(scd.scd_fit_workspace_bytes(model, T), dtype=torch.uint8, device=dev)
+    n2 = 2 * w
+    grams, solves = [], []
+    keep = []  # every tensor the prepared calls point to stays alive until the timing ends
+    for br, code in (("k", scd.FIT_KEYS), ("v", scd.FIT_VALUES)):
+        a_in, b_in, gram, colsum, w_enc, w_dec, mu_e, mu_d = ([None] * L for _ in range(8))
+        keep.append((a_in, b_in, gram, colsum, w_enc, w_dec, mu_e, mu_d))
+        ranks = wl.ranks if br == "k" else wl.rank_v
+        for l in R:
+            a_in[l], b_in[l] = W.fit_pair(wl, l, br, dev)
+            gram[l] = torch.empty((n2, n2), dtype=torch.float32, device=dev)
+            colsum[l] = torch.empty((n2,), dtype=torch.float32, device=dev)
+            w_enc[l] = torch.empty((ranks[l], w), dtype=wl.torch_dtype, device=dev)
+            w_dec[l] = torch.empty((w, ranks[l]), dtype=wl.torch_dtype, device=dev)
+            mu_e[l] = torch.empty((w,), dtype=wl.torch_dtype, device=dev)
+            mu_d[l] = torch.empty((w,), dtype=wl.torch_dtype, device=dev)
+        grams.append(scd.prepare_fit_gram(model, batch, rope if br == "k" else None, code, a_in,
+                                          b_in, gram, colsum, ws))
+        solves.append(scd.prepare_fit_solve(model, code, T * g, 0.05 * T * g, True, gram, colsum,
+                                            w_enc, w_dec, mu_e, mu_d, ws))
+    torch.cuda.synchronize()
+
+    def timed(calls, n, nw):
+        for _ in range(nw):
+            for c in calls:
+                c(stream)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(n):
+            for c in calls:
+                c(stream)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    gram_ms = timed(grams, steps, warmup)
+    solve_ms = timed(solves, max(1, steps // 4), 1)
+    nbytes = 2 * len(R) * (2 * T * D * wl.elem_bytes + (n2 * n2 + n2) * 4)  # both branches
+    flops = 2 * len(R) * (T * g) * n2 * (n2 + 1)  # symmetric X^T X
+    ach = nbytes / (gram_ms * 1e-3) / 1e9
+    return {"config": {"workload": wl.name, "n_tokens": T, "rows_per_layer": T * g,
+                       "basis_width": w, "reuse_layers": len(R), "rank_k": wl.ranks[R[0]],
+                       "rank_v": wl.rank_v[R[0]]},
+            "gram": {"kernel": "fit_gram_bf16_kernel", "ms_per_call": round(gram_ms / 2, 4),
+                     "calls": 2, "bound": "hbm", "achieved": round(ach, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                     "alg_bytes": nbytes, "alg_flops": flops,
+                     "tflops": round(flops / (gram_ms * 1e-3) / 1e12, 2)},
+            "solve": {"kernel": "fit_solve_kernel", "ms_per_call": round(solve_ms / 2, 3),
+                      "calls": 2, "layers_per_call": len(R)}}
+
+
 def time_receive(wl, dev, steps, warmup, stream, model, batch, rope, inp, z_k, z_v, z_h,
                  k_cache, v_cache):
     """The consumer's receipt of the packed payload from pinned host memory (PCIe-inclusive;
@@ -291,6 +364,8 @@ def main():
     ap.add_argument("--no-receive", action="store_true",
                     help="skip the receipt timing (its decode launches share the step's kernel "
                          "and grid, so kernel traces of the step leave it out)")
+    ap.add_argument("--no-fit", action="store_true",
+                    help="skip the offline fit timing (it runs after the step's timing)")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run a plain copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -422,12 +497,19 @@ def main():
     # The Patch aligner (Eq. aligner, the row after the hot path): timed on its own over the same
     # step count, reported beside the step and not part of ``value``.
     if any(wl.is_patch):
+        print("[bench] timing the aligner", file=sys.stderr, flush=True)
         out["aligner"] = time_aligner(wl, dev, args.steps, args.warmup, stream)
 
     # The consumer's receipt from host memory (PCIe-inclusive), beside the step.
     if not args.no_receive:
+        print("[bench] timing the streamed receipt", file=sys.stderr, flush=True)
         out["receive"] = time_receive(wl, dev, args.steps, args.warmup, stream, model, batch, rope,
                                       inp, z_k, z_v, z_h, k_cache, v_cache)
+
+    # The offline Reuse fit (Section 4.3.1), at the head-shared calibration shape, beside the step.
+    if not args.no_fit:
+        print("[bench] timing the offline fit", file=sys.stderr, flush=True)
+        out["fit"] = time_fit(dev, args.steps, args.warmup, stream)
 
     # The combined readings of the decode-side target (Reuse decode + Patch at this workload):
     #   reuse_hbm_frac:   Reuse algorithmic bytes / t_reuse / 8 TB/s

@@ -560,12 +560,16 @@ __global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolve
     __syncthreads();
   }
 
-  // the r largest eigenvalues (ties by index), in decreasing order
+  // the r largest eigenvalues in decreasing order.  The order is total (NaN counts as -inf and
+  // ties go to the lower index), so the ranks are a permutation of [0, n) and every sel[k], k < r,
+  // is written even when non-finite inputs reached the matrix.
   for (int i = tid; i < n; i += kSolveThreads) {
-    const double li = mj[i * n + i];
+    const double di = mj[i * n + i];
+    const double li = isnan(di) ? -INFINITY : di;
     int cnt = 0;
     for (int j = 0; j < n; ++j) {
-      const double lj = mj[j * n + j];
+      const double dj = mj[j * n + j];
+      const double lj = isnan(dj) ? -INFINITY : dj;
       cnt += (lj > li || (lj == li && j < i)) ? 1 : 0;
     }
     if (cnt < r) sel[cnt] = i;

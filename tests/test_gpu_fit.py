@@ -188,3 +188,62 @@ def test_fitted_translator_through_the_codec():
         # the translator generalises: held-out consumer rows within the noise level
         assert U.max_abs_rel(want_v, U.f64(held["v"][1][l])) < 0.2
     U.assert_within(errs, U.TOL[wl.dtype], "fitted translator through the codec")
+
+
+def test_fit_full_size_sampled_layers():
+    # The calibration shape bench.py times (65,536 rows of the head-shared basis per layer): the
+    # Gram of two layers per branch against the oracle, and the values' fit.
+    wl = W.FIT_LLAMA3_8B
+    dev = torch.device("cuda")
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    L, n2, T = wl.n_layers, 2 * wl.w, wl.n_tokens
+    layers = [1, L - 1]
+    ws = torch.empty(scd.scd_fit_workspace_bytes(model, T), dtype=torch.uint8, device=dev)
+    pos = U.host_positions(wl)
+    for br in ("k", "v"):
+        a_in, b_in = [None] * L, [None] * L
+        R = [l for l in range(L) if not wl.is_patch[l]]
+        for l in R:
+            a_in[l], b_in[l] = W.fit_pair(wl, l, br, dev)
+        rope = scd.scd_rope_table(model, wl.max_position) if br == "k" else None
+        print(f"[fit full size] branch={br} rows={T * wl.g} layers={len(R)}", flush=True)
+        w_enc, w_dec, mu_enc, mu_dec, gram, colsum = scd.fit_reuse(
+            model, batch, rope, BRANCHES[br], a_in, b_in, _lam(wl), center=True)
+        torch.cuda.synchronize()
+        errs = {}
+        for l in layers:
+            G, s = O.fit_gram(U.f64(a_in[l]), U.f64(b_in[l]), pos, wl.n_kv_heads, wl.head_dim,
+                              wl.rope_theta, wl.w, br == "k")
+            errs[("gram", l)] = U.max_abs_rel(U.f64(gram[l]), G)
+            errs[("colsum", l)] = U.max_abs_rel(U.f64(colsum[l]), s)
+            if br == "v":
+                e_o, d_o, ma_o, mb_o = _oracle_fit(wl, br, a_in, b_in, l, _lam(wl))
+                errs[("w_enc", l)] = U.max_abs_rel(U.f64(w_enc[l]), e_o)
+                errs[("w_dec", l)] = U.max_abs_rel(U.f64(w_dec[l]), d_o)
+                errs[("mu_enc", l)] = U.max_abs_rel(U.f64(mu_enc[l]), ma_o)
+                errs[("mu_dec", l)] = U.max_abs_rel(U.f64(mu_dec[l]), mb_o)
+        for l in R:
+            assert torch.isfinite(w_enc[l]).all() and torch.isfinite(w_dec[l]).all()
+        U.assert_within(errs, U.TOL[wl.dtype], f"fit full size {br}")
+
+
+def test_fit_solve_contains_non_finite_input():
+    # A Gram with NaN (e.g. from NaN in the caches) gives NaN outputs for its own layer only; the
+    # eigenvalue ranking stays a permutation, so the solve reads nothing outside its workspace.
+    wl = W.FIT_SMALL_BF16
+    dev = torch.device("cuda")
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    R, a_in, b_in, _ = _setup(wl, "v", dev)
+    lam = _lam(wl)
+    w_enc, w_dec, mu_enc, mu_dec, gram, colsum = scd.fit_reuse(model, batch, None, scd.FIT_VALUES,
+                                                               a_in, b_in, lam, center=True)
+    ref = [t.clone() if t is not None else None for t in w_dec]
+    bad, good = R[0], R[1]
+    gram[bad][3, :] = float("nan")
+    gram[bad][:, 3] = float("nan")
+    ws = torch.empty(scd.scd_fit_workspace_bytes(model, wl.n_tokens), dtype=torch.uint8, device=dev)
+    scd.scd_fit_solve(model, scd.FIT_VALUES, wl.n_tokens * wl.g, lam, True, gram, colsum, w_enc,
+                      w_dec, mu_enc, mu_dec, ws)
+    torch.cuda.synchronize()
+    assert torch.isnan(w_dec[bad].float()).any()
+    assert torch.equal(w_dec[good], ref[good])
