@@ -251,7 +251,9 @@ def time_fit(dev, steps, warmup, stream):
         torch.cuda.synchronize()
         return ev[0].elapsed_time(ev[1]) / n
 
-    gram_ms = timed(grams, steps, warmup)
+    gram_k = timed(grams[:1], steps, warmup)
+    gram_v = timed(grams[1:], steps, warmup)
+    gram_ms = gram_k + gram_v
     solve_ms = timed(solves, max(1, steps // 4), 1)
     nbytes = 2 * len(R) * (2 * T * D * wl.elem_bytes + (n2 * n2 + n2) * 4)  # both branches
     flops = 2 * len(R) * (T * g) * n2 * (n2 + 1)  # symmetric X^T X
@@ -260,6 +262,7 @@ def time_fit(dev, steps, warmup, stream):
                        "basis_width": w, "reuse_layers": len(R), "rank_k": wl.ranks[R[0]],
                        "rank_v": wl.rank_v[R[0]]},
             "gram": {"kernel": "fit_gram_bf16_kernel", "ms_per_call": round(gram_ms / 2, 4),
+                     "ms_keys": round(gram_k, 4), "ms_values": round(gram_v, 4),
                      "calls": 2, "bound": "hbm", "achieved": round(ach, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                      "alg_bytes": nbytes, "alg_flops": flops,

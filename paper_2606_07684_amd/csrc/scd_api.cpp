@@ -743,11 +743,12 @@ namespace {
 
 constexpr int kFitMaxSweeps = 40;
 
-// Slices of the row axis for a Gram launch of n_jobs jobs: about four workgroups per CU over the
-// whole launch, at least 512 rows per slice, slice lengths a multiple of the kernels' k-step.
+// Slices of the row axis for a Gram launch of n_jobs jobs: at most 1024 workgroups (two rounds of
+// two per CU) when the tiles allow, at least 512 rows per slice, slice lengths a multiple of the
+// kernels' k-step.
 int64_t fit_slices(int n_jobs, int w, int64_t n_rows, int64_t* slice_rows) {
   const int64_t units = static_cast<int64_t>(n_jobs) * scd::fit_upper_tiles(w);
-  int64_t ns = (1024 + units - 1) / units;
+  int64_t ns = 1024 / units;
   const int64_t max_ns = (n_rows + 511) / 512;
   if (ns > max_ns) ns = max_ns;
   if (ns < 1) ns = 1;

@@ -62,6 +62,21 @@ __device__ inline int pair_col(int cp) {
   return (cp / PER_HEAD) * DH + (cp % PER_HEAD) * VEC;
 }
 
+// Loads through the global address space.  The row pointers come out of the job table through a
+// select between two sources, which hides their address space from the compiler; as generic (flat)
+// loads they would also count against the LDS counter, so every LDS wait would drain them.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 g_u32x4;
+typedef __attribute__((address_space(1))) const f32x4 g_f32x4;
+__device__ inline uint4 gload16(const char* p) {
+  const u32x4 v = *(g_u32x4*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline float4 gload_f4(const float2* p) {
+  const f32x4 v = *(g_f32x4*)(p);
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
 struct BlockSrc {
   const char* base;  // producer or consumer cache
   int col;           // column inside the w-wide row
@@ -82,20 +97,27 @@ __device__ inline BlockSrc block_src(const FitGramJob& j, int w, int jc, int eb)
 // operand fragment is 8 consecutive rows of one column) and runs v_mfma_f32_32x32x16_bf16 with the
 // I block as A and the J block as B: C[m][n] = sum_rows X[row][I0+m] X[row][J0+n].  Keys are
 // de-rotated in registers and rounded to bf16 once before the product (as the encoder does).
-// Thread t stages row pair t % 32 and chunk pair t / 32 (8 columns + their RoPE partners); the
-// next k-step's rows are loaded while the current one's MFMAs run.
+// Thread t stages row pair t % 32 and chunk pair t / 32 (8 columns + their RoPE partners).
+//
+// The step is bound by HBM latency, so rows travel two k-steps ahead in two register sets and the
+// RoPE factors one step ahead; each is issued before the far data prefetch, so the in-order
+// vector-memory counter never makes a step wait for rows it does not use yet.  The LDS tiles are
+// double-buffered, which leaves one barrier per step, and that barrier waits for LDS only.
+// PAIR: both rows of a thread's pair belong to one token (g even), so they share RoPE factors.
 // ---------------------------------------------------------------------------------------------
-template <int DH, bool DEROPE>
-__global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams p) {
-  constexpr int BK = kFitRowStep, S = BK + 8, HALF = DH / 2;
-  __shared__ __attribute__((aligned(16))) uint16_t xt[2][kTB * S];
+template <int DH, bool DEROPE, bool PAIR>
+__global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramParams p) {
+  constexpr int BK = kFitRowStep, S = BK + 8, HALF = DH / 2, NR = PAIR ? 1 : 2;
+  __shared__ __attribute__((aligned(16))) uint16_t xt[2][2][kTB * S];  // [stage][block]
 
   const int nt = 2 * p.w / kTB, n_upper = nt * (nt + 1) / 2;
-  int unit = blockIdx.x;
-  const int slice = unit % p.n_slices;
-  unit /= p.n_slices;
+  // the tiles of one (job, slice) read the same rows: consecutive units on one XCD, so the second
+  // read of a column block hits that XCD's L2
+  int unit = xcd_remap(blockIdx.x, gridDim.x);
   const int tile = unit % n_upper;
-  const int job = unit / n_upper;
+  unit /= n_upper;
+  const int slice = unit % p.n_slices;
+  const int job = unit / p.n_slices;
   int ti, tj;
   tile_of(tile, nt, ti, tj);
   const bool diag = ti == tj;
@@ -104,16 +126,20 @@ __global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams 
   const int64_t r0 = static_cast<int64_t>(slice) * p.slice_rows;
   const int64_t r1 = r0 + p.slice_rows < p.n_rows ? r0 + p.slice_rows : p.n_rows;
   const int64_t row_bytes = static_cast<int64_t>(p.w) * 2;
+  const int tj_src = diag ? ti : tj;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int rp = tid & 31, cp = tid >> 5;
+  // eight consecutive lanes cover the eight chunk pairs of one row pair: a load instruction reads
+  // 8 rows x 128 contiguous bytes
+  const int cp = tid & 7, rp = tid >> 3;
   const int c = pair_col<DH, 8>(cp);
   const int ri = c % DH;  // RoPE pair index of the first column (< d_h / 2)
   BlockSrc src[2];
   src[0] = block_src(jb, p.w, ti * kTB + c, 2);
-  src[1] = block_src(jb, p.w, tj * kTB + c, 2);
+  src[1] = block_src(jb, p.w, tj_src * kTB + c, 2);
 
-  uint4 ld[2][2][2];  // [block][row of the pair][first half / partner]
+  uint4 la[2][2][2], lb[2][2][2];  // [block][row of the pair][first half / partner]
+  float4 rc[NR][4];                // RoPE (cos, sin) of the next step's rows, pairs ri .. ri+7
   float csum[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) csum[i] = 0.f;
@@ -126,87 +152,89 @@ __global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams 
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
-  auto issue_loads = [&](int64_t k0) {
+  // Every step issues the same loads on every path (rows past the slice read its last row and are
+  // zeroed when staged; a diagonal tile's J block re-reads its I block from L1/L2), so the
+  // compiler's counter waits can leave the far prefetch in flight.
+  auto issue_rows = [&](uint4 (&ld)[2][2][2], int64_t k0) {
 #pragma unroll
     for (int rr = 0; rr < 2; ++rr) {
-      const int64_t n = k0 + 2 * rp + rr;
+      int64_t n = k0 + 2 * rp + rr;
+      n = n < r1 ? n : r1 - 1;
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        if (b < nblk && n < r1) {
-          const char* rowp = src[b].base + n * row_bytes + src[b].col;
-          ld[b][rr][0] = *reinterpret_cast<const uint4*>(rowp);
-          ld[b][rr][1] = *reinterpret_cast<const uint4*>(rowp + HALF * 2);
-        } else {
-          ld[b][rr][0] = zero4;
-          ld[b][rr][1] = zero4;
-        }
+        const char* rowp = src[b].base + n * row_bytes + src[b].col;
+        ld[b][rr][0] = gload16(rowp);
+        ld[b][rr][1] = gload16(rowp + HALF * 2);
       }
     }
   };
-
-  const int wy = wave >> 1, wx = wave & 1;
-  const int h = lane >> 5;
-  const uint16_t* xa = xt[0] + (wy * 64 + (lane & 31)) * S + 8 * h;
-  const uint16_t* xb = xt[diag ? 0 : 1] + (wx * 64 + (lane & 31)) * S + 8 * h;
-
-  if (r0 < r1) issue_loads(r0);
-  for (int64_t k0 = r0; k0 < r1; k0 += BK) {
-    // de-rotate (keys) and round the staged rows; accumulate the diagonal tile's column sums
-    uint32_t pk[2][2][8];  // [block][first half / partner][column]: rows 2rp (low), 2rp+1 (high)
+  auto issue_rope = [&](int64_t k0) {
+    if constexpr (DEROPE) {
+#pragma unroll
+      for (int q = 0; q < NR; ++q) {
+        const int64_t n = k0 + 2 * rp + q;
+        const float2* tab = p.rope + static_cast<int64_t>(n < r1 ? fit_position(p, n) : 0) * HALF + ri;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) rc[q][j] = gload_f4(tab + 2 * j);
+      }
+    }
+  };
+  // de-rotate (keys), round, and write one k-step's rows into LDS stage sb; accumulate the diagonal
+  // tile's column sums
+  auto stage = [&](const uint4 (&ld)[2][2][2], int64_t k0, int sb) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       if (b >= nblk) break;
       float f[2][2][8];
 #pragma unroll
       for (int rr = 0; rr < 2; ++rr) {
-        unpack8(ld[b][rr][0], f[rr][0]);
-        unpack8(ld[b][rr][1], f[rr][1]);
+        const bool live = k0 + 2 * rp + rr < r1;
+        unpack8(live ? ld[b][rr][0] : zero4, f[rr][0]);
+        unpack8(live ? ld[b][rr][1] : zero4, f[rr][1]);
         if constexpr (DEROPE) {
-          const int64_t n = k0 + 2 * rp + rr;
-          if (n < r1) {
-            const float2* tab = p.rope + static_cast<int64_t>(fit_position(p, n)) * HALF + ri;
+          const int q = PAIR ? 0 : rr;
 #pragma unroll
-            for (int j = 0; j < 8; j += 2) {
-              const float4 cs = *reinterpret_cast<const float4*>(tab + j);
-              const float u0 = f[rr][0][j], v0 = f[rr][1][j];
-              const float u1 = f[rr][0][j + 1], v1 = f[rr][1][j + 1];
-              // inverse rotation by the position's angle
-              f[rr][0][j] = u0 * cs.x + v0 * cs.y;
-              f[rr][1][j] = v0 * cs.x - u0 * cs.y;
-              f[rr][0][j + 1] = u1 * cs.z + v1 * cs.w;
-              f[rr][1][j + 1] = v1 * cs.z - u1 * cs.w;
-            }
+          for (int j = 0; j < 4; ++j) {
+            const float4 cs = rc[q][j];
+            const float u0 = f[rr][0][2 * j], v0 = f[rr][1][2 * j];
+            const float u1 = f[rr][0][2 * j + 1], v1 = f[rr][1][2 * j + 1];
+            // inverse rotation by the position's angle
+            f[rr][0][2 * j] = u0 * cs.x + v0 * cs.y;
+            f[rr][1][2 * j] = v0 * cs.x - u0 * cs.y;
+            f[rr][0][2 * j + 1] = u1 * cs.z + v1 * cs.w;
+            f[rr][1][2 * j + 1] = v1 * cs.z - u1 * cs.w;
           }
         }
       }
+      uint32_t* dst = reinterpret_cast<uint32_t*>(xt[sb][b]);
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          pk[b][q][j] = pack_bf16x2(f[0][q][j], f[1][q][j]);
-          if (b == 0 && diag) csum[8 * q + j] += bf16_lo(pk[b][q][j]) + bf16_hi(pk[b][q][j]);
+          const uint32_t v = pack_bf16x2(f[0][q][j], f[1][q][j]);  // rows 2rp (low), 2rp+1 (high)
+          if (b == 0 && diag) csum[8 * q + j] += bf16_lo(v) + bf16_hi(v);
+          const int col = c + q * HALF + j;
+          dst[col * (S / 2) + ((((rp >> 2) ^ (col >> 3)) & 7) << 2) + (rp & 3)] = v;
         }
     }
-    __syncthreads();  // every wave has finished reading the previous k-step's tiles
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      if (b >= nblk) break;
-      uint32_t* dst = reinterpret_cast<uint32_t*>(xt[b]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        dst[((c + j) * S) / 2 + rp] = pk[b][0][j];
-        dst[((c + HALF + j) * S) / 2 + rp] = pk[b][1][j];
-      }
-    }
-    __syncthreads();
-    if (k0 + BK < r1) issue_loads(k0 + BK);
+  };
+
+  const int wy = wave >> 1, wx = wave & 1;
+  const int h = lane >> 5;
+  // LDS tile layout: row group kg (8 rows) of column col sits at slot kg ^ ((col >> 3) & 7) of the
+  // column's padded row, so neither the transposed writes nor the fragment reads conflict
+  const int jblk = diag ? 0 : 1;
+  auto frag = [&](const uint16_t* base, int col, int kg) {
+    return *reinterpret_cast<const bf16x8*>(base + col * S + (((kg ^ (col >> 3)) & 7) << 3));
+  };
+  auto products = [&](int sb) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 fa[2], fb[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        fa[i] = *reinterpret_cast<const bf16x8*>(xa + i * 32 * S + ks * 16);
-        fb[i] = *reinterpret_cast<const bf16x8*>(xb + i * 32 * S + ks * 16);
+        fa[i] = frag(xt[sb][0], wy * 64 + i * 32 + (lane & 31), 2 * ks + h);
+        fb[i] = frag(xt[sb][jblk], wx * 64 + i * 32 + (lane & 31), 2 * ks + h);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -214,6 +242,37 @@ __global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams 
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
+  };
+
+  // prologue: rows of steps 0 and 1 in flight, RoPE of step 0 ahead of the step-1 rows.  Steps run
+  // in pairs; a slice with an odd step count ends with a step of zeroed rows.
+  // The scheduling fences keep each group of loads in issue order, so that the counter waits of a
+  // step cover its own rows only.
+  issue_rows(la, r0);
+  __builtin_amdgcn_sched_barrier(0);
+  issue_rope(r0);
+  __builtin_amdgcn_sched_barrier(0);
+  issue_rows(lb, r0 + BK);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int64_t k0 = r0; k0 < r1; k0 += 2 * BK) {
+    stage(la, k0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_rope(k0 + BK);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_rows(la, k0 + 2 * BK);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    products(0);
+    __builtin_amdgcn_sched_barrier(0);
+    stage(lb, k0 + BK, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_rope(k0 + 2 * BK);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_rows(lb, k0 + 3 * BK);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    products(1);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   float* out = p.partial + ((static_cast<int64_t>(job) * p.n_slices + slice) * n_upper + tile) *
@@ -229,16 +288,25 @@ __global__ __launch_bounds__(256) void fit_gram_bf16_kernel(const FitGramParams 
         out[m * kTB + n] = acc[i][j][r];
       }
   if (diag) {
+    // a chunk pair's rows are spread over the lanes tid % 8 == cp of every wave: reduce in the
+    // wave, then over the four waves through LDS (the tiles are no longer read)
 #pragma unroll
     for (int i = 0; i < 16; ++i)
 #pragma unroll
-      for (int o = 16; o >= 1; o >>= 1) csum[i] += __shfl_xor(csum[i], o, 64);
-    if (rp == 0) {
+      for (int o = 8; o <= 32; o <<= 1) csum[i] += __shfl_xor(csum[i], o, 64);
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(&xt[0][0][0]);  // [wave][cp][16]
+    if (lane < 8) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        out[kTB * kTB + c + j] = csum[j];
-        out[kTB * kTB + c + HALF + j] = csum[8 + j];
-      }
+      for (int i = 0; i < 16; ++i) red[(wave * 8 + cp) * 16 + i] = csum[i];
+    }
+    __syncthreads();
+    if (tid < 8 * 16) {
+      const int pc = tid >> 4, i = tid & 15;
+      const float v = red[(0 * 8 + pc) * 16 + i] + red[(1 * 8 + pc) * 16 + i] +
+                      red[(2 * 8 + pc) * 16 + i] + red[(3 * 8 + pc) * 16 + i];
+      const int cc = pair_col<DH, 8>(pc) + (i >> 3) * HALF + (i & 7);
+      out[kTB * kTB + cc] = v;
     }
   }
 }
@@ -254,11 +322,13 @@ __global__ __launch_bounds__(256) void fit_gram_f32_kernel(const FitGramParams p
   __shared__ __attribute__((aligned(16))) float xs[2][BK * LD];
 
   const int nt = 2 * p.w / kTB, n_upper = nt * (nt + 1) / 2;
-  int unit = blockIdx.x;
-  const int slice = unit % p.n_slices;
-  unit /= p.n_slices;
+  // the tiles of one (job, slice) read the same rows: consecutive units on one XCD, so the second
+  // read of a column block hits that XCD's L2
+  int unit = xcd_remap(blockIdx.x, gridDim.x);
   const int tile = unit % n_upper;
-  const int job = unit / n_upper;
+  unit /= n_upper;
+  const int slice = unit % p.n_slices;
+  const int job = unit / p.n_slices;
   int ti, tj;
   tile_of(tile, nt, ti, tj);
   const bool diag = ti == tj;
@@ -295,8 +365,11 @@ __global__ __launch_bounds__(256) void fit_gram_f32_kernel(const FitGramParams p
       float4 u = make_float4(0.f, 0.f, 0.f, 0.f), v = u;
       if (n < r1) {
         const char* rowp = src[b].base + n * row_bytes + src[b].col;
-        u = *reinterpret_cast<const float4*>(rowp);
-        v = *reinterpret_cast<const float4*>(rowp + HALF * 4);
+        const uint4 ui = gload16(rowp), vi = gload16(rowp + HALF * 4);
+        u = make_float4(__uint_as_float(ui.x), __uint_as_float(ui.y), __uint_as_float(ui.z),
+                        __uint_as_float(ui.w));
+        v = make_float4(__uint_as_float(vi.x), __uint_as_float(vi.y), __uint_as_float(vi.z),
+                        __uint_as_float(vi.w));
       }
       f[b][0][0] = u.x; f[b][0][1] = u.y; f[b][0][2] = u.z; f[b][0][3] = u.w;
       f[b][1][0] = v.x; f[b][1][1] = v.y; f[b][1][2] = v.z; f[b][1][3] = v.w;
@@ -370,33 +443,47 @@ __global__ __launch_bounds__(256) void fit_gram_f32_kernel(const FitGramParams p
 }
 
 // Sums each job's partial tiles over its slices in slice order (so the result does not depend on
-// scheduling) and writes the full symmetric Gram (element (i, j) and (j, i) both come from the
-// upper tile's (min, max) element) and the column sums.
+// scheduling) and writes the full symmetric Gram and the column sums.  A workgroup owns one 32 x 32
+// sub-block of an upper tile: it reads the partials coalesced, writes the block in place and its
+// mirror image through an LDS transpose.  Inside a diagonal tile only sub-blocks on or above its
+// diagonal run, and a diagonal sub-block takes element (min, max) for both (i, j) and (j, i), so the
+// Gram is exactly symmetric.
 __global__ __launch_bounds__(256) void fit_gram_reduce_kernel(const FitGramParams p) {
   const int n2 = 2 * p.w, nt = n2 / kTB, n_upper = nt * (nt + 1) / 2;
   const int job = blockIdx.y;
+  const int tile = blockIdx.x / 16, sub = blockIdx.x % 16, sr = sub / 4, sc = sub % 4;
+  int ti, tj;
+  tile_of(tile, nt, ti, tj);
+  const bool diag = ti == tj;
+  if (diag && sr > sc) return;
   const FitGramJob& jb = p.jobs[job];
-  const float* base = p.partial + static_cast<int64_t>(job) * p.n_slices * n_upper * kTileFloats;
+  const float* base = p.partial + (static_cast<int64_t>(job) * p.n_slices * n_upper + tile) *
+                                      static_cast<int64_t>(kTileFloats);
   const int64_t slice_stride = static_cast<int64_t>(n_upper) * kTileFloats;
-  const int64_t total = static_cast<int64_t>(n2) * n2 + n2;
-  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += gridDim.x * 256) {
-    int64_t off;
-    if (e < static_cast<int64_t>(n2) * n2) {
-      int i = static_cast<int>(e / n2), j = static_cast<int>(e % n2);
-      if (i > j) {
-        const int t = i; i = j; j = t;
-      }
-      const int tile = upper_index(i / kTB, j / kTB, nt);
-      off = static_cast<int64_t>(tile) * kTileFloats + (i % kTB) * kTB + (j % kTB);
-    } else {
-      const int i = static_cast<int>(e - static_cast<int64_t>(n2) * n2);
-      const int tile = upper_index(i / kTB, i / kTB, nt);
-      off = static_cast<int64_t>(tile) * kTileFloats + kTB * kTB + (i % kTB);
-    }
-    float s = 0.f;
-    for (int sl = 0; sl < p.n_slices; ++sl) s += base[sl * slice_stride + off];
-    if (e < static_cast<int64_t>(n2) * n2) jb.gram[e] = s;
-    else jb.colsum[e - static_cast<int64_t>(n2) * n2] = s;
+  __shared__ float blk[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = ty + 8 * k;
+    const int off = (sr * 32 + r) * kTB + sc * 32 + tx;
+    float v = 0.f;
+    for (int sl = 0; sl < p.n_slices; ++sl) v += base[sl * slice_stride + off];
+    blk[r][tx] = v;
+  }
+  __syncthreads();
+  const int i0 = ti * kTB + sr * 32, j0 = tj * kTB + sc * 32;
+  const bool dsub = diag && sr == sc;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = ty + 8 * k;
+    const float up = dsub && r > tx ? blk[tx][r] : blk[r][tx];
+    jb.gram[static_cast<int64_t>(i0 + r) * n2 + j0 + tx] = up;      // G[i][j], i <= j
+    if (!dsub) jb.gram[static_cast<int64_t>(j0 + r) * n2 + i0 + tx] = blk[tx][r];  // G[j][i]
+  }
+  if (diag && sub == 0 && threadIdx.x < kTB) {
+    float v = 0.f;
+    for (int sl = 0; sl < p.n_slices; ++sl) v += base[sl * slice_stride + kTB * kTB + threadIdx.x];
+    jb.colsum[ti * kTB + threadIdx.x] = v;
   }
 }
 
@@ -632,8 +719,9 @@ template <int DH>
 hipError_t launch_gram_dh(bool bf16, bool derope, const FitGramParams& p, dim3 grid,
                           hipStream_t stream) {
   if (bf16) {
-    if (derope) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true>), grid, dim3(256), 0, stream, p);
-    else hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, false>), grid, dim3(256), 0, stream, p);
+    if (!derope) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, false, true>), grid, dim3(256), 0, stream, p);
+    else if (p.g % 2 == 0) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true, true>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true, false>), grid, dim3(256), 0, stream, p);
   } else {
     if (derope) hipLaunchKernelGGL((fit_gram_f32_kernel<DH, true>), grid, dim3(256), 0, stream, p);
     else hipLaunchKernelGGL((fit_gram_f32_kernel<DH, false>), grid, dim3(256), 0, stream, p);
@@ -659,10 +747,7 @@ hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;
-  const int64_t n2 = 2 * static_cast<int64_t>(p.w);
-  const int64_t per_job = n2 * n2 + n2;
-  int64_t bx = (per_job + 255) / 256;
-  if (bx > 1024) bx = 1024;
+  const int64_t bx = fit_upper_tiles(p.w) * 16;  // 32 x 32 sub-blocks of every upper tile
   hipLaunchKernelGGL(fit_gram_reduce_kernel, dim3(static_cast<unsigned>(bx), p.n_jobs), dim3(256),
                      0, stream, p);
   return hipGetLastError();
