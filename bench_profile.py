@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 PHASES = {"encode_bf16_kernel": "encode", "reuse_decode": "reuse_decode",
           "patch_kv": "patch_kv", "patch_align": "aligner", "EncodeKV": "encode",
           "EncodeH": "encode", "ReuseDecode": "reuse_decode", "PatchKV": "patch_kv",
-          "PatchAlign": "aligner"}
+          "PatchAlign": "aligner", "fit_gram": "fit_gram", "fit_solve": "fit_solve"}
 
 
 def phase_of(name: str):
