@@ -220,12 +220,17 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
   load_x(nchunks > 1 ? 1 : 0, x1);
   __builtin_amdgcn_s_waitcnt(kWait8);
   lds_barrier();
+  const int last = nchunks - 1;
   auto step = [&](int c, uint4 (&xcur)[8], uint4 (&xfar)[8]) {
     const int buf = c & 1;
     // weights of chunk c + 1 and inputs of chunk c + 2 (past the end: in-bounds re-loads that are
-    // never used, so every chunk issues the same loads)
-    stage_weights(c + 1 < nchunks ? c + 1 : c, buf ^ 1);
-    load_x(c + 2 < nchunks ? c + 2 : c, xfar);
+    // never used, so every step issues the same loads and the compiler's counter waits can leave
+    // the far inputs in flight)
+    stage_weights(c + 1 < last ? c + 1 : last, buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(c + 2 < last ? c + 2 : last, xfar);
+    __builtin_amdgcn_sched_barrier(0);
+    if (c < nchunks) {
     // B operands, one (first half, second half) pair of k-steps at a time: deRoPE in fp32 and one
     // bf16 rounding (keys), or the loaded values themselves, then the MFMAs of both steps.
     const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
@@ -278,15 +283,20 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
         }
       }
     }
+    }
     // chunk c + 1's weights and inputs have landed once only chunk c + 2's 8 input loads are
-    // pending; the barrier makes that true for every wave and retires this chunk's LDS reads
+    // pending; the barrier makes that true for every wave and retires this chunk's LDS reads.  The
+    // scheduling fences keep each step's loads on their side of the count.
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(kWait8);
     lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
   };
+  // chunks run in threes; steps past the last chunk only keep the load pattern uniform
   for (int c = 0; c < nchunks; c += 3) {
     step(c, x0, x2);
-    if (c + 1 < nchunks) step(c + 1, x1, x0);
-    if (c + 2 < nchunks) step(c + 2, x2, x1);
+    step(c + 1, x1, x0);
+    step(c + 2, x2, x1);
   }
   wait_vmem();
   }

@@ -495,14 +495,18 @@ constexpr int kSolveThreads = 1024;
 // Pair k of round `round` of the cyclic ("round-robin") ordering of n indices: the n/2 pairs of a
 // round are disjoint and the n - 1 rounds visit every pair once.
 __device__ inline void jacobi_pair(int round, int k, int n, int& lo, int& hi) {
+  // round < m and k < n / 2 <= m, so both sums lie in [0, 2m): one conditional subtraction
+  // replaces the modulo
   const int m = n - 1;
   int a, b;
   if (k == 0) {
     a = m;
     b = round;
   } else {
-    a = (round + k) % m;
-    b = (round - k + m) % m;
+    a = round + k;
+    a = a >= m ? a - m : a;
+    b = round - k + m;
+    b = b >= m ? b - m : b;
   }
   lo = a < b ? a : b;
   hi = a < b ? b : a;
@@ -592,7 +596,10 @@ __global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolve
     trace = t;
   }
   __syncthreads();
-  const double floor_abs = 1e-18 * trace;
+  // Rotations below these thresholds change the eigenvectors far below fp32 precision; lower
+  // thresholds would keep rotating on roundoff (off-diagonal entries of about eps * lambda_max)
+  // and never report convergence.
+  const double floor_abs = 1e-15 * trace;
 
   // parallel cyclic Jacobi: every round applies n/2 disjoint rotations at once
   for (int sweep = 0; sweep < p.max_sweeps; ++sweep) {
@@ -602,7 +609,7 @@ __global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolve
         jacobi_pair(round, k, n, a, b);
         const double app = mj[a * n + a], aqq = mj[b * n + b], apq = mj[a * n + b];
         double cr = 1.0, sr = 0.0;
-        if (fabs(apq) > floor_abs && fabs(apq) > 1e-15 * sqrt(fabs(app * aqq))) {
+        if (fabs(apq) > floor_abs && fabs(apq) > 1e-12 * sqrt(fabs(app * aqq))) {
           // zero the (a, b) entry of J^T M J with J = [[c, s], [-s, c]] on (a, b)
           const double th = (aqq - app) / (2.0 * apq);
           const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(th * th + 1.0));
