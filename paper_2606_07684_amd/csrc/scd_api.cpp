@@ -743,12 +743,12 @@ namespace {
 
 constexpr int kFitMaxSweeps = 40;
 
-// Slices of the row axis for a Gram launch of n_jobs jobs: at most 1024 workgroups (two rounds of
-// two per CU) when the tiles allow, at least 512 rows per slice, slice lengths a multiple of the
-// kernels' k-step.
-int64_t fit_slices(int n_jobs, int w, int64_t n_rows, int64_t* slice_rows) {
-  const int64_t units = static_cast<int64_t>(n_jobs) * scd::fit_upper_tiles(w);
-  int64_t ns = 1024 / units;
+// Slices of the row axis for a Gram launch of n_jobs jobs: about two rounds of workgroups (the
+// whole-Gram kernel fits one workgroup per CU, the tile kernels two) when the tiles allow, at
+// least 512 rows per slice, slice lengths a multiple of the kernels' k-step.
+int64_t fit_slices(int n_jobs, int w, bool bf16, int64_t n_rows, int64_t* slice_rows) {
+  const int64_t units = scd::fit_units_per_slice(bf16, w, n_jobs);
+  int64_t ns = (scd::fit_full_gram(bf16, w) ? 512 : 1024) / units;
   const int64_t max_ns = (n_rows + 511) / 512;
   if (ns > max_ns) ns = max_ns;
   if (ns < 1) ns = 1;
@@ -772,7 +772,7 @@ size_t fit_gram_ws(const scd_model_t* m, int64_t n_rows) {
   for (int done = 0; done < R; done += scd::kMaxJobs) {
     const int jobs = R - done < scd::kMaxJobs ? R - done : scd::kMaxJobs;
     int64_t sr;
-    const int64_t ns = fit_slices(jobs, m->basis_width, n_rows, &sr);
+    const int64_t ns = fit_slices(jobs, m->basis_width, m->dtype == SCD_BF16, n_rows, &sr);
     const size_t b = static_cast<size_t>(jobs) * ns * scd::fit_upper_tiles(m->basis_width) *
                      (scd::kFitTile * scd::kFitTile + scd::kFitTile) * sizeof(float);
     if (b > best) best = b;
@@ -848,7 +848,8 @@ scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
     p.g = g;
     p.head_dim = model->head_dim;
     p.derope = branch == 0 ? 1 : 0;
-    p.n_slices = static_cast<int32_t>(fit_slices(p.n_jobs, w, n_rows, &p.slice_rows));
+    p.n_slices = static_cast<int32_t>(
+        fit_slices(p.n_jobs, w, model->dtype == SCD_BF16, n_rows, &p.slice_rows));
     p.n_seqs = batch->n_seqs;
     p.cu_seqlens = batch->cu_seqlens;
     p.pos0 = batch->pos0;

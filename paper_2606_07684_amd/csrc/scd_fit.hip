@@ -105,21 +105,28 @@ __device__ inline BlockSrc block_src(const FitGramJob& j, int w, int jc, int eb)
 // double-buffered, which leaves one barrier per step, and that barrier waits for LDS only.
 // PAIR: both rows of a thread's pair belong to one token (g even), so they share RoPE factors.
 // ---------------------------------------------------------------------------------------------
-template <int DH, bool DEROPE, bool PAIR>
-__global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramParams p) {
+//
+// FULL (2w = 256 only): one workgroup owns the whole Gram of its (job, slice), so every row is read
+// once.  Its two column blocks are the producer's (A) and the consumer's (B) columns; each wave
+// computes one 128 x 128 tile (AA, AB, BB, and the mirror BA, which keeps the code uniform and is
+// not stored), so a 64-row step is 64 MFMAs per wave against 32 KB of rows: about HBM speed.  The
+// partial tiles keep the tile kernel's layout (AA, AB, BB), so the slice reduction is shared.
+template <int DH, bool DEROPE, bool PAIR, bool FULL>
+__device__ __forceinline__ void fit_gram_bf16_body(const FitGramParams& p) {
   constexpr int BK = kFitRowStep, S = BK + 8, HALF = DH / 2, NR = PAIR ? 1 : 2;
+  constexpr int NA = FULL ? 4 : 2;  // accumulator blocks per wave and dimension
   __shared__ __attribute__((aligned(16))) uint16_t xt[2][2][kTB * S];  // [stage][block]
 
   const int nt = 2 * p.w / kTB, n_upper = nt * (nt + 1) / 2;
   // the tiles of one (job, slice) read the same rows: consecutive units on one XCD, so the second
   // read of a column block hits that XCD's L2
   int unit = xcd_remap(blockIdx.x, gridDim.x);
-  const int tile = unit % n_upper;
-  unit /= n_upper;
+  const int tile = FULL ? 0 : unit % n_upper;
+  if (!FULL) unit /= n_upper;
   const int slice = unit % p.n_slices;
   const int job = unit / p.n_slices;
-  int ti, tj;
-  tile_of(tile, nt, ti, tj);
+  int ti = 0, tj = 1;
+  if (!FULL) tile_of(tile, nt, ti, tj);
   const bool diag = ti == tj;
   const int nblk = diag ? 1 : 2;
   const FitGramJob& jb = p.jobs[job];
@@ -140,14 +147,15 @@ __global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramPara
 
   uint4 la[2][2][2], lb[2][2][2];  // [block][row of the pair][first half / partner]
   float4 rc[NR][4];                // RoPE (cos, sin) of the next step's rows, pairs ri .. ri+7
-  float csum[16];
+  constexpr int NCS = FULL ? 32 : 16;  // column sums kept: one or both blocks
+  float csum[NCS];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) csum[i] = 0.f;
-  f32x16 acc[2][2];
+  for (int i = 0; i < NCS; ++i) csum[i] = 0.f;
+  f32x16 acc[NA][NA];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NA; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NA; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
@@ -212,7 +220,8 @@ __global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramPara
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const uint32_t v = pack_bf16x2(f[0][q][j], f[1][q][j]);  // rows 2rp (low), 2rp+1 (high)
-          if (b == 0 && diag) csum[8 * q + j] += bf16_lo(v) + bf16_hi(v);
+          if (FULL) csum[16 * b + 8 * q + j] += bf16_lo(v) + bf16_hi(v);
+          else if (b == 0 && diag) csum[8 * q + j] += bf16_lo(v) + bf16_hi(v);
           const int col = c + q * HALF + j;
           dst[col * (S / 2) + ((((rp >> 2) ^ (col >> 3)) & 7) << 2) + (rp & 3)] = v;
         }
@@ -227,20 +236,41 @@ __global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramPara
   auto frag = [&](const uint16_t* base, int col, int kg) {
     return *reinterpret_cast<const bf16x8*>(base + col * S + (((kg ^ (col >> 3)) & 7) << 3));
   };
+  // FULL: waves 0..3 multiply (A block, B block) = (0,0), (0,1), (1,1), (1,0): tiles AA, AB, BB
+  // and the mirror BA, which is not stored
+  const int fa_blk = (wave == 2 || wave == 3) ? 1 : 0;
+  const int fb_blk = (wave == 1 || wave == 2) ? 1 : 0;
   auto products = [&](int sb) {
+    if constexpr (FULL) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 fa[2], fb[2];
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        bf16x8 fa[4], fb[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[i] = frag(xt[sb][0], wy * 64 + i * 32 + (lane & 31), 2 * ks + h);
-        fb[i] = frag(xt[sb][jblk], wx * 64 + i * 32 + (lane & 31), 2 * ks + h);
+        for (int i = 0; i < 4; ++i) {
+          fa[i] = frag(xt[sb][fa_blk], i * 32 + (lane & 31), 2 * ks + h);
+          fb[i] = frag(xt[sb][fb_blk], i * 32 + (lane & 31), 2 * ks + h);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
+    } else {
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        bf16x8 fa[2], fb[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        for (int i = 0; i < 2; ++i) {
+          fa[i] = frag(xt[sb][0], wy * 64 + i * 32 + (lane & 31), 2 * ks + h);
+          fb[i] = frag(xt[sb][jblk], wx * 64 + i * 32 + (lane & 31), 2 * ks + h);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
     }
   };
 
@@ -277,17 +307,55 @@ __global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramPara
 
   float* out = p.partial + ((static_cast<int64_t>(job) * p.n_slices + slice) * n_upper + tile) *
                                static_cast<int64_t>(kTileFloats);
+  if constexpr (FULL) {
+    // waves 0, 1, 2 hold tiles AA, AB, BB (tile indices 0, 1, 2); wave 3's BA is the mirror of AB
+    if (wave < 3) {
+      float* to = out + wave * static_cast<int64_t>(kTileFloats);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = wy * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const int n = wx * 64 + j * 32 + (lane & 31);
-        out[m * kTB + n] = acc[i][j][r];
-      }
-  if (diag) {
+          for (int r = 0; r < 16; ++r) {
+            const int m = i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            const int n = j * 32 + (lane & 31);
+            to[m * kTB + n] = acc[i][j][r];
+          }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = wy * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          const int n = wx * 64 + j * 32 + (lane & 31);
+          out[m * kTB + n] = acc[i][j][r];
+        }
+  }
+  if (FULL) {
+    // both blocks' column sums: block 0 is tile AA's, block 1 tile BB's
+#pragma unroll
+    for (int i = 0; i < 32; ++i)
+#pragma unroll
+      for (int o = 8; o <= 32; o <<= 1) csum[i] += __shfl_xor(csum[i], o, 64);
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(&xt[0][0][0]);  // [wave][cp][32]
+    if (lane < 8) {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) red[(wave * 8 + cp) * 32 + i] = csum[i];
+    }
+    __syncthreads();
+    {
+      const int pc = tid >> 5, i = tid & 31;  // 8 chunk pairs x 32 sums
+      const float v = red[(0 * 8 + pc) * 32 + i] + red[(1 * 8 + pc) * 32 + i] +
+                      red[(2 * 8 + pc) * 32 + i] + red[(3 * 8 + pc) * 32 + i];
+      const int b = i >> 4, e = i & 15;
+      const int cc = pair_col<DH, 8>(pc) + (e >> 3) * HALF + (e & 7);
+      out[(b == 0 ? 0 : 2) * static_cast<int64_t>(kTileFloats) + kTB * kTB + cc] = v;
+    }
+  } else if (diag) {
     // a chunk pair's rows are spread over the lanes tid % 8 == cp of every wave: reduce in the
     // wave, then over the four waves through LDS (the tiles are no longer read)
 #pragma unroll
@@ -309,6 +377,16 @@ __global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramPara
       out[kTB * kTB + cc] = v;
     }
   }
+}
+
+template <int DH, bool DEROPE, bool PAIR>
+__global__ __launch_bounds__(256, 2) void fit_gram_bf16_kernel(const FitGramParams p) {
+  fit_gram_bf16_body<DH, DEROPE, PAIR, false>(p);
+}
+
+template <int DH, bool DEROPE, bool PAIR>
+__global__ __launch_bounds__(256, 1) void fit_gram_full_bf16_kernel(const FitGramParams p) {
+  fit_gram_bf16_body<DH, DEROPE, PAIR, true>(p);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -725,7 +803,11 @@ __global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolve
 template <int DH>
 hipError_t launch_gram_dh(bool bf16, bool derope, const FitGramParams& p, dim3 grid,
                           hipStream_t stream) {
-  if (bf16) {
+  if (bf16 && fit_full_gram(true, p.w)) {
+    if (!derope) hipLaunchKernelGGL((fit_gram_full_bf16_kernel<DH, false, true>), grid, dim3(256), 0, stream, p);
+    else if (p.g % 2 == 0) hipLaunchKernelGGL((fit_gram_full_bf16_kernel<DH, true, true>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((fit_gram_full_bf16_kernel<DH, true, false>), grid, dim3(256), 0, stream, p);
+  } else if (bf16) {
     if (!derope) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, false, true>), grid, dim3(256), 0, stream, p);
     else if (p.g % 2 == 0) hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true, true>), grid, dim3(256), 0, stream, p);
     else hipLaunchKernelGGL((fit_gram_bf16_kernel<DH, true, false>), grid, dim3(256), 0, stream, p);
@@ -743,8 +825,15 @@ int64_t fit_upper_tiles(int w) {
   return nt * (nt + 1) / 2;
 }
 
+bool fit_full_gram(bool bf16, int w) { return bf16 && 2 * w == 2 * kTB; }
+
+int64_t fit_units_per_slice(bool bf16, int w, int n_jobs) {
+  return static_cast<int64_t>(n_jobs) * (fit_full_gram(bf16, w) ? 1 : fit_upper_tiles(w));
+}
+
 hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream) {
-  const int64_t units = static_cast<int64_t>(p.n_jobs) * fit_upper_tiles(p.w) * p.n_slices;
+  const int64_t units = static_cast<int64_t>(p.n_jobs) * fit_units_per_slice(bf16, p.w, 1) *
+                        p.n_slices;
   const dim3 grid(static_cast<unsigned>(units));
   hipError_t e;
   switch (p.head_dim) {

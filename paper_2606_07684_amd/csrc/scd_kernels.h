@@ -148,6 +148,10 @@ static_assert(sizeof(FitSolveParams) <= 4096, "kernel argument block");
 constexpr int kFitMaxSolveWidth = 256;
 
 int64_t fit_upper_tiles(int w);  // upper 128 x 128 tiles of the 2w x 2w Gram
+// bf16 with 2w = 256: one workgroup per (job, slice) computes the whole Gram
+bool fit_full_gram(bool bf16, int w);
+// workgroups of a Gram launch per row slice
+int64_t fit_units_per_slice(bool bf16, int w, int n_jobs);
 hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream);
 hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream);
 

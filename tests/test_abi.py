@@ -376,10 +376,11 @@ def test_fit_workspace_bytes_cover_both_calls(lib):
     # Gram partials: jobs x slices x upper tiles x (128^2 + 128) floats, slices = 1024 // units
     # capped by one per 512 rows; solve: 3 (2w)^2 doubles
     # per job.  One Reuse-only model, w = 128 (one 256 x 256 Gram = 3 upper tiles).
+    # bf16 with w = 128 takes the whole-Gram kernel: one workgroup per (layer, slice), 512 // jobs
     m = _model(is_patch=[0, 0, 0])
     for T in (1, 100, 511, 512, 5000, 200000):
-        units = 3 * 3
-        ns = max(1, min(1024 // units, -(-T // 512)))
+        units = 3
+        ns = max(1, min(512 // units, -(-T // 512)))
         sr = -(-T // ns)
         sr = -(-sr // 64) * 64
         ns = -(-T // sr)
