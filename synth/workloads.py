@@ -171,7 +171,15 @@ FIT_F32 = Workload("fit_f32", 2, 128, 2, 64, (200, 61), (16, 16), (), 1e4, "f32"
 FIT_DH32 = Workload("fit_dh32_bf16", 2, 128, 4, 32, (333,), (16, 32), (0,), 1e4, "bf16")
 FIT_POS0_KEYS = Workload("fit_single_tokens_bf16", 2, 128, 2, 64, (1,) * 700, (32, 32), (), 1e4,
                          "bf16", ranks_v=(16, 16))
-FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KEYS)
+# Basis widths other than 128 take the bf16 Gram's tile kernel: w = D = 256 (2w = 512: ten upper
+# tiles, three of them diagonal) with a packed batch, and the head-shared w = d_h = 64 (2w = 128: one
+# tile spanning both models' columns).
+FIT_W256_BF16 = Workload("fit_w256_bf16", 2, 256, 2, 128, (333, 190), (64, 64), (), 5e5, "bf16",
+                         pos0=(3, 0), ranks_v=(32, 32))
+FIT_W64_BF16 = Workload("fit_w64_bf16", 2, 128, 4, 64, (150, 211), (16, 16), (0,), 1e4, "bf16",
+                        basis_width=64, ranks_v=(32, 32))
+FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KEYS, FIT_W256_BF16,
+                 FIT_W64_BF16)
 # Calibration at the Llama-3-8B shape with the head-shared basis: 8192 tokens x 8 heads = 65,536
 # rows of 128 channels per layer (the paper calibrates on 100-500 prefixes of ~600 tokens).
 FIT_LLAMA3_8B = LLAMA3_8B_HEAD_SHARED.replace(name="fit_llama3_8b_head_shared_bf16")
