@@ -111,6 +111,35 @@ def per_phase_bytes(rows, scale: float):
     return dict(out)
 
 
+N_XCD, N_SIMD = 8, 256 * 4
+
+
+def mfma_table(folder: str):
+    """Per (kernel, grid): median duration, MFMA flops from SQ_INSTS_VALU_MFMA_MOPS_BF16 (512 flops
+    per op), MFMA-busy cycles per SIMD over the kernel's cycles (GRBM_GUI_ACTIVE is summed over the
+    XCDs), and the clock those cycles imply."""
+    rows = list(csv.DictReader(open(one_csv(folder, "counter_collection.csv"))))
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    durs = collections.defaultdict(list)
+    for r in rows:
+        if phase_of(r["Kernel_Name"]) is None:
+            continue
+        key = (r["Kernel_Name"], int(r["Grid_Size"]))
+        vals[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        durs[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    out = []
+    for key, cs in vals.items():
+        med = {c: statistics.median(v) for c, v in cs.items()}
+        dur_us = statistics.median(durs[key])
+        cycles = med.get("GRBM_GUI_ACTIVE", 0.0) / N_XCD
+        busy = med.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / N_SIMD
+        out.append({"kernel": short(key[0]), "phase": phase_of(key[0]), "grid": key[1],
+                    "us": dur_us, "gflop": med.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512 / 1e9,
+                    "busy": busy / cycles if cycles else 0.0,
+                    "ghz": cycles / (dur_us * 1e3) if dur_us else 0.0})
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--workload", default="llama3_8b_bf16")
@@ -122,6 +151,9 @@ def main():
     ap.add_argument("--write")
     ap.add_argument("--pmc-cmd", default="")
     ap.add_argument("--probe-gib", type=float, default=1.0)
+    ap.add_argument("--mfma", help="rocprofv3 --pmc folder with SQ_VALU_MFMA_BUSY_CYCLES, "
+                    "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
+    ap.add_argument("--mfma-cmd", default="")
     args = ap.parse_args()
 
     from synth import workloads as W
@@ -187,6 +219,9 @@ def main():
         open(path, "w").write("\n".join(lines) + "\n")
         print("wrote", path)
 
+    if args.mfma:
+        write_mfma(args, wl, alg, digest)
+
     if args.fetch and args.write:
         true_bytes = int(args.probe_gib * (1 << 30))
         frows, wrows = counters(args.fetch, "FETCH_SIZE"), counters(args.write, "WRITE_SIZE")
@@ -220,6 +255,33 @@ def main():
         open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.md"), "w").write(
             "\n".join(lines) + "\n")
         print("wrote", jpath)
+
+
+def write_mfma(args, wl, alg, digest):
+    rows = mfma_table(args.mfma)
+    lines = [f"# MFMA counters per kernel, {wl.name}", "",
+             f"Command: `{args.mfma_cmd}`", "",
+             f"Source digest of csrc/: `{digest}`. Medians over the run's launches.",
+             "- `SQ_INSTS_VALU_MFMA_MOPS_BF16` counts MFMA work in units of 512 flops: the flop "
+             "column checks the algorithmic count.",
+             "- MFMA busy = `SQ_VALU_MFMA_BUSY_CYCLES` per SIMD (1024 SIMDs) over the kernel's "
+             "cycles (`GRBM_GUI_ACTIVE` over 8 XCDs).",
+             "- The clock is those cycles over the kernel's duration; the 2.5 PFLOP/s bf16 peak "
+             "assumes 2.4 GHz.", "",
+             "| kernel | step | grid | us | MFMA GFLOP | MFMA busy | clock GHz | flops / peak at 2.4 GHz | flops / peak at that clock |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        pk = 2500.0e12 * r["us"] * 1e-6
+        frac = r["gflop"] * 1e9 / pk if pk else 0.0
+        frac_clk = frac * 2.4 / r["ghz"] if r["ghz"] else 0.0
+        lines.append(f"| `{r['kernel']}` | {r['phase']} | {r['grid']} | {r['us']:.1f} | "
+                     f"{r['gflop']:.1f} | {r['busy']:.3f} | {r['ghz']:.2f} | {frac:.3f} | "
+                     f"{frac_clk:.3f} |")
+    if "patch_kv" in alg:
+        lines += ["", f"Algorithmic Patch flops per call: {alg['patch_kv'][1] / 1e9:.1f} GFLOP."]
+    path = os.path.join(ROOT, "profiles", f"mfma_{wl.name}.md")
+    open(path, "w").write("\n".join(lines) + "\n")
+    print("wrote", path)
 
 
 if __name__ == "__main__":
