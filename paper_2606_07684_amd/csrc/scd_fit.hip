@@ -77,6 +77,13 @@ __device__ inline float4 gload_f4(const float2* p) {
   return make_float4(v.x, v.y, v.z, v.w);
 }
 
+// Column sums of a staged dword (two bf16 values of one column): acc + lo + hi in one dot product.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ inline float add_bf16_pair(uint32_t v, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, v),
+                                         __builtin_bit_cast(bf16x2_t, 0x3f803f80u), acc, false);
+}
+
 struct BlockSrc {
   const char* base;  // producer or consumer cache
   int col;           // column inside the w-wide row
@@ -190,6 +197,31 @@ __device__ __forceinline__ void fit_gram_bf16_body(const FitGramParams& p) {
   // de-rotate (keys), round, and write one k-step's rows into LDS stage sb; accumulate the diagonal
   // tile's column sums
   auto stage = [&](const uint4 (&ld)[2][2][2], int64_t k0, int sb) {
+    if constexpr (!DEROPE) {
+      // values: the staged dword of column j is the j-th bf16 of row 2rp (low half) and of row
+      // 2rp + 1 (high half): one byte permute per dword, no conversions
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        if (b >= nblk) break;
+        uint32_t* dst = reinterpret_cast<uint32_t*>(xt[sb][b]);
+        const bool live0 = k0 + 2 * rp < r1, live1 = k0 + 2 * rp + 1 < r1;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint4 a0 = live0 ? ld[b][0][q] : zero4, a1 = live1 ? ld[b][1][q] : zero4;
+          const uint32_t w0[4] = {a0.x, a0.y, a0.z, a0.w}, w1[4] = {a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t v = __builtin_amdgcn_perm(w1[j >> 1], w0[j >> 1],
+                                                     (j & 1) ? 0x07060302u : 0x05040100u);
+            if (FULL) csum[16 * b + 8 * q + j] = add_bf16_pair(v, csum[16 * b + 8 * q + j]);
+            else if (b == 0 && diag) csum[8 * q + j] = add_bf16_pair(v, csum[8 * q + j]);
+            const int col = c + q * HALF + j;
+            dst[col * (S / 2) + ((((rp >> 2) ^ (col >> 3)) & 7) << 2) + (rp & 3)] = v;
+          }
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       if (b >= nblk) break;
@@ -220,8 +252,8 @@ __device__ __forceinline__ void fit_gram_bf16_body(const FitGramParams& p) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const uint32_t v = pack_bf16x2(f[0][q][j], f[1][q][j]);  // rows 2rp (low), 2rp+1 (high)
-          if (FULL) csum[16 * b + 8 * q + j] += bf16_lo(v) + bf16_hi(v);
-          else if (b == 0 && diag) csum[8 * q + j] += bf16_lo(v) + bf16_hi(v);
+          if (FULL) csum[16 * b + 8 * q + j] = add_bf16_pair(v, csum[16 * b + 8 * q + j]);
+          else if (b == 0 && diag) csum[8 * q + j] = add_bf16_pair(v, csum[8 * q + j]);
           const int col = c + q * HALF + j;
           dst[col * (S / 2) + ((((rp >> 2) ^ (col >> 3)) & 7) << 2) + (rp & 3)] = v;
         }
