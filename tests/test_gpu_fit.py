@@ -247,3 +247,30 @@ def test_fit_solve_contains_non_finite_input():
     torch.cuda.synchronize()
     assert torch.isnan(w_dec[bad].float()).any()
     assert torch.equal(w_dec[good], ref[good])
+
+
+@pytest.mark.parametrize("wl", [W.FIT_SMALL_BF16, W.FIT_F32], ids=lambda w: w.name)
+def test_fit_without_centring_and_without_ridge(wl):
+    # The paper's formulas exactly: no offsets (center = 0 writes none) and lambda = 0 (the
+    # decoder is the consumer half of V_r, the encoder a least-squares fit; A^T A is non-singular
+    # here because every row carries noise).
+    dev = torch.device("cuda")
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    R, a_in, b_in, _ = _setup(wl, "v", dev)
+    w_enc, w_dec, mu_enc, mu_dec, _, _ = scd.fit_reuse(model, batch, None, scd.FIT_VALUES, a_in,
+                                                       b_in, 0.0, center=False)
+    torch.cuda.synchronize()
+    assert all(m is None for m in mu_enc) and all(m is None for m in mu_dec)
+    # Without the ridge term the encoder solves the normal equations of A itself: the fp32
+    # rounding of the accumulated Gram (about sqrt(N) u relative) reaches the result amplified by
+    # cond(A^T A).  The bar is the codec's tolerance or that first-order bound, whichever is larger.
+    errs, bound = {}, U.TOL[wl.dtype]
+    for l in R:
+        e_o, d_o, ma_o, mb_o = _oracle_fit(wl, "v", a_in, b_in, l, 0.0, center=False)
+        assert ma_o is None and mb_o is None
+        errs[("w_enc", l)] = U.max_abs_rel(U.f64(w_enc[l]), e_o)
+        errs[("w_dec", l)] = U.max_abs_rel(U.f64(w_dec[l]), d_o)
+        A = U.f64(a_in[l]).reshape(-1, wl.w)
+        bound = max(bound, np.linalg.cond(A.T @ A) * np.sqrt(A.shape[0]) * 2.0 ** -24)
+    print(f"[fit no centring, lambda 0] tolerance {bound:.3g}", flush=True)
+    U.assert_within(errs, bound, f"fit no centring, lambda 0, {wl.name}")
