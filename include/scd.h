@@ -246,9 +246,11 @@ scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch
  *    (rounded once).  Needs basis_width <= 256 and 16 <= rank <= basis_width, rank % 16 == 0,
  *    lambda >= 0.  lambda = 0 with a singular A^T A (fewer independent rows than w) leaves NaN in
  *    the layer's outputs.
- * `workspace` (device, 16-byte aligned, caller-owned, contents undefined on entry and exit) must
- * hold scd_fit_workspace_bytes(model, n_tokens) bytes; one buffer serves both calls.  Layers run
- * 64 per launch; the calls never synchronise.  Patch layers are not touched. */
+ * `workspace` (device, 16-byte aligned, caller-owned, contents undefined on entry and exit, not
+ * overlapping any argument) must hold scd_fit_workspace_bytes(model, n_tokens) bytes; one buffer
+ * serves both calls.  Each layer's outputs need buffers of their own (a buffer that repeats across
+ * layers returns SCD_ERR_SHAPE).  Layers run 64 per launch; the calls never synchronise.  Patch
+ * layers are not touched. */
 size_t scd_fit_workspace_bytes(const scd_model_t* model, int64_t n_tokens);
 scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
                           const void* rope_table, int64_t max_position, int32_t branch,

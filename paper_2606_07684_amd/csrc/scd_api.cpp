@@ -787,6 +787,17 @@ size_t fit_solve_ws(const scd_model_t* m) {
   return jobs * 3 * n * n * sizeof(double);
 }
 
+// Per-layer output buffers of the fit must be distinct: the layers of a launch are written
+// concurrently.
+scd_status_t distinct_outputs(const std::vector<int>& layers, const void* const* arr,
+                              const char* name) {
+  for (size_t i = 0; i < layers.size(); ++i)
+    for (size_t j = 0; j < i; ++j)
+      if (arr[layers[i]] == arr[layers[j]])
+        return fail(SCD_ERR_SHAPE, "%s[%d] repeats layer %d's buffer", name, layers[i], layers[j]);
+  return SCD_OK;
+}
+
 scd_status_t check_fit_model(const scd_model_t* model, int32_t branch) {
   SCD_TRY(check_model(model));
   if (branch != 0 && branch != 1)
@@ -829,6 +840,8 @@ scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
     SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(colsum), l, "colsum"));
   }
   if (layers.empty()) return ok();
+  SCD_TRY(distinct_outputs(layers, reinterpret_cast<const void* const*>(gram), "gram"));
+  SCD_TRY(distinct_outputs(layers, reinterpret_cast<const void* const*>(colsum), "colsum"));
   if (branch == 0) SCD_TRY(check_rope(rope_table, max_position));
   if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
   if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
@@ -892,6 +905,12 @@ scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_r
     }
   }
   if (layers.empty()) return ok();
+  SCD_TRY(distinct_outputs(layers, w_enc, "w_enc"));
+  SCD_TRY(distinct_outputs(layers, w_dec, "w_dec"));
+  if (center) {
+    SCD_TRY(distinct_outputs(layers, mu_enc, "mu_enc"));
+    SCD_TRY(distinct_outputs(layers, mu_dec, "mu_dec"));
+  }
   if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
   if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
   const size_t need = fit_solve_ws(model);

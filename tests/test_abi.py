@@ -303,15 +303,21 @@ def test_payload_views_and_streamed_decode_validation(lib):
     assert streamed(batch=_batch(n_tokens=0), src=None, dst=None)[0] == OK
 
 
+def _distinct_ptrs(L, k):
+    """Per-layer fake addresses, distinct across layers and arguments (never dereferenced)."""
+    arr = (ctypes.c_void_p * L)(*[FAKE + (16 * k + l + 1) * 4096 for l in range(L)])
+    return ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), arr
+
+
 def _fit_gram(lib, model, batch, branch=0, rope=FAKE, maxp=100, ws=FAKE, ws_bytes=1 << 40,
               **over):
     L = model.n_layers
     keep, args = [], {}
-    for name in ("a_in", "b_in", "gram", "colsum"):
+    for k, name in enumerate(("a_in", "b_in", "gram", "colsum")):
         if name in over:
             args[name] = over[name]
         else:
-            p, a = _ptrs(L)
+            p, a = _distinct_ptrs(L, k)
             keep.append(a)
             args[name] = p
     st = lib.scd_fit_gram(ctypes.byref(model._c), ctypes.byref(batch._c), rope, maxp, branch,
@@ -324,11 +330,11 @@ def _fit_solve(lib, model, branch=0, n_rows=100, lam=0.1, center=1, ws=FAKE, ws_
                **over):
     L = model.n_layers
     keep, args = [], {}
-    for name in ("gram", "colsum", "w_enc", "w_dec", "mu_enc", "mu_dec"):
+    for k, name in enumerate(("gram", "colsum", "w_enc", "w_dec", "mu_enc", "mu_dec")):
         if name in over:
             args[name] = over[name]
         else:
-            p, a = _ptrs(L)
+            p, a = _distinct_ptrs(L, k)
             keep.append(a)
             args[name] = p
     st = lib.scd_fit_solve(ctypes.byref(model._c), branch, n_rows, lam, center, args["gram"],
@@ -367,6 +373,12 @@ def test_fit_validation(lib):
     pm, keepm = _ptrs(3, skip=(0,))
     st, msg = _fit_solve(lib, m, mu_dec=pm)
     assert st == NULL and "mu_dec[0]" in msg
+    # one buffer for two layers' outputs: the layers of a launch write concurrently
+    same = (ctypes.c_void_p * 3)(FAKE, FAKE + 4096, FAKE)
+    st, msg = _fit_gram(lib, m, b, gram=ctypes.cast(same, ctypes.POINTER(ctypes.c_void_p)))
+    assert st == SHAPE and "gram[2]" in msg
+    st, msg = _fit_solve(lib, m, w_dec=ctypes.cast(same, ctypes.POINTER(ctypes.c_void_p)))
+    assert st == SHAPE and "w_dec[2]" in msg
     solve_need = 2 * 3 * 256 * 256 * 8  # two Reuse layers, w = 128
     st, msg = _fit_solve(lib, m, ws_bytes=solve_need - 8)
     assert st == SHAPE and "workspace" in msg
