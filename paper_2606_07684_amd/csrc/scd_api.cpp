@@ -662,7 +662,10 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
                 model->d_model);
   const int rh_max = model->d_model < 256 ? model->d_model : 256;
   bool any = false;
-  bool fast = model->dtype == SCD_BF16 && hidden % 128 == 0 && model->d_model % 128 == 0;
+  // The second product (K = hidden) takes the bf16 GEMM body whenever the widths allow; the first
+  // (K = r_H) needs r_H % 64 == 0 there, unless the decode body takes it (below).
+  const bool fast2 = model->dtype == SCD_BF16 && hidden % 128 == 0 && model->d_model % 128 == 0;
+  bool fast1 = fast2;
   std::vector<const void*> acts;
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
@@ -683,17 +686,19 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
           return fail(SCD_ERR_SHAPE, "act[%d] repeats an earlier Patch layer's buffer", l);
       acts.push_back(act[l]);
     }
-    if (model->rank_h[l] % 64 != 0) fast = false;
+    if (model->rank_h[l] % 64 != 0) fast1 = false;
   }
   if (!any || batch->n_tokens == 0) return ok();
 
   const int64_t T = batch->n_tokens;
   const int d = model->d_model;
   scd::GemmParams base = base_params(model, batch, T, 1, nullptr, 0);
-  const int bm = fast ? scd::kPatchBM : scd::kGenericBM, bn = fast ? scd::kPatchBN : scd::kGenericBN;
   // act = SiLU(z_h w1^T + b1) for every Patch layer, then h_hat = act w2^T + b2
   std::vector<scd::GemmJob> first_jobs;
-  JobPacker first(base, bm, bn), second(base, bm, bn);
+  JobPacker first(base, fast1 ? scd::kPatchBM : scd::kGenericBM,
+                  fast1 ? scd::kPatchBN : scd::kGenericBN);
+  JobPacker second(base, fast2 ? scd::kPatchBM : scd::kGenericBM,
+                   fast2 ? scd::kPatchBN : scd::kGenericBN);
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
     const scd::GemmJob j1{z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
@@ -723,7 +728,7 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
   }
   for (JobPacker* jp : {&first, &second}) {
     if (jp == &first && decode_first) continue;
-    if (!fast) {
+    if (!(jp == &first ? fast1 : fast2)) {
       SCD_TRY(run(scd::Op::kPatchAlign, jp->build(), model->dtype, stream));
       continue;
     }
