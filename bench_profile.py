@@ -133,10 +133,13 @@ def mfma_table(folder: str):
         dur_us = statistics.median(durs[key])
         cycles = med.get("GRBM_GUI_ACTIVE", 0.0) / N_XCD
         busy = med.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / N_SIMD
+        wave = med.get("SQ_WAVE_CYCLES", 0.0)
         out.append({"kernel": short(key[0]), "phase": phase_of(key[0]), "grid": key[1],
                     "us": dur_us, "gflop": med.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512 / 1e9,
                     "busy": busy / cycles if cycles else 0.0,
-                    "ghz": cycles / (dur_us * 1e3) if dur_us else 0.0})
+                    "ghz": cycles / (dur_us * 1e3) if dur_us else 0.0,
+                    "wait": med.get("SQ_WAIT_ANY", 0.0) / wave if wave else 0.0,
+                    "valu": med.get("SQ_ACTIVE_INST_VALU", 0.0) / wave if wave else 0.0})
     return out
 
 
@@ -267,16 +270,18 @@ def write_mfma(args, wl, alg, digest):
              "- MFMA busy = `SQ_VALU_MFMA_BUSY_CYCLES` per SIMD (1024 SIMDs) over the kernel's "
              "cycles (`GRBM_GUI_ACTIVE` over 8 XCDs).",
              "- The clock is those cycles over the kernel's duration; the 2.5 PFLOP/s bf16 peak "
-             "assumes 2.4 GHz.", "",
-             "| kernel | step | grid | us | MFMA GFLOP | MFMA busy | clock GHz | flops / peak at 2.4 GHz | flops / peak at that clock |",
-             "|---|---|---|---|---|---|---|---|---|"]
+             "assumes 2.4 GHz.",
+             "- Waiting and VALU issue are `SQ_WAIT_ANY` and `SQ_ACTIVE_INST_VALU` over "
+             "`SQ_WAVE_CYCLES` (fractions of the waves' lifetimes).", "",
+             "| kernel | step | grid | us | MFMA GFLOP | MFMA busy | clock GHz | flops / peak at 2.4 GHz | flops / peak at that clock | waves waiting | waves issuing VALU |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
         pk = 2500.0e12 * r["us"] * 1e-6
         frac = r["gflop"] * 1e9 / pk if pk else 0.0
         frac_clk = frac * 2.4 / r["ghz"] if r["ghz"] else 0.0
         lines.append(f"| `{r['kernel']}` | {r['phase']} | {r['grid']} | {r['us']:.1f} | "
                      f"{r['gflop']:.1f} | {r['busy']:.3f} | {r['ghz']:.2f} | {frac:.3f} | "
-                     f"{frac_clk:.3f} |")
+                     f"{frac_clk:.3f} | {r['wait']:.2f} | {r['valu']:.2f} |")
     if "patch_kv" in alg:
         lines += ["", f"Algorithmic Patch flops per call: {alg['patch_kv'][1] / 1e9:.1f} GFLOP."]
     path = os.path.join(ROOT, "profiles", f"mfma_{wl.name}.md")
