@@ -9,13 +9,14 @@
 // one lane and the epilogue needs no LDS: bias, rotation and bf16 rounding happen in registers and
 // each lane stores two 16-byte vectors per block.
 //
-// K advances 32 at a time through a ring of kStages LDS stages ((256 + 256) x 32 bf16 = 32 KiB
-// each; the 16-byte chunks of each row are XOR-swizzled so MFMA operand reads are conflict-free).
-// Both operand tiles travel global -> LDS directly (global_load_lds_dwordx4): the copy of stage
-// k + kStages - 1 is issued between the MFMAs of stage k, so kStages - 1 stages are in flight and
-// the copy latency (over a microsecond under full load) hides behind that many steps of MFMAs.
-// Each step is two 16-wide k-slices; the workgroup barrier sits between them, so the operand reads
-// of the next stage's first slice also run under MFMAs.
+// K advances 64 at a time through a ring of two LDS stages ((256 + 256) x 64 bf16 = 64 KiB each;
+// the 16-byte chunks of each row are XOR-swizzled so MFMA operand reads are conflict-free).  Both
+// operand tiles travel global -> LDS directly (global_load_lds_dwordx4), each lane-octet of a copy
+// instruction reading one row's whole 128-byte line.  Each step is four 16-wide k-slices; the
+// workgroup barrier sits before the last one, so the operand reads of the next stage's first
+// slice run under MFMAs, and the copy of stage k + 2 is issued right after that barrier, into the
+// buffer stage k has just released: the copy latency (about a microsecond under full load) hides
+// behind four slices of MFMAs.
 #include "scd_device.h"
 
 namespace scd {
@@ -26,8 +27,8 @@ using namespace dev;
 constexpr int kBM = kPatchBM;   // tokens per tile
 constexpr int kBN = kPatchBN;   // channels per tile
 #ifndef SCD_PATCH_BK
-#define SCD_PATCH_BK 32
-#define SCD_PATCH_STAGES 4
+#define SCD_PATCH_BK 64
+#define SCD_PATCH_STAGES 2
 #endif
 constexpr int kBK = SCD_PATCH_BK;     // contraction step (one pipeline stage)
 constexpr int kLDK = kBK;             // LDS row (bf16 elements): kBK / 8 16-byte chunks, swizzled
@@ -40,17 +41,16 @@ constexpr int kDmaPerStage = 2 * (kBN * kBK / 8) / kThreads;  // DMA instruction
 static_assert(kSlices == 2 || kSlices == 4, "stage = 2 or 4 k-slices");
 static_assert(kStages * kStage * 2 <= 160 * 1024, "LDS");
 
-// Chunk c of LDS row r (64 bytes) sits at chunk position c ^ swz(r).  Among the swizzles tried on
-// this kernel's exact read sequence (both operand regions, 4 waves, both k-slices of a stage),
-// (r ^ (r >> 2)) & 3 is the fastest, together with ((r >> 2) ^ (r >> 1)) & 3 and 16-byte row
-// padding; no swizzle is 4x slower and (r >> 1) & 3 1.2x slower (SQ_LDS_BANK_CONFLICT agrees).
-// The fragment reads plus the copies' LDS writes come close to the LDS bandwidth, so this matters.
-#ifndef SCD_PATCH_SWZ8
-#define SCD_PATCH_SWZ8 0
-#endif
+// Chunk c of LDS row r sits at chunk position c ^ swz(r).  A swizzle must depend on r % 32 only
+// (fragment reads take it from the lane's row within a 32-row block).  For 128-byte rows, r & 7 is
+// conflict-free for the MFMA operand reads.  For 64-byte rows (32-wide stages), among the swizzles
+// tried on this kernel's exact read sequence, (r ^ (r >> 2)) & 3 is the fastest, together with
+// ((r >> 2) ^ (r >> 1)) & 3 and 16-byte row padding; no swizzle is 4x slower and (r >> 1) & 3 1.2x
+// slower (SQ_LDS_BANK_CONFLICT agrees).  The fragment reads plus the copies' LDS writes come close
+// to the LDS bandwidth, so this matters.
 __device__ __forceinline__ int swz(int r) {
   if constexpr (kChunks == 4) return (r ^ (r >> 2)) & 3;
-  return SCD_PATCH_SWZ8 == 0 ? r & 7 : (r ^ (r >> 3)) & 7;
+  return r & 7;
 }
 
 // s_waitcnt immediates: at most n vector-memory operations outstanding (optionally with every LDS
@@ -61,27 +61,28 @@ constexpr int vmcnt_imm(int n, bool lds_done = false) {
 constexpr int kLgkmDone = 0xF | (0x3 << 14) | (0x7 << 4);
 
 // Scheduling groups for one block of 16 MFMAs and 8 LDS reads that do not feed them: one read
-// after each of the first eight MFMAs.  interleave_reads_dma spreads the stage's LDS-DMA copies over
-// the first MFMAs of the block the same way.
-__device__ __forceinline__ void interleave_reads() {
+// after each of the first eight MFMAs.  interleave_reads_dma also spreads the stage's LDS-DMA
+// copies over the last eight MFMAs (the compiler cannot tell that the copies and the reads touch
+// different LDS buffers, so it keeps them in program order: reads first).
 #define SCD_MFMA_THEN_READ                          \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
   __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#define SCD_MFMA_THEN_DMA                            \
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
+  __builtin_amdgcn_sched_group_barrier(0x020, kDmaPerStage / 8, 0);
+__device__ __forceinline__ void interleave_reads() {
   SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
   SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-#undef SCD_MFMA_THEN_READ
   __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
 }
 __device__ __forceinline__ void interleave_reads_dma() {
-#define SCD_MFMA_READ_DMA                            \
-  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x020, kDmaPerStage / 8, 0);
-  SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
-  SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA SCD_MFMA_READ_DMA
-#undef SCD_MFMA_READ_DMA
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+  SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA
+  SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA
 }
+#undef SCD_MFMA_THEN_DMA
+#undef SCD_MFMA_THEN_READ
 
 // The product C = A B^T of one launch (both operands row-major with the contraction contiguous,
 // 256 x 256 tiles), with the epilogue the job flags select.  Two kernels run it: the Patch KV
@@ -105,9 +106,10 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const uint16_t* Hh = static_cast<const uint16_t*>(job.a);
   const int nk = K / kBK;
 
-  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x 4 chunks = 1024
-  // 16-byte slots = 4 wave-wide instructions per wave; lane i of instruction j of wave w fills slot
-  // (4j + w) * 64 + i (row slot / 4, position slot % 4) with the chunk that belongs there.  Weight
+  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x kChunks chunks of
+  // 16 bytes = kDmaIters wave-wide instructions per wave; lane i of instruction j of wave w fills
+  // slot (4j + w) * 64 + i (row slot / kChunks, position slot % kChunks) with the chunk that belongs
+  // there.  Weight
   // rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
   // accumulators that are never stored.
   constexpr int kDmaIters = kBN * kChunks / (4 * 64);
@@ -164,21 +166,20 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
         acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
-  // Prologue: stages 0 .. kStages - 2 in flight, wait for stage 0, read its first slice.  A stage
+  // Prologue: every buffer's stage in flight, wait for stage 0, read its first slice.  A stage
   // index past the end re-copies the last stage into a buffer that is never read for data (its
   // reads only feed the discarded look-ahead of the final step), so every step issues the same
   // number of copies and one vmcnt threshold holds throughout.
   auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
 #pragma unroll
-  for (int st = 0; st < kStages - 1; ++st) stage(clamp(st), st);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
+  for (int st = 0; st < kStages; ++st) stage(clamp(st), st);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 1), true));
   lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
   const uint16_t* hrow = smem + kBN * kLDK + (wt * 128 + lr) * kLDK;
   bf16x8 a0[4], b0[4], a1[4], b1[4];
   frags(wrow, hrow, 0, a0, b0);
   int rb = 0;                // buffer holding stage kc
-  int wbuf = kStages - 1;    // buffer stage kc + kStages - 1 goes to
   for (int kc = 0; kc < nk; ++kc) {
     const int nb = rb + 1 == kStages ? 0 : rb + 1;
     const uint16_t* wb = wrow + rb * kStage;
@@ -187,12 +188,10 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     // inside this block from covering the reads it issues itself.
     __builtin_amdgcn_s_waitcnt(kLgkmDone);
     __builtin_amdgcn_sched_barrier(0);
-    // Slice 0's MFMAs, with slice 1's reads and the next copy between them.  The copy overwrites
-    // the buffer stage kc - 1 used, whose last reads completed before the previous barrier.
+    // The first slices' MFMAs, each with the next slice's reads between them.
     mma(a0, b0);
     frags(wb, hb, 1, a1, b1);
-    stage(clamp(kc + kStages - 1), wbuf);
-    interleave_reads_dma();
+    interleave_reads();
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kSlices == 4) {
       mma(a1, b1);
@@ -210,13 +209,16 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // The last slice's MFMAs, with the next stage's slice-0 reads between them.
+    // The last slice's MFMAs, with the next stage's slice-0 reads between them and the copy of
+    // stage kc + kStages into the buffer stage kc has just released (every wave's reads of it
+    // completed before the barrier).  Issued here, a copy has the whole of the next kStages - 1
+    // steps' MFMAs before the barrier that needs it.
     mma(a1, b1);
     frags(wrow + nb * kStage, hrow + nb * kStage, 0, a0, b0);
-    interleave_reads();
+    stage(clamp(kc + kStages), rb);
+    interleave_reads_dma();
     __builtin_amdgcn_sched_barrier(0);
     rb = nb;
-    wbuf = wbuf + 1 == kStages ? 0 : wbuf + 1;
   }
   // drain the look-ahead copies before the workgroup's LDS is released
   wait_vmem();
