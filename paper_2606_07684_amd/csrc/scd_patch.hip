@@ -9,14 +9,16 @@
 // one lane and the epilogue needs no LDS: bias, rotation and bf16 rounding happen in registers and
 // each lane stores two 16-byte vectors per block.
 //
-// K advances 64 at a time through a ring of two LDS stages ((256 + 256) x 64 bf16 = 64 KiB each;
-// the 16-byte chunks of each row are XOR-swizzled so MFMA operand reads are conflict-free).  Both
-// operand tiles travel global -> LDS directly (global_load_lds_dwordx4), each lane-octet of a copy
-// instruction reading one row's whole 128-byte line.  Each step is four 16-wide k-slices; the
-// workgroup barrier sits before the last one, so the operand reads of the next stage's first
-// slice run under MFMAs, and the copy of stage k + 2 is issued right after that barrier, into the
-// buffer stage k has just released: the copy latency (about a microsecond under full load) hides
-// behind four slices of MFMAs.
+// K advances 64 at a time.  An operand tile of one 64-wide step (256 rows x 64 bf16 = 32 KiB, its
+// 16-byte chunks XOR-swizzled so MFMA operand reads are conflict-free) fills one slot of a ring of
+// five, the whole 160 KiB of LDS.  Both operand tiles travel global -> LDS directly
+// (global_load_lds_dwordx4), eight lanes of a copy instruction reading one row's whole 128-byte
+// line.  Each step is four 16-wide k-slices; the workgroup barrier sits before the last one, so
+// the operand reads of the next step's first slice run under MFMAs, and right after it the two
+// slots the current step has released receive the weight tile of step k + 2 and the token tile of
+// step k + 3.  Token tiles, the operand that misses L2 more often, thus get two steps of MFMAs to
+// land and weight tiles one; five slots hold one and a half steps of copies in flight, against
+// one for a ring of two whole steps.
 #include "scd_device.h"
 
 namespace scd {
@@ -26,32 +28,22 @@ using namespace dev;
 
 constexpr int kBM = kPatchBM;   // tokens per tile
 constexpr int kBN = kPatchBN;   // channels per tile
-#ifndef SCD_PATCH_BK
-#define SCD_PATCH_BK 64
-#define SCD_PATCH_STAGES 2
-#endif
-constexpr int kBK = SCD_PATCH_BK;     // contraction step (one pipeline stage)
-constexpr int kLDK = kBK;             // LDS row (bf16 elements): kBK / 8 16-byte chunks, swizzled
+constexpr int kBK = 64;                     // contraction step
+constexpr int kLDK = kBK;                   // LDS row (bf16 elements): 8 16-byte chunks, swizzled
 constexpr int kChunks = kBK / 8;
-constexpr int kSlices = kBK / 16;     // 16-wide MFMA k-slices per stage
-constexpr int kStage = (kBN + kBM) * kLDK;  // elements per pipeline stage
-constexpr int kStages = SCD_PATCH_STAGES;   // ring depth; kStages * kStage * 2 bytes of LDS
+constexpr int kSlot = kBN * kLDK;           // elements per ring slot (one operand tile of a step)
+constexpr int kRing = 5;                    // slots
 constexpr int kThreads = 256;
-constexpr int kDmaPerStage = 2 * (kBN * kBK / 8) / kThreads;  // DMA instructions per wave per stage
-static_assert(kSlices == 2 || kSlices == 4, "stage = 2 or 4 k-slices");
-static_assert(kStages * kStage * 2 <= 160 * 1024, "LDS");
+constexpr int kDmaIters = kBN * kChunks / kThreads;  // copy instructions per wave per operand tile
+constexpr int kDmaPerStage = 2 * kDmaIters;          // ... per step (both operands)
+static_assert(kBN == kBM, "square tiles: both operand tiles fill one slot");
+static_assert(kRing * kSlot * 2 <= 160 * 1024, "LDS");
 
 // Chunk c of LDS row r sits at chunk position c ^ swz(r).  A swizzle must depend on r % 32 only
-// (fragment reads take it from the lane's row within a 32-row block).  For 128-byte rows, r & 7 is
-// conflict-free for the MFMA operand reads.  For 64-byte rows (32-wide stages), among the swizzles
-// tried on this kernel's exact read sequence, (r ^ (r >> 2)) & 3 is the fastest, together with
-// ((r >> 2) ^ (r >> 1)) & 3 and 16-byte row padding; no swizzle is 4x slower and (r >> 1) & 3 1.2x
-// slower (SQ_LDS_BANK_CONFLICT agrees).  The fragment reads plus the copies' LDS writes come close
-// to the LDS bandwidth, so this matters.
-__device__ __forceinline__ int swz(int r) {
-  if constexpr (kChunks == 4) return (r ^ (r >> 2)) & 3;
-  return r & 7;
-}
+// (fragment reads take it from the lane's row within a 32-row block); for 128-byte rows, r & 7 is
+// conflict-free for the MFMA operand reads.  The fragment reads plus the copies' LDS writes come
+// close to the LDS bandwidth, so this matters.
+__device__ __forceinline__ int swz(int r) { return r & 7; }
 
 // s_waitcnt immediates: at most n vector-memory operations outstanding (optionally with every LDS
 // access completed), or every LDS access completed.
@@ -106,14 +98,11 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const uint16_t* Hh = static_cast<const uint16_t*>(job.a);
   const int nk = K / kBK;
 
-  // Stage kc -> LDS buffer b, asynchronously.  Each operand tile is 256 rows x kChunks chunks of
-  // 16 bytes = kDmaIters wave-wide instructions per wave; lane i of instruction j of wave w fills
-  // slot (4j + w) * 64 + i (row slot / kChunks, position slot % kChunks) with the chunk that belongs
-  // there.  Weight
-  // rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
+  // Operand tile of step kc -> ring slot, asynchronously.  A tile is 256 rows x 8 chunks of 16
+  // bytes = kDmaIters wave-wide instructions per wave; lane i of instruction j of wave w fills
+  // chunk position (4j + w) * 64 + i (row / 8, position % 8) with the chunk that belongs there.
+  // Weight rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
   // accumulators that are never stored.
-  constexpr int kDmaIters = kBN * kChunks / (4 * 64);
-  static_assert(kBN == kBM && 2 * kDmaIters == kDmaPerStage, "DMA slot cover");
   const uint16_t* wsrc[kDmaIters];
   const uint16_t* hsrc[kDmaIters];
 #pragma unroll
@@ -125,16 +114,13 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * c;
     hsrc[j] = Hh + t * K + 8 * c;
   }
-  auto stage = [&](int kc, int b) {
-    uint16_t* ws = smem + b * kStage;
-    uint16_t* hs = ws + kBN * kLDK;
+  auto copy_tile = [&](const uint16_t* const* src, int kc, int slot) {
+    uint16_t* dst = smem + slot * kSlot;
     const int kb = kc * kBK;
 #pragma unroll
-    for (int j = 0; j < kDmaIters; ++j) {
-      const int base = (4 * j + wave) * 64;
-      __builtin_amdgcn_global_load_lds(wsrc[j] + kb, (lds_void_t)(ws + 8 * base), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(hsrc[j] + kb, (lds_void_t)(hs + 8 * base), 16, 0, 0);
-    }
+    for (int j = 0; j < kDmaIters; ++j)
+      __builtin_amdgcn_global_load_lds(src[j] + kb, (lds_void_t)(dst + 8 * ((4 * j + wave) * 64)),
+                                       16, 0, 0);
   };
 
   f32x16 acc[4][4];
@@ -166,59 +152,65 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
         acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
-  // Prologue: every buffer's stage in flight, wait for stage 0, read its first slice.  A stage
-  // index past the end re-copies the last stage into a buffer that is never read for data (its
-  // reads only feed the discarded look-ahead of the final step), so every step issues the same
-  // number of copies and one vmcnt threshold holds throughout.
+  // Copies in issue order: token tile of step 0, weight tile of step 0, token tile of step 1, ...;
+  // the i-th goes to slot i mod 5.  Step kc reads slots 2kc and 2kc + 1 (mod 5), and after its
+  // barrier issues copies 2kc + 5 and 2kc + 6 into exactly those slots.  A step index past the end
+  // re-copies the last step into a slot that is never read for data (its reads only feed the
+  // discarded look-ahead of the final step), so every step issues the same number of copies and
+  // one vmcnt threshold holds throughout.
   auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
-#pragma unroll
-  for (int st = 0; st < kStages; ++st) stage(clamp(st), st);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 1), true));
+  copy_tile(hsrc, 0, 0);
+  copy_tile(wsrc, 0, 1);
+  copy_tile(hsrc, clamp(1), 2);
+  copy_tile(wsrc, clamp(1), 3);
+  copy_tile(hsrc, clamp(2), 4);
+  // step 0's two tiles have landed once at most the last three copies are pending
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * kDmaIters, true));
   lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
-  const uint16_t* hrow = smem + kBN * kLDK + (wt * 128 + lr) * kLDK;
+  const uint16_t* hrow = smem + (wt * 128 + lr) * kLDK;
   bf16x8 a0[4], b0[4], a1[4], b1[4];
-  frags(wrow, hrow, 0, a0, b0);
-  int rb = 0;                // buffer holding stage kc
+  int sh = 0, sw = 1;        // slots of step kc's token and weight tiles
+  frags(wrow + sw * kSlot, hrow + sh * kSlot, 0, a0, b0);
   for (int kc = 0; kc < nk; ++kc) {
-    const int nb = rb + 1 == kStages ? 0 : rb + 1;
-    const uint16_t* wb = wrow + rb * kStage;
-    const uint16_t* hb = hrow + rb * kStage;
+    const int next_h = sh + 2 >= kRing ? sh + 2 - kRing : sh + 2;
+    const int next_w = sw + 2 >= kRing ? sw + 2 - kRing : sw + 2;
+    const uint16_t* wb = wrow + sw * kSlot;
+    const uint16_t* hb = hrow + sh * kSlot;
     // Slice 0's operands were read between the previous MFMAs; retiring them here keeps the waits
     // inside this block from covering the reads it issues itself.
     __builtin_amdgcn_s_waitcnt(kLgkmDone);
     __builtin_amdgcn_sched_barrier(0);
-    // The first slices' MFMAs, each with the next slice's reads between them.
+    // The first three slices' MFMAs, each with the next slice's reads between them.
     mma(a0, b0);
     frags(wb, hb, 1, a1, b1);
     interleave_reads();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (kSlices == 4) {
-      mma(a1, b1);
-      frags(wb, hb, 2, a0, b0);
-      interleave_reads();
-      __builtin_amdgcn_sched_barrier(0);
-      mma(a0, b0);
-      frags(wb, hb, 3, a1, b1);
-      interleave_reads();
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // Stage kc + 1 has landed for this wave once at most kStages - 2 stages' copies are pending, and
-    // its reads of stage kc are complete once no LDS access is pending; the barrier makes both
-    // true for every wave.  (A plain s_barrier: a fenced one would wait for every copy in flight.)
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerStage * (kStages - 2), true));
+    mma(a1, b1);
+    frags(wb, hb, 2, a0, b0);
+    interleave_reads();
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a0, b0);
+    frags(wb, hb, 3, a1, b1);
+    interleave_reads();
+    __builtin_amdgcn_sched_barrier(0);
+    // Step kc + 1's tiles have landed for this wave once at most the last copy (the token tile
+    // of step kc + 2) is pending, and its reads of step kc are complete once no LDS access is
+    // pending; the barrier makes both true for every wave.  (A plain s_barrier: a fenced one would
+    // wait for every copy in flight.)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaIters, true));
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // The last slice's MFMAs, with the next stage's slice-0 reads between them and the copy of
-    // stage kc + kStages into the buffer stage kc has just released (every wave's reads of it
-    // completed before the barrier).  Issued here, a copy has the whole of the next kStages - 1
-    // steps' MFMAs before the barrier that needs it.
+    // The last slice's MFMAs, with the next step's slice-0 reads and then the two copies into the
+    // slots step kc has released (every wave's reads of them completed before the barrier).
     mma(a1, b1);
-    frags(wrow + nb * kStage, hrow + nb * kStage, 0, a0, b0);
-    stage(clamp(kc + kStages), rb);
+    frags(wrow + next_w * kSlot, hrow + next_h * kSlot, 0, a0, b0);
+    copy_tile(wsrc, clamp(kc + 2), sh);
+    copy_tile(hsrc, clamp(kc + 3), sw);
     interleave_reads_dma();
     __builtin_amdgcn_sched_barrier(0);
-    rb = nb;
+    sh = next_h;
+    sw = next_w;
   }
   // drain the look-ahead copies before the workgroup's LDS is released
   wait_vmem();
@@ -315,13 +307,14 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   }
 }
 
+constexpr int kSmemElems = kRing * kSlot;
 __global__ __launch_bounds__(kThreads, 1) void patch_kv_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kSmemElems];
   patch_gemm_bf16(p, smem);
 }
 
 __global__ __launch_bounds__(kThreads, 1) void patch_align_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[kStages * kStage];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kSmemElems];
   patch_gemm_bf16(p, smem);
 }
 
