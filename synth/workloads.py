@@ -184,8 +184,21 @@ FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KE
 # rows of 128 channels per layer (the paper calibrates on 100-500 prefixes of ~600 tokens).
 FIT_LLAMA3_8B = LLAMA3_8B_HEAD_SHARED.replace(name="fit_llama3_8b_head_shared_bf16")
 
+# Patch contractions of 5 and 7 steps of 64 (d_model 320 and 448), whose bf16 kernel cycles its
+# operand tiles through a ring of five LDS slots: the ring wraps exactly at the last step, then
+# part-way.  (These widths are not multiples of 128, so the aligner and the H encode take the
+# generic kernel here.)
+SMALL_RING5 = Workload("small_ring5_bf16", 2, 320, 2, 64, (300, 213), (64, 64), (0,), 1e4, "bf16",
+                       with_bias=True)
+SMALL_RING7 = Workload("small_ring7_bf16", 2, 448, 2, 64, (257,), (32, 64), (1,), 1e4, "bf16")
+# The aligner on the same kernel with a second product of 10 steps (hidden width 640) and a first
+# of 3 (rank 192).
+SMALL_ALIGN_RING = Workload("small_align_ring_bf16", 2, 256, 2, 64, (300,), (64, 192), (0, 1),
+                            1e4, "bf16", aligner_hidden=640)
+
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
-                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS)
+                  SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS, SMALL_RING5,
+                  SMALL_RING7, SMALL_ALIGN_RING)
 
 
 # --------------------------------------------------------------------------------------------
