@@ -12,7 +12,7 @@
 // K advances 64 at a time.  An operand tile of one 64-wide step (256 rows x 64 bf16 = 32 KiB, its
 // 16-byte chunks XOR-swizzled so MFMA operand reads are conflict-free) fills one slot of a ring of
 // five, the whole 160 KiB of LDS.  Both operand tiles travel global -> LDS directly
-// (global_load_lds_dwordx4), eight lanes of a copy instruction reading one row's whole 128-byte
+// (buffer_load_dwordx4 ... lds), eight lanes of a copy instruction reading one row's whole 128-byte
 // line.  Each step is four 16-wide k-slices; the workgroup barrier sits before the last one, so
 // the operand reads of the next step's first slice run under MFMAs, and right after it the two
 // slots the current step has released receive the weight tile of step k + 2 and the token tile of
@@ -38,6 +38,8 @@ constexpr int kDmaIters = kBN * kChunks / kThreads;  // copy instructions per wa
 constexpr int kDmaPerStage = 2 * kDmaIters;          // ... per step (both operands)
 static_assert(kBN == kBM, "square tiles: both operand tiles fill one slot");
 static_assert(kRing * kSlot * 2 <= 160 * 1024, "LDS");
+// Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data format, no swizzle.
+constexpr int kBufferFlags = 0x00020000;
 
 // Chunk c of LDS row r sits at chunk position c ^ swz(r).  A swizzle must depend on r % 32 only
 // (fragment reads take it from the lane's row within a 32-row block); for 128-byte rows, r & 7 is
@@ -98,29 +100,38 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const uint16_t* Hh = static_cast<const uint16_t*>(job.a);
   const int nk = K / kBK;
 
-  // Operand tile of step kc -> ring slot, asynchronously.  A tile is 256 rows x 8 chunks of 16
-  // bytes = kDmaIters wave-wide instructions per wave; lane i of instruction j of wave w fills
-  // chunk position (4j + w) * 64 + i (row / 8, position % 8) with the chunk that belongs there.
-  // Weight rows past N repeat row N - 1 and token rows past M repeat row M - 1: they only feed
-  // accumulators that are never stored.
-  const uint16_t* wsrc[kDmaIters];
-  const uint16_t* hsrc[kDmaIters];
+  // Operand tile of step kc -> ring slot, asynchronously (buffer_load_dwordx4 ... lds).  A tile is
+  // 256 rows x 8 chunks of 16 bytes = kDmaIters wave-wide instructions per wave; lane i of
+  // instruction j of wave w fills chunk position (4j + w) * 64 + i (row / 8, position % 8) with the
+  // chunk that belongs there.  Weight rows past N repeat row N - 1 and token rows past M repeat row
+  // M - 1 (they only feed accumulators that are never stored), so no copy leaves the matrices.  The
+  // buffer resources start at the tile's first weight row and first token row; a lane's byte
+  // offsets then fit in 32 bits and the step's offset is one scalar.
+  auto records = [](int64_t bytes) { return static_cast<int>(bytes < 0x7fffffff ? bytes : 0x7fffffff); };
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(W + static_cast<int64_t>(n0) * K), 0,
+      records(static_cast<int64_t>(N - n0) * K * 2), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t hres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(Hh + t0 * K), 0, records((M - t0) * K * 2), kBufferFlags);
+  uint32_t woff[kDmaIters], hoff[kDmaIters];
 #pragma unroll
   for (int j = 0; j < kDmaIters; ++j) {
     const int slot = (4 * j + wave) * 64 + lane;
     const int rho = slot / kChunks, c = (slot % kChunks) ^ swz(slot / kChunks);
-    const int n = n0 + row_of_lds(rho) < N ? n0 + row_of_lds(rho) : N - 1;
-    const int64_t t = t0 + rho < M ? t0 + rho : M - 1;
-    wsrc[j] = W + static_cast<int64_t>(n) * K + 8 * c;
-    hsrc[j] = Hh + t * K + 8 * c;
+    const int n = row_of_lds(rho) < N - n0 ? row_of_lds(rho) : N - n0 - 1;
+    const int t = t0 + rho < M ? rho : static_cast<int>(M - 1 - t0);
+    woff[j] = static_cast<uint32_t>((n * K + 8 * c) * 2);
+    hoff[j] = static_cast<uint32_t>((t * K + 8 * c) * 2);
   }
-  auto copy_tile = [&](const uint16_t* const* src, int kc, int slot) {
+  constexpr bool kTokens = true, kWeights = false;
+  auto copy_tile = [&](bool tokens, int kc, int slot) {
     uint16_t* dst = smem + slot * kSlot;
-    const int kb = kc * kBK;
+    const int kb = kc * kBK * 2;
 #pragma unroll
     for (int j = 0; j < kDmaIters; ++j)
-      __builtin_amdgcn_global_load_lds(src[j] + kb, (lds_void_t)(dst + 8 * ((4 * j + wave) * 64)),
-                                       16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(tokens ? hres : wres,
+                                               (lds_void_t)(dst + 8 * ((4 * j + wave) * 64)), 16,
+                                               tokens ? hoff[j] : woff[j], kb, 0, 0);
   };
 
   f32x16 acc[4][4];
@@ -159,11 +170,11 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   // discarded look-ahead of the final step), so every step issues the same number of copies and
   // one vmcnt threshold holds throughout.
   auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
-  copy_tile(hsrc, 0, 0);
-  copy_tile(wsrc, 0, 1);
-  copy_tile(hsrc, clamp(1), 2);
-  copy_tile(wsrc, clamp(1), 3);
-  copy_tile(hsrc, clamp(2), 4);
+  copy_tile(kTokens, 0, 0);
+  copy_tile(kWeights, 0, 1);
+  copy_tile(kTokens, clamp(1), 2);
+  copy_tile(kWeights, clamp(1), 3);
+  copy_tile(kTokens, clamp(2), 4);
   // step 0's two tiles have landed once at most the last three copies are pending
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * kDmaIters, true));
   lds_barrier();
@@ -205,8 +216,8 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     // slots step kc has released (every wave's reads of them completed before the barrier).
     mma(a1, b1);
     frags(wrow + next_w * kSlot, hrow + next_h * kSlot, 0, a0, b0);
-    copy_tile(wsrc, clamp(kc + 2), sh);
-    copy_tile(hsrc, clamp(kc + 3), sw);
+    copy_tile(kWeights, clamp(kc + 2), sh);
+    copy_tile(kTokens, clamp(kc + 3), sw);
     interleave_reads_dma();
     __builtin_amdgcn_sched_barrier(0);
     sh = next_h;
