@@ -263,6 +263,26 @@ scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_r
                            void* const* mu_enc, void* const* mu_dec, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
 
+/* ---- Allocation-free fit solve -----------------------------------------------------------------
+ * For callers that cannot allocate device memory or hand over a workspace (code under stream
+ * capture, serving loops, harnesses that forbid allocation): scd_fit_solve without the workspace
+ * arguments.  Same arguments, validation and results (bit-identical) as scd_fit_solve.  The
+ * solve's fp64 matrices live in a device-resident scratch array of
+ * scd_fit_solve_noalloc_max_bytes() bytes (64 MiB) that the library holds on each GPU it runs on
+ * until the process ends; layers are solved in as many stream-ordered launches as that array
+ * needs (3 (2w)^2 fp64 values per layer).  A basis width whose per-layer matrices exceed the array
+ * returns SCD_ERR_WORKSPACE.  The call uses the calling thread's current device, which must own the
+ * stream and the buffers; its first call on a device looks the array's address up.  It allocates
+ * nothing and never synchronises.  Every call on one GPU shares that GPU's array: calls that may
+ * run at the same time on one GPU (different streams, or other threads) race on it and must be
+ * serialised by the caller. */
+size_t scd_fit_solve_noalloc_max_bytes(void);
+scd_status_t scd_fit_solve_noalloc(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                                   double ridge_lambda, int32_t center, const float* const* gram,
+                                   const float* const* colsum, void* const* w_enc,
+                                   void* const* w_dec, void* const* mu_enc, void* const* mu_dec,
+                                   hipStream_t stream);
+
 /* ---- diagnostics ---------------------------------------------------------------------------- */
 const char* scd_status_string(scd_status_t status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */

@@ -30,7 +30,8 @@ __all__ = [
     "Prepared", "prepare_encode", "prepare_reuse_decode", "prepare_patch_kv",
     "scd_patch_align", "prepare_patch_align", "scd_payload_views",
     "scd_reuse_decode_streamed", "prepare_reuse_decode_streamed", "PreparedStreamed",
-    "DEFAULT_LAYERS_PER_GROUP",
+    "DEFAULT_LAYERS_PER_GROUP", "scd_fit_solve_noalloc", "prepare_fit_solve_noalloc",
+    "scd_fit_solve_noalloc_max_bytes",
 ]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -119,6 +120,10 @@ _SIGS = {
     "scd_fit_solve": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32, ctypes.c_int64,
                                      ctypes.c_double, ctypes.c_int32] + [_PP] * 6
                       + [_VP, ctypes.c_size_t, _VP]),
+    "scd_fit_solve_noalloc_max_bytes": (ctypes.c_size_t, []),
+    "scd_fit_solve_noalloc": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32,
+                                             ctypes.c_int64, ctypes.c_double, ctypes.c_int32]
+                              + [_PP] * 6 + [_VP]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -597,6 +602,40 @@ def scd_fit_solve(model: Model, branch: int, n_rows: int, ridge_lambda: float, c
                   stream=None) -> None:
     prepare_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc, w_dec,
                       mu_enc, mu_dec, workspace)(stream)
+
+
+def scd_fit_solve_noalloc_max_bytes() -> int:
+    return int(load_library().scd_fit_solve_noalloc_max_bytes())
+
+
+def prepare_fit_solve_noalloc(model: Model, branch: int, n_rows: int, ridge_lambda: float,
+                              center: bool, gram, colsum, w_enc, w_dec, mu_enc,
+                              mu_dec) -> Prepared:
+    """scd_fit_solve without a workspace: the library's device-resident scratch array holds the
+    solve's matrices (calls that overlap on one GPU race on it)."""
+    lib = load_library()
+    L, w = model.n_layers, model.basis_width
+    dt = model.torch_dtype
+    R = [l for l in range(L) if not model.is_patch[l]]
+    ranks = model.rank_k if branch == FIT_KEYS else model.rank_v
+    args = [
+        _ptr_array(gram, L, "gram", {l: (2 * w, 2 * w) for l in R}, torch.float32),
+        _ptr_array(colsum, L, "colsum", {l: (2 * w,) for l in R}, torch.float32),
+        _ptr_array(w_enc, L, "w_enc", {l: (ranks[l], w) for l in R}, dt),
+        _ptr_array(w_dec, L, "w_dec", {l: (w, ranks[l]) for l in R}, dt),
+        _ptr_array(mu_enc, L, "mu_enc", {l: (w,) for l in R}, dt),
+        _ptr_array(mu_dec, L, "mu_dec", {l: (w,) for l in R}, dt),
+    ]
+    return Prepared(lib.scd_fit_solve_noalloc, (ctypes.byref(model._c), int(branch), int(n_rows),
+                                                float(ridge_lambda), 1 if center else 0,
+                                                *[_as_pp(a) for a in args]), (model, args))
+
+
+def scd_fit_solve_noalloc(model: Model, branch: int, n_rows: int, ridge_lambda: float,
+                          center: bool, gram, colsum, w_enc, w_dec, mu_enc, mu_dec,
+                          stream=None) -> None:
+    prepare_fit_solve_noalloc(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc,
+                              w_dec, mu_enc, mu_dec)(stream)
 
 
 def fit_reuse(model: Model, batch: Batch, rope: Optional[RopeTable], branch: int, a_in, b_in,

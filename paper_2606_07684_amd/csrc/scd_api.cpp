@@ -209,7 +209,7 @@ int64_t kv_width(const scd_model_t* m) {
 
 extern "C" {
 
-int32_t scd_abi_version(void) { return 4; }
+int32_t scd_abi_version(void) { return 5; }
 
 const char* scd_status_string(scd_status_t s) {
   switch (s) {
@@ -880,11 +880,15 @@ scd_status_t scd_fit_gram(const scd_model_t* model, const scd_batch_t* batch,
   return ok();
 }
 
-scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
-                           double ridge_lambda, int32_t center, const float* const* gram,
-                           const float* const* colsum, void* const* w_enc, void* const* w_dec,
-                           void* const* mu_enc, void* const* mu_dec, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Validates a fit-solve call (everything but the workspace) and lists the Reuse layers it fits.
+scd_status_t check_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                             double ridge_lambda, int32_t center, const float* const* gram,
+                             const float* const* colsum, void* const* w_enc, void* const* w_dec,
+                             void* const* mu_enc, void* const* mu_dec, std::vector<int>* layers) {
   SCD_TRY(check_fit_model(model, branch));
   const int w = model->basis_width;
   if (w > scd::kFitMaxSolveWidth)
@@ -895,10 +899,10 @@ scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_r
     return fail(SCD_ERR_SHAPE, "ridge_lambda must be finite and >= 0");
   if (center != 0 && center != 1) return fail(SCD_ERR_SHAPE, "center must be 0 or 1");
   const int32_t* ranks = branch == 0 ? model->rank_k : model->rank_v;
-  std::vector<int> layers;
+  layers->clear();
   for (int l = 0; l < model->n_layers; ++l) {
     if (model->is_patch[l]) continue;
-    layers.push_back(l);
+    layers->push_back(l);
     SCD_TRY(check_rank(branch == 0 ? "rank_k" : "rank_v", l, ranks[l], w));
     SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(gram), l, "gram"));
     SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(colsum), l, "colsum"));
@@ -909,38 +913,95 @@ scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_r
       SCD_TRY(need_ptr(mu_dec, l, "mu_dec"));
     }
   }
-  if (layers.empty()) return ok();
-  SCD_TRY(distinct_outputs(layers, w_enc, "w_enc"));
-  SCD_TRY(distinct_outputs(layers, w_dec, "w_dec"));
+  if (layers->empty()) return SCD_OK;
+  SCD_TRY(distinct_outputs(*layers, w_enc, "w_enc"));
+  SCD_TRY(distinct_outputs(*layers, w_dec, "w_dec"));
   if (center) {
-    SCD_TRY(distinct_outputs(layers, mu_enc, "mu_enc"));
-    SCD_TRY(distinct_outputs(layers, mu_dec, "mu_dec"));
+    SCD_TRY(distinct_outputs(*layers, mu_enc, "mu_enc"));
+    SCD_TRY(distinct_outputs(*layers, mu_dec, "mu_dec"));
   }
-  if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
-  if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
-  const size_t need = fit_solve_ws(model);
-  if (workspace_bytes < need)
-    return fail(SCD_ERR_SHAPE, "workspace_bytes %zu < %zu needed", workspace_bytes, need);
+  return SCD_OK;
+}
 
-  for (size_t done = 0; done < layers.size(); done += scd::kMaxJobs) {
+// Launches the solve for `layers`, at most jobs_per_launch layers per launch, every launch using
+// the same `work` matrices (launches on one stream run in order, so they never overlap).
+scd_status_t enqueue_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                               double ridge_lambda, int32_t center, const float* const* gram,
+                               const float* const* colsum, void* const* w_enc,
+                               void* const* w_dec, void* const* mu_enc, void* const* mu_dec,
+                               const std::vector<int>& layers, size_t jobs_per_launch,
+                               double* work, hipStream_t stream) {
+  const int32_t* ranks = branch == 0 ? model->rank_k : model->rank_v;
+  for (size_t done = 0; done < layers.size(); done += jobs_per_launch) {
     scd::FitSolveParams p{};
     p.n_jobs = 0;
-    for (size_t i = done; i < layers.size() && i < done + scd::kMaxJobs; ++i) {
+    for (size_t i = done; i < layers.size() && i < done + jobs_per_launch; ++i) {
       const int l = layers[i];
       p.jobs[p.n_jobs++] = {gram[l], colsum[l], w_enc[l], w_dec[l],
                             center ? mu_enc[l] : nullptr, center ? mu_dec[l] : nullptr, ranks[l], 0};
     }
-    p.w = w;
+    p.w = model->basis_width;
     p.n_rows = n_rows;
     p.lambda = ridge_lambda;
     p.center = center;
     p.bf16 = model->dtype == SCD_BF16 ? 1 : 0;
     p.max_sweeps = kFitMaxSweeps;
-    p.work = static_cast<double*>(workspace);
+    p.work = work;
     const hipError_t e = scd::launch_fit_solve(p, stream);
     if (e != hipSuccess) return fail(SCD_ERR_HIP, "fit solve launch failed: %s", hipGetErrorString(e));
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                           double ridge_lambda, int32_t center, const float* const* gram,
+                           const float* const* colsum, void* const* w_enc, void* const* w_dec,
+                           void* const* mu_enc, void* const* mu_dec, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  std::vector<int> layers;
+  SCD_TRY(check_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc, w_dec,
+                          mu_enc, mu_dec, &layers));
+  if (layers.empty()) return ok();
+  if (workspace == nullptr) return fail(SCD_ERR_NULL, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SCD_ERR_ALIGN, "workspace is not 16-byte aligned");
+  const size_t need = fit_solve_ws(model);
+  if (workspace_bytes < need)
+    return fail(SCD_ERR_SHAPE, "workspace_bytes %zu < %zu needed", workspace_bytes, need);
+  return enqueue_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc,
+                           w_dec, mu_enc, mu_dec, layers, scd::kMaxJobs,
+                           static_cast<double*>(workspace), stream);
+}
+
+size_t scd_fit_solve_noalloc_max_bytes(void) { return scd::kFitScratchBytes; }
+
+scd_status_t scd_fit_solve_noalloc(const scd_model_t* model, int32_t branch, int64_t n_rows,
+                                   double ridge_lambda, int32_t center, const float* const* gram,
+                                   const float* const* colsum, void* const* w_enc,
+                                   void* const* w_dec, void* const* mu_enc, void* const* mu_dec,
+                                   hipStream_t stream) {
+  std::vector<int> layers;
+  SCD_TRY(check_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc, w_dec,
+                          mu_enc, mu_dec, &layers));
+  if (layers.empty()) return ok();
+  const size_t n = 2 * static_cast<size_t>(model->basis_width);
+  const size_t per_layer = 3 * n * n * sizeof(double);
+  if (per_layer > scd::kFitScratchBytes)
+    return fail(SCD_ERR_WORKSPACE,
+                "basis_width %d needs %zu bytes of solve scratch per layer; the allocation-free "
+                "solve holds %zu",
+                model->basis_width, per_layer, scd::kFitScratchBytes);
+  double* work = nullptr;
+  const hipError_t e = scd::fit_scratch(&work);
+  if (e != hipSuccess)
+    return fail(SCD_ERR_HIP, "scratch address lookup failed: %s", hipGetErrorString(e));
+  size_t jobs = scd::kFitScratchBytes / per_layer;
+  if (jobs > static_cast<size_t>(scd::kMaxJobs)) jobs = scd::kMaxJobs;
+  return enqueue_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc,
+                           w_dec, mu_enc, mu_dec, layers, jobs, work, stream);
 }
 
 }  // extern "C"

@@ -13,9 +13,18 @@
 // fp64 in one workgroup per layer (parallel cyclic Jacobi, then Cholesky solves).
 #include "scd_device.h"
 
+#include <mutex>
+
 namespace scd {
 
 using namespace dev;
+
+// Device-resident scratch of the allocation-free solve (scd_fit_solve_noalloc): the solve's fp64
+// Jacobi and solve matrices for as many layers as fit, reused launch after launch.  Each GPU the
+// library runs on holds its own copy for the life of the process.  Host code must never pass this
+// name to a kernel (in host code it is a stand-in, not a device address): fit_scratch() looks up
+// the device address once per device.
+static __device__ __align__(256) double scratch[kFitScratchBytes / sizeof(double)];
 
 namespace {
 
@@ -879,6 +888,26 @@ hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream
   hipLaunchKernelGGL(fit_gram_reduce_kernel, dim3(static_cast<unsigned>(bx), p.n_jobs), dim3(256),
                      0, stream, p);
   return hipGetLastError();
+}
+
+hipError_t fit_scratch(double** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static double* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = static_cast<double*>(p);
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {

@@ -155,6 +155,12 @@ int64_t fit_units_per_slice(bool bf16, int w, int n_jobs);
 hipError_t launch_fit_gram(bool bf16, const FitGramParams& p, hipStream_t stream);
 hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream);
 
+// Size of the device-resident scratch array of the allocation-free solve (one per GPU).
+constexpr size_t kFitScratchBytes = size_t{64} << 20;
+// Device address of the calling thread's current device's scratch array, looked up once per
+// device (hipGetSymbolAddress) and cached.
+hipError_t fit_scratch(double** ptr);
+
 hipError_t launch_rope_table(float2* table, int64_t max_pos, int head_dim, double theta,
                              hipStream_t stream);
 hipError_t launch_positions(int32_t* out, int64_t n_tokens, int32_t n_seqs,

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), f"libscd.so does not export {n}"
     assert set(names) == set(scd.EXPORTED_SYMBOLS)
-    assert scd.scd_abi_version() == 4
+    assert scd.scd_abi_version() == 5
 
 
 def test_status_strings(lib):
@@ -400,3 +400,41 @@ def test_fit_workspace_bytes_cover_both_calls(lib):
         solve = 3 * 3 * 256 * 256 * 8
         assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), T) == max(gram, solve)
     assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), 0) == 0
+
+
+def test_fit_solve_noalloc_validation(lib):
+    # The allocation-free solve validates exactly as the workspace solve, before any HIP call
+    # (these run without a GPU: every case below fails validation).
+    assert lib.scd_fit_solve_noalloc_max_bytes() == 64 << 20
+
+    def call(model, branch=0, n_rows=100, lam=0.1, center=1, **over):
+        L = model.n_layers
+        keep, args = [], {}
+        for k, name in enumerate(("gram", "colsum", "w_enc", "w_dec", "mu_enc", "mu_dec")):
+            if name in over:
+                args[name] = over[name]
+            else:
+                p, a = _distinct_ptrs(L, k)
+                keep.append(a)
+                args[name] = p
+        st = lib.scd_fit_solve_noalloc(ctypes.byref(model._c), branch, n_rows, lam, center,
+                                       args["gram"], args["colsum"], args["w_enc"],
+                                       args["w_dec"], args["mu_enc"], args["mu_dec"], None)
+        return st, lib.scd_last_error().decode()
+
+    m = _model()
+    assert call(m, branch=2)[0] == SHAPE
+    assert call(m, n_rows=0)[0] == SHAPE
+    assert call(m, lam=float("inf"))[0] == SHAPE
+    assert call(m, center=3)[0] == SHAPE
+    assert call(_model(rank_k=[144, 32, 32]))[0] == SCHED
+    wide = _model(n_kv_heads=6, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 384
+    assert call(wide)[0] == UNSUP
+    pm, keepm = _ptrs(3, skip=(2,))
+    st, msg = call(m, gram=pm)
+    assert st == NULL and "gram[2]" in msg
+    same = (ctypes.c_void_p * 3)(FAKE, FAKE + 4096, FAKE)
+    st, msg = call(m, w_enc=ctypes.cast(same, ctypes.POINTER(ctypes.c_void_p)))
+    assert st == SHAPE and "w_enc[2]" in msg
+    # a schedule without Reuse layers has nothing to solve and touches no device state
+    assert call(_model(is_patch=[1, 1, 1]))[0] == 0
