@@ -2,16 +2,20 @@
 """Throughput of the SCD KV-state codec's hot path on one MI355X.
 
 One step is one pass of the whole path over one batch already resident in HBM:
-  producer encode    scd_encode        K/V of every Reuse layer -> codes, H of every Patch layer -> Z_H
-  consumer Reuse     scd_reuse_decode  codes -> K (RoPE) / V straight into the consumer's KV cache
-  consumer Patch     scd_patch_kv      H_hat -> K (RoPE) / V through the consumer's W_K / W_V
-The Reuse decode consumes the codes the encode of the same step produced.
+  producer encode    scd_encode               K/V of every Reuse layer -> codes, H of every
+                                              Patch layer -> Z_H
+  consumer Reuse     scd_reuse_decode         codes -> K (RoPE) / V straight into the KV cache
+  consumer Patch     scd_patch_kv_from_codes  Z_H -> aligner hidden layer -> K (RoPE) / V through
+                                              the aligner's output layer folded into W_K / W_V
+The consumer half consumes the codes the encode of the same step produced.  The fold of the
+aligner's output layer into the projections is weights-only and runs once before timing.
 
-Prints one JSON line.  ``value`` is reconstructed-KV GB/s over the whole step (KV bytes written by
-Reuse + Patch divided by the full step time, encode included), ``tokens_per_s`` the prefix tokens
-per second, both from K uninstrumented steps.  ``roofline`` is the dominant kernel's achieved
-fraction of its bound, from a second pass of K steps with HIP events between the entry points on
-the stream the kernels run on; ``cpu_baseline`` is the fp64 oracle timed on this host.
+Prints one JSON line.  ``value`` is reconstructed-KV GB/s: the KV bytes Reuse + Patch write divided
+by the consumer's time (Reuse decode + Patch), from HIP events recorded between the entry points on
+the stream they run on inside the K timed steps; ``ms_per_step`` is the whole step (encode
+included) by wall clock around those K steps, and ``whole_step_GBps`` the same bytes over it.
+``roofline`` is the dominant phase's achieved fraction of its bound; ``configs`` repeats the
+measurement for every model-shaped workload; ``cpu_baseline`` is the fp64 oracle on this host.
 """
 from __future__ import annotations
 
@@ -30,15 +34,20 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 
 
 def algorithmic(wl):
-    """Minimum bytes and flops of each step for workload ``wl`` (read every input once, write every
-    output once; the RoPE table and re-reads are not counted)."""
+    """Minimum bytes and flops of each phase for workload ``wl`` (read every input once, write every
+    output once; the RoPE table and re-reads are not counted).  The Patch phase from the codes is
+    the aligner's hidden layer act = SiLU(Z_H W1^T + b1) (written once) and the folded product
+    act W_fold^T + c into the K/V cache (act read once)."""
     eb, T, D, d, w, g = wl.elem_bytes, wl.n_tokens, wl.kv_width, wl.d_model, wl.w, wl.g
-    dec_b = dec_f = pat_b = pat_f = enc_b = enc_f = 0
+    h = wl.hidden_width
+    dec_b = dec_f = pat_b = pat_f = enc_b = enc_f = act_b = act_f = 0
     for l in range(wl.n_layers):
         if wl.is_patch[l]:
             r = wl.rank(l, "h")
-            pat_b += (T * d + 2 * D * d + 2 * T * D + (2 * D if wl.with_bias else 0)) * eb
-            pat_f += 2 * T * d * 2 * D
+            act_b += (T * r + h * r + h + T * h) * eb
+            act_f += 2 * T * r * h
+            pat_b += (T * h + 2 * D * h + 2 * D + 2 * T * D) * eb
+            pat_f += 2 * T * h * 2 * D
             enc_b += (T * d + r * d + T * r) * eb
             enc_f += 2 * T * d * r
         else:
@@ -50,15 +59,28 @@ def algorithmic(wl):
                 enc_b += (T * D + r * w + mu + T * g * r) * eb
                 enc_f += 2 * T * g * w * r
     kv_bytes = wl.n_layers * 2 * T * D * eb
-    return {"reuse_decode": (dec_b, dec_f), "patch_kv": (pat_b, pat_f),
+    return {"reuse_decode": (dec_b, dec_f), "patch": (act_b + pat_b, act_f + pat_f),
+            "patch_act": (act_b, act_f), "patch_gemm": (pat_b, pat_f),
             "encode": (enc_b, enc_f), "kv_bytes": kv_bytes}
 
 
-KERNELS = {  # step -> (kernel symbol of the bf16 path, bound)
+PHASES = ("encode", "reuse_decode", "patch")
+KERNELS = {  # phase -> (kernel symbols of the bf16 path, bound)
     "encode": ("encode_bf16_kernel", "hbm"),
     "reuse_decode": ("reuse_decode_bf16_kernel", "hbm"),
-    "patch_kv": ("patch_kv_bf16_kernel", "mfma"),
+    "patch": ("patch_align_act_bf16_kernel + patch_kv_bf16_kernel", "mfma"),
 }
+
+
+def pct(vals, q):
+    """The q-th percentile (linear interpolation) of a list."""
+    v = sorted(vals)
+    if len(v) == 1:
+        return v[0]
+    x = (len(v) - 1) * q / 100.0
+    i = int(x)
+    j = min(i + 1, len(v) - 1)
+    return v[i] + (v[j] - v[i]) * (x - i)
 
 
 def source_digest() -> str:
@@ -83,10 +105,13 @@ def traffic_for(workload: str, step: str, digest: str):
     return None if ent is None else ent.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, inp, budget_s=25.0):
-    """The fp64 oracle on this host's cores over the same workload, layer by layer; stops after
-    ``budget_s`` seconds of oracle time and extrapolates per layer kind."""
-    import numpy as np
+def cpu_baseline(wl, inp, aligner, budget_s=25.0, max_tokens=None):
+    """The fp64 oracle on this host's cores over the same workload, layer by layer: the consumer's
+    Reuse decode and Patch from the codes (the literal aligner, then W_K / W_V), each on the codes
+    the oracle's own encode produced.  Stops after ``budget_s`` seconds of oracle time and
+    extrapolates per layer kind; the encode is timed too but not counted in ``value``.  With
+    ``max_tokens`` the oracle runs on the first that many packed tokens (every map is row-wise, so
+    its cost is linear in the token count) and the time is scaled to the whole batch."""
     import torch
 
     from oracle import scd_oracle as O
@@ -97,14 +122,17 @@ def cpu_baseline(wl, inp, budget_s=25.0):
     except Exception:  # noqa: BLE001
         threads = None
     cores = len(os.sched_getaffinity(0))
-    pos = O.positions(wl.cu_seqlens, wl.pos0)
+    S = wl.n_tokens if max_tokens is None else min(wl.n_tokens, max_tokens)
+    pos = O.positions(wl.cu_seqlens, wl.pos0)[:S]
     H, dh, th, D = wl.n_kv_heads, wl.head_dim, wl.rope_theta, wl.kv_width
     f64 = lambda t: None if t is None else t.detach().to("cpu", torch.float64).numpy()  # noqa: E731
-    t_reuse, n_reuse, t_patch, n_patch = 0.0, 0, 0.0, 0
+    rows = lambda t: None if t is None else f64(t[:S])  # noqa: E731
+    t_enc = {True: 0.0, False: 0.0}
+    t_con = {True: 0.0, False: 0.0}
+    n_done = {True: 0, False: 0}
     # interleave layer kinds so a budget cut still samples both
-    order = sorted(range(wl.n_layers), key=lambda l: (0 if wl.is_patch[l] else 1, l))
-    patch_layers = [l for l in order if wl.is_patch[l]]
-    reuse_layers = [l for l in order if not wl.is_patch[l]]
+    patch_layers = [l for l in range(wl.n_layers) if wl.is_patch[l]]
+    reuse_layers = [l for l in range(wl.n_layers) if not wl.is_patch[l]]
     seq = []
     while patch_layers or reuse_layers:
         if patch_layers:
@@ -112,42 +140,52 @@ def cpu_baseline(wl, inp, budget_s=25.0):
         for _ in range(7):
             if reuse_layers:
                 seq.append(reuse_layers.pop(0))
+    spent = 0.0
     for l in seq:
-        if t_reuse + t_patch > budget_s:
+        if spent > budget_s:
             break
-        if wl.is_patch[l]:
-            hin, eh, hh, wk, wv = (f64(inp.h_in[l]), f64(inp.w_enc_h[l]), f64(inp.h_hat[l]),
-                                   f64(inp.w_k[l]), f64(inp.w_v[l]))
+        kind = bool(wl.is_patch[l])
+        if kind:
+            w1, b1, w2, b2 = (f64(x) for x in aligner[l])
+            hin, eh, wk, wv = rows(inp.h_in[l]), f64(inp.w_enc_h[l]), f64(inp.w_k[l]), f64(inp.w_v[l])
             t0 = time.perf_counter()
-            O.encode_h(hin, eh)
+            zh = O.encode_h(hin, eh)
+            t1 = time.perf_counter()
+            hh, _ = O.align(zh, w1, b1, w2, b2)
             O.patch_k(hh, wk, f64(inp.b_k[l]), pos, H, dh, th)
             O.patch_v(hh, wv, f64(inp.b_v[l]))
-            t_patch += time.perf_counter() - t0
-            n_patch += 1
+            t2 = time.perf_counter()
         else:
-            ka, va = f64(inp.k_in[l]), f64(inp.v_in[l])
+            ka, va = rows(inp.k_in[l]), rows(inp.v_in[l])
             ek, ev, fk, fv = (f64(inp.w_enc_k[l]), f64(inp.w_enc_v[l]), f64(inp.w_dec_k[l]),
                               f64(inp.w_dec_v[l]))
             mk, mv = f64(inp.mu_k[l]), f64(inp.mu_v[l])
             t0 = time.perf_counter()
             zk = O.encode_k(ka, pos, ek, mk, H, dh, th)
             zv = O.encode_v(va, ev, mv)
+            t1 = time.perf_counter()
             O.decode_k(zk, fk, mk, pos, H, dh, th)
             O.decode_v(zv, fv, mv, D)
-            t_reuse += time.perf_counter() - t0
-            n_reuse += 1
-    n_r_all = sum(1 for p in wl.is_patch if not p)
-    n_p_all = sum(1 for p in wl.is_patch if p)
-    est = (t_reuse / max(n_reuse, 1)) * n_r_all + (t_patch / max(n_patch, 1)) * n_p_all
+            t2 = time.perf_counter()
+        t_enc[kind] += t1 - t0
+        t_con[kind] += t2 - t1
+        n_done[kind] += 1
+        spent += t2 - t0
+    n_all = {True: sum(1 for p in wl.is_patch if p), False: sum(1 for p in wl.is_patch if not p)}
+    est = lambda t: sum(t[k] / max(n_done[k], 1) * n_all[k] for k in (True, False))  # noqa: E731
+    scale = wl.n_tokens / max(S, 1)
+    est_con, est_enc = est(t_con) * scale, est(t_enc) * scale
     kv = algorithmic(wl)["kv_bytes"]
     return {
-        "value": round(kv / est / 1e9, 4), "unit": "GB/s", "cores": threads or cores,
+        "value": round(kv / est_con / 1e9, 4), "unit": "GB/s", "cores": threads or cores,
         "host_cpus": cores, "kind": "oracle",
-        "sample": (f"fp64 numpy oracle, full step of encode + Reuse decode + Patch over "
-                   f"{n_reuse}/{n_r_all} Reuse and {n_patch}/{n_p_all} Patch layers at "
-                   f"T={wl.n_tokens} (timed {t_reuse + t_patch:.1f} s), extrapolated per layer "
-                   f"kind to the whole step; inputs converted to fp64 outside the timed region"),
-        "est_step_s": round(est, 3),
+        "sample": (f"fp64 numpy oracle on {n_done[False]}/{n_all[False]} Reuse and "
+                   f"{n_done[True]}/{n_all[True]} Patch layers over {S} of {wl.n_tokens} tokens "
+                   f"(timed {spent:.1f} s), extrapolated per layer kind and token count: value = "
+                   f"KV bytes over the "
+                   f"consumer's Reuse decode + Patch (aligner, then W_K/W_V) on the oracle's own "
+                   f"codes; inputs converted to fp64 outside the timed region"),
+        "est_consumer_s": round(est_con, 3), "est_encode_s": round(est_enc, 3),
     }
 
 
@@ -357,18 +395,195 @@ def copy_ceiling(dev, gib=1.0, reps=10):
     return gbps
 
 
+
+
+def make_model(wl):
+    import paper_2606_07684_amd as scd
+
+    return scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
+                     head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
+                     is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
+                     basis_width=wl.w)
+
+
+def make_batch(wl, dev):
+    import paper_2606_07684_amd as scd
+    from synth import workloads as W
+
+    cu = W.cu_seqlens(wl, dev) if wl.n_seqs > 1 or wl.pos0 is not None else None
+    return scd.Batch(n_tokens=wl.n_tokens, cu_seqlens=cu, pos0=W.pos0(wl, dev))
+
+
+class Codec:
+    """Every buffer of one workload on the GPU and the step's three prepared entry-point calls."""
+
+    def __init__(self, wl, dev):
+        import torch
+
+        import paper_2606_07684_amd as scd
+        from synth import workloads as W
+
+        self.wl = wl
+        L, T, D, h = wl.n_layers, wl.n_tokens, wl.kv_width, wl.hidden_width
+        dt = wl.torch_dtype
+        self.inp = W.Inputs(wl, dev, decode=False)  # the decode consumes this step's own codes
+        self.model, self.batch = make_model(wl), make_batch(wl, dev)
+        self.rope = scd.scd_rope_table(self.model, wl.max_position)
+        self.z_k, self.z_v, self.z_h = W.alloc_codes(wl, dev)
+        self.k_cache, self.v_cache = W.alloc_caches(wl, dev)
+        inp = self.inp
+        # aligner weights and their fold into the consumer's projections (once, weights only)
+        self.aligner = [None] * L
+        fk, fv, ck, cv = ([None] * L for _ in range(4))
+        w2, b2 = [None] * L, [None] * L
+        for l in wl.patch_layers:
+            self.aligner[l] = W.aligner_weights(wl, l, dev)
+            w2[l], b2[l] = self.aligner[l][2], self.aligner[l][3]
+            fk[l] = torch.empty((D, h), dtype=dt, device=dev)
+            fv[l] = torch.empty((D, h), dtype=dt, device=dev)
+            ck[l] = torch.empty((D,), dtype=dt, device=dev)
+            cv[l] = torch.empty((D,), dtype=dt, device=dev)
+        self.fold = scd.prepare_patch_fold(self.model, h, w2, b2, inp.w_k, inp.w_v, inp.b_k,
+                                           inp.b_v, fk, fv, ck, cv)
+        self.folded = (fk, fv, ck, cv)
+        act_buf = torch.empty((T, h), dtype=dt, device=dev) if wl.patch_layers else None
+        self.act = [act_buf if wl.is_patch[l] else None for l in range(L)]
+        w1 = [a[0] if a is not None else None for a in self.aligner]
+        b1 = [a[1] if a is not None else None for a in self.aligner]
+        self.enc = scd.prepare_encode(self.model, self.batch, self.rope, inp.k_in, inp.v_in,
+                                      inp.h_in, inp.w_enc_k, inp.w_enc_v, inp.w_enc_h, inp.mu_k,
+                                      inp.mu_v, self.z_k, self.z_v, self.z_h)
+        self.dec = scd.prepare_reuse_decode(self.model, self.batch, self.rope, self.z_k, self.z_v,
+                                            inp.w_dec_k, inp.w_dec_v, inp.mu_k, inp.mu_v,
+                                            self.k_cache, self.v_cache)
+        self.pat = scd.prepare_patch_kv_from_codes(self.model, self.batch, self.rope, h, self.z_h,
+                                                   w1, b1, fk, fv, ck, cv, self.act,
+                                                   self.k_cache, self.v_cache)
+
+    def step(self, stream, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        self.enc(stream)
+        if ev is not None:
+            ev[1].record(stream)
+        self.dec(stream)
+        if ev is not None:
+            ev[2].record(stream)
+        self.pat(stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+
+def measure(wl, dev, steps, warmup, stream, codec=None):
+    """W warm-up steps, then K timed steps bracketed by synchronisations (wall clock), with HIP
+    events on the stream between the entry points.  Returns the workload's block."""
+    import torch
+
+    codec = codec or Codec(wl, dev)
+    torch.cuda.synchronize()
+    ev_fold = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev_fold[0].record(stream)
+    codec.fold(stream)
+    ev_fold[1].record(stream)
+    for _ in range(warmup):
+        codec.step(stream)
+    torch.cuda.synchronize()
+    fold_ms = ev_fold[0].elapsed_time(ev_fold[1])
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        codec.step(stream, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    phase = {k: [] for k in PHASES}
+    consumer = []
+    for ev in events:
+        phase["encode"].append(ev[0].elapsed_time(ev[1]))
+        phase["reuse_decode"].append(ev[1].elapsed_time(ev[2]))
+        phase["patch"].append(ev[2].elapsed_time(ev[3]))
+        consumer.append(ev[1].elapsed_time(ev[3]))
+    mean = {k: sum(v) / len(v) for k, v in phase.items()}
+    cons_ms = sum(consumer) / len(consumer)
+    alg = algorithmic(wl)
+    kv = alg["kv_bytes"]
+    ms_per_step = wall * 1e3 / steps
+    digest = source_digest()
+    rooflines = {}
+    for k in PHASES:
+        sym, bound = KERNELS[k]
+        b, f = alg[k]
+        t = mean[k] * 1e-3
+        if bound == "hbm":
+            ach, peak, unit = b / t / 1e9, HBM_PEAK_GBPS, "GB/s"
+        else:
+            ach, peak, unit = f / t / 1e12, MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"
+        rooflines[k] = {"kernel": sym, "bound": bound, "achieved": round(ach, 2), "peak": peak,
+                        "unit": unit, "frac": round(ach / peak, 4),
+                        "traffic": traffic_for(wl.name, k, digest),
+                        "ms_per_launch": round(mean[k], 4), "alg_bytes": b, "alg_flops": f}
+    stats = lambda v: {"mean": round(sum(v) / len(v), 4), "median": round(pct(v, 50), 4),  # noqa
+                       "p10": round(pct(v, 10), 4), "p90": round(pct(v, 90), 4)}
+    # the combined readings of the decode-side target (Reuse decode + Patch from the codes):
+    #   reuse_hbm_frac:     Reuse algorithmic bytes / t_reuse / 8 TB/s
+    #   patch_mfma_frac:    Patch flops (aligner hidden layer + folded product) / t_patch / peak
+    #   roofline_time_frac: the serial roofline time of the two phases (Reuse bytes at 8 TB/s, the
+    #                       aligner's hidden layer bytes at 8 TB/s, the folded product's flops at
+    #                       the MFMA peak) over their measured time
+    #   literal_hbm_frac:   (Reuse + Patch algorithmic bytes) / (t_reuse + t_patch) / 8 TB/s
+    t_r, t_p = mean["reuse_decode"] * 1e-3, mean["patch"] * 1e-3
+    hbm, mfma = HBM_PEAK_GBPS * 1e9, MFMA_PEAK_TFLOPS[wl.dtype] * 1e12
+    roof = alg["reuse_decode"][0] / hbm + alg["patch_act"][0] / hbm + alg["patch_gemm"][1] / mfma
+    block = {
+        "workload": wl.name,
+        "value_GBps": round(kv / (cons_ms * 1e-3) / 1e9, 2),
+        "consumer_ms": stats(consumer),
+        "tokens_per_s": round(wl.n_tokens / (cons_ms * 1e-3), 1),
+        "ms_per_step": round(ms_per_step, 4),
+        "whole_step_GBps": round(kv / (ms_per_step * 1e-3) / 1e9, 2),
+        "phase_ms": {k: stats(v) for k, v in phase.items()},
+        "rooflines": rooflines,
+        "decode_readings": {
+            "reuse_hbm_frac": round(alg["reuse_decode"][0] / t_r / hbm, 4),
+            "patch_mfma_frac": round(alg["patch"][1] / t_p / mfma, 4) if t_p > 0 else None,
+            "roofline_time_frac": round(roof / (t_r + t_p), 4),
+            "literal_hbm_frac": round((alg["reuse_decode"][0] + alg["patch"][0]) / (t_r + t_p)
+                                      / hbm, 4),
+        },
+        "fold_ms_once": round(fold_ms, 4),
+        "kv_bytes": kv,
+        "shape": {"n_layers": wl.n_layers, "d_model": wl.d_model, "n_kv_heads": wl.n_kv_heads,
+                  "head_dim": wl.head_dim, "n_tokens": wl.n_tokens, "n_requests": wl.n_seqs,
+                  "ranks": sorted(set(wl.ranks)), "ranks_v": sorted(set(wl.rank_v)),
+                  "patch_layers": list(wl.patch_layers), "basis_width": wl.w,
+                  "aligner_hidden": wl.hidden_width, "rope_theta": wl.rope_theta,
+                  "dtype": wl.dtype},
+    }
+    if wl.n_seqs > 1:  # every request's tokens over the consumer time of the packed batch
+        lens = [int(wl.cu_seqlens[b + 1] - wl.cu_seqlens[b]) for b in range(wl.n_seqs)]
+        per = sorted(n / (cons_ms * 1e-3) for n in lens)
+        block["tokens_per_s_per_request"] = {"min": round(per[0], 1),
+                                             "median": round(pct(per, 50), 1),
+                                             "max": round(per[-1], 1)}
+    return block, codec
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b_bf16")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="measure only --workload (skip the per-config blocks)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-receive", action="store_true",
                     help="skip the receipt timing (its decode launches share the step's kernel "
                          "and grid, so kernel traces of the step leave it out)")
     ap.add_argument("--no-fit", action="store_true",
                     help="skip the offline fit timing (it runs after the step's timing)")
+    ap.add_argument("--no-aligner", action="store_true",
+                    help="skip the unfolded aligner timing (scd_patch_align)")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run a plain copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -383,158 +598,60 @@ def main():
     import paper_2606_07684_amd as scd
     from synth import workloads as W
 
-    wl = {w.name: w for w in (*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS)}[args.workload]
+    known = {w.name: w for w in (*W.CONFIGS, *W.MODEL_SCALE_EXTRA, *W.TEST_WORKLOADS)}
+    wl = known[args.workload]
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     scd.load_library()
-    print(f"[bench] building inputs for {wl.name} (T={wl.n_tokens}, L={wl.n_layers})",
-          file=sys.stderr, flush=True)
-
-    inp = W.Inputs(wl, dev, decode=False)  # the decode consumes this step's encoded codes
-    model = scd.Model(n_layers=wl.n_layers, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
-                      head_dim=wl.head_dim, rope_theta=wl.rope_theta, dtype=wl.dtype,
-                      is_patch=wl.is_patch, rank_k=wl.ranks, rank_v=wl.rank_v, rank_h=wl.ranks,
-                      basis_width=wl.w)
-    cu = W.cu_seqlens(wl, dev) if wl.n_seqs > 1 or wl.pos0 is not None else None
-    batch = scd.Batch(n_tokens=wl.n_tokens, cu_seqlens=cu, pos0=W.pos0(wl, dev))
-    rope = scd.scd_rope_table(model, wl.max_position)
-    z_k, z_v, z_h = W.alloc_codes(wl, dev)
-    k_cache, v_cache = W.alloc_caches(wl, dev)
-    enc = scd.prepare_encode(model, batch, rope, inp.k_in, inp.v_in, inp.h_in, inp.w_enc_k,
-                             inp.w_enc_v, inp.w_enc_h, inp.mu_k, inp.mu_v, z_k, z_v, z_h)
-    dec = scd.prepare_reuse_decode(model, batch, rope, z_k, z_v, inp.w_dec_k, inp.w_dec_v,
-                                   inp.mu_k, inp.mu_v, k_cache, v_cache)
-    pat = scd.prepare_patch_kv(model, batch, rope, inp.h_hat, inp.w_k, inp.w_v, inp.b_k,
-                               inp.b_v, k_cache, v_cache)
     stream = torch.cuda.current_stream()
-    torch.cuda.synchronize()
-
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        enc(stream)
-        if ev is not None:
-            ev[1].record(stream)
-        dec(stream)
-        if ev is not None:
-            ev[2].record(stream)
-        pat(stream)
-        if ev is not None:
-            ev[3].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print("[bench] warmup done", file=sys.stderr, flush=True)
-
-    # the headline: K whole steps back to back, bracketed by synchronizations, no instrumentation
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    print("[bench] timed steps done", file=sys.stderr, flush=True)
-    # per-step breakdown: the same steps again, with HIP events between the entry points
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(events[i])
-    torch.cuda.synchronize()
-
-    phase = {"encode": [], "reuse_decode": [], "patch_kv": []}
-    for ev in events:
-        phase["encode"].append(ev[0].elapsed_time(ev[1]))
-        phase["reuse_decode"].append(ev[1].elapsed_time(ev[2]))
-        phase["patch_kv"].append(ev[2].elapsed_time(ev[3]))
-    mean = {k: sum(v) / len(v) for k, v in phase.items()}
-
-    alg = algorithmic(wl)
-    ms_per_step = wall * 1e3 / args.steps
-    kv = alg["kv_bytes"]
-    digest = source_digest()
-    rooflines = {}
-    for k, (sym, bound) in KERNELS.items():
-        b, f = alg[k]
-        t = mean[k] * 1e-3
-        if bound == "hbm":
-            ach, peak, unit = b / t / 1e9, HBM_PEAK_GBPS, "GB/s"
-        else:
-            ach, peak, unit = f / t / 1e12, MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"
-        rooflines[k] = {"kernel": sym, "bound": bound, "achieved": round(ach, 2),
-                        "peak": peak, "unit": unit, "frac": round(ach / peak, 4),
-                        "traffic": traffic_for(wl.name, k, digest),
-                        "ms_per_launch": round(mean[k], 4), "alg_bytes": b, "alg_flops": f}
-    dominant = max(mean, key=mean.get)
-    dom = rooflines[dominant]
-
+    print(f"[bench] {wl.name}: building inputs (T={wl.n_tokens}, L={wl.n_layers})",
+          file=sys.stderr, flush=True)
+    block, codec = measure(wl, dev, args.steps, args.warmup, stream)
+    print(f"[bench] {wl.name}: timed steps done", file=sys.stderr, flush=True)
+    dominant = max(PHASES, key=lambda k: block["phase_ms"][k]["mean"])
+    dom = block["rooflines"][dominant]
     out = {
         "metric": "reconstructed KV GB/s & tokens/s (Reuse+Patch decode); % of HBM roofline",
-        "value": round(kv / (ms_per_step * 1e-3) / 1e9, 2),
+        "value": block["value_GBps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": block["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded, model-shaped; no weights or datasets)",
-        "config": {"workload": wl.name, "n_layers": wl.n_layers, "d_model": wl.d_model,
-                   "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
-                   "n_tokens": wl.n_tokens, "n_requests": wl.n_seqs,
-                   "ranks": sorted(set(wl.ranks)), "ranks_v": sorted(set(wl.rank_v)),
-                   "patch_layers": list(wl.patch_layers),
-                   "basis_width": wl.w, "rope_theta": wl.rope_theta},
-        "tokens_per_s": round(wl.n_tokens / (ms_per_step * 1e-3), 1),
-        "phase_ms": {k: round(v, 4) for k, v in mean.items()},
-        "decode_patch_GBps": round(kv / ((mean["reuse_decode"] + mean["patch_kv"]) * 1e-3) / 1e9,
-                                   2),
+        "config": {"workload": wl.name, **block["shape"]},
+        "tokens_per_s": block["tokens_per_s"],
+        "consumer_ms": block["consumer_ms"],
+        "whole_step_GBps": block["whole_step_GBps"],
+        "phase_ms": block["phase_ms"],
         "roofline": {k: dom[k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")},
         "roofline_kernel": dom["kernel"],
-        "rooflines": rooflines,
-        "source_digest": digest,
+        "rooflines": block["rooflines"],
+        "decode_readings": block["decode_readings"],
+        "fold_ms_once": block["fold_ms_once"],
+        "source_digest": source_digest(),
     }
+    copy_gbps = copy_ceiling(dev)
+    out["decode_readings"]["copy_ceiling_GBps"] = round(copy_gbps, 1)
+    out["decode_readings"]["reuse_frac_of_copy_ceiling"] = round(
+        block["rooflines"]["reuse_decode"]["achieved"] / copy_gbps, 4)
 
-    # The Patch aligner (Eq. aligner, the row after the hot path): timed on its own over the same
-    # step count, reported beside the step and not part of ``value``.
-    if any(wl.is_patch):
-        print("[bench] timing the aligner", file=sys.stderr, flush=True)
-        out["aligner"] = time_aligner(wl, dev, args.steps, args.warmup, stream)
+    # The aligner without the fold (scd_patch_align, the unfolded chain's first half), beside.
+    if any(wl.is_patch) and not args.no_aligner:
+        print("[bench] timing the unfolded aligner", file=sys.stderr, flush=True)
+        out["aligner_unfolded"] = time_aligner(wl, dev, args.steps, args.warmup, stream)
 
     # The consumer's receipt from host memory (PCIe-inclusive), beside the step.
     if not args.no_receive:
         print("[bench] timing the streamed receipt", file=sys.stderr, flush=True)
-        out["receive"] = time_receive(wl, dev, args.steps, args.warmup, stream, model, batch, rope,
-                                      inp, z_k, z_v, z_h, k_cache, v_cache)
-
-    # The offline Reuse fit (Section 4.3.1), at the head-shared calibration shape, beside the step.
-    if not args.no_fit:
-        print("[bench] timing the offline fit", file=sys.stderr, flush=True)
-        out["fit"] = time_fit(dev, args.steps, args.warmup, stream)
-
-    # The combined readings of the decode-side target (Reuse decode + Patch at this workload):
-    #   reuse_hbm_frac:   Reuse algorithmic bytes / t_reuse / 8 TB/s
-    #   patch_mfma_frac:  Patch flops / t_patch / 2.5 PFLOP/s
-    #   roofline_time_frac: (t_HBM(Reuse) + t_MFMA(Patch)) / (t_reuse + t_patch), the fraction of the
-    #                     serial roofline time the two steps achieve together
-    #   literal_hbm_frac: (Reuse + Patch algorithmic bytes) / (t_reuse + t_patch) / 8 TB/s
-    # and the same decode and copy rates against a plain device copy timed in this run.
-    t_r, t_p = mean["reuse_decode"] * 1e-3, mean["patch_kv"] * 1e-3
-    b_r, b_p = alg["reuse_decode"][0], alg["patch_kv"][0]
-    f_p = alg["patch_kv"][1]
-    peak_flops = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12
-    copy_gbps = copy_ceiling(dev)
-    out["decode_readings"] = {
-        "reuse_hbm_frac": round(b_r / t_r / (HBM_PEAK_GBPS * 1e9), 4),
-        "patch_mfma_frac": round(f_p / t_p / peak_flops, 4),
-        "roofline_time_frac": round((b_r / (HBM_PEAK_GBPS * 1e9) + f_p / peak_flops) / (t_r + t_p),
-                                    4),
-        "literal_hbm_frac": round((b_r + b_p) / (t_r + t_p) / (HBM_PEAK_GBPS * 1e9), 4),
-        "copy_ceiling_GBps": round(copy_gbps, 1),
-        "reuse_frac_of_copy_ceiling": round(b_r / t_r / 1e9 / copy_gbps, 4),
-    }
+        out["receive"] = time_receive(wl, dev, args.steps, args.warmup, stream, codec.model,
+                                      codec.batch, codec.rope, codec.inp, codec.z_k, codec.z_v,
+                                      codec.z_h, codec.k_cache, codec.v_cache)
 
     if args.copy_probe_gib > 0:
         n = int(args.copy_probe_gib * (1 << 30)) // 4
@@ -548,7 +665,36 @@ def main():
 
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, inp)
+        out["cpu_baseline"] = cpu_baseline(wl, codec.inp, codec.aligner)
+    del codec
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    # The offline Reuse fit (Section 4.3.1), at the head-shared calibration shape, beside the step.
+    if not args.no_fit:
+        print("[bench] timing the offline fit", file=sys.stderr, flush=True)
+        out["fit"] = time_fit(dev, args.steps, args.warmup, stream)
+        torch.cuda.empty_cache()
+
+    # Every model-shaped workload in the same run (the same step and readings; a CPU baseline with
+    # a smaller budget each).
+    if not args.no_configs:
+        out["configs"] = {}
+        for other in W.CONFIGS:
+            if other.name == wl.name:
+                continue
+            print(f"[bench] {other.name}: building inputs (T={other.n_tokens}, "
+                  f"L={other.n_layers})", file=sys.stderr, flush=True)
+            blk, cdc = measure(other, dev, args.steps, args.warmup, stream)
+            if not args.no_cpu_baseline:
+                print(f"[bench] {other.name}: CPU oracle baseline", file=sys.stderr, flush=True)
+                blk["cpu_baseline"] = cpu_baseline(other, cdc.inp, cdc.aligner, budget_s=8.0,
+                                                   max_tokens=2048)
+            out["configs"][other.name] = blk
+            del cdc
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            print(f"[bench] {other.name}: {blk['value_GBps']} GB/s", file=sys.stderr, flush=True)
     print(json.dumps(out), flush=True)
 
 

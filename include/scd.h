@@ -184,6 +184,45 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
                              const void* const* w2, const void* const* b2,
                              void* const* act, void* const* h_hat, hipStream_t stream);
 
+/* ---- Patch from the codes, with the aligner's output layer folded (Section 4.4.2) -------------
+ * Eq. aligner ends in an affine layer (h_hat = act w2^T + b2) and Eq. kv_from_patch applies the
+ * consumer's projections to h_hat with no nonlinearity in between, so for P = K, V:
+ *   h_hat w_p^T + b_p = act (w_p w2)^T + (w_p b2 + b_p).
+ * scd_patch_fold forms, once per model pair, for every Patch layer l:
+ *   w_fold_k[l] = w_k[l] w2[l]   [D, hidden],    c_k[l] = w_k[l] b2[l] + b_k[l]   [D]
+ *   w_fold_v[l] = w_v[l] w2[l]   [D, hidden],    c_v[l] = w_v[l] b2[l] + b_v[l]   [D]
+ * with w2 [d_model, hidden] and b2 [d_model] the aligner's output layer (scd_patch_align's), w_k,
+ * w_v [D, d_model] and b_k, b_v [D] the consumer's projections (b2, b_k, b_v optional: NULL array
+ * or entry = 0), accumulated in fp32 and rounded once to the model's dtype.  Every output buffer
+ * is written whole; outputs must not repeat across layers or branches (SCD_ERR_SHAPE) nor overlap
+ * the inputs.  hidden % 16 == 0.  The batch plays no part.
+ *
+ * scd_patch_kv_from_codes is the consumer's Patch from the transmitted codes (Algorithm 1): for
+ * every Patch layer l, in layer order,
+ *   act[l]     = SiLU(z_h[l] w1[l]^T + b1[l])                 [T, hidden]
+ *   k_cache[l] = RoPE(act[l] w_fold_k[l]^T + c_k[l]),   v_cache[l] = act[l] w_fold_v[l]^T + c_v[l]
+ * which equals scd_patch_align followed by scd_patch_kv up to rounding, without forming h_hat
+ * (its product of inner dimension d_model disappears).  act holds caller-owned [T, hidden]
+ * activations and may repeat across layers: a run of consecutive Patch layers with distinct act
+ * buffers is computed together (one launch of each product), and a buffer that repeats starts a
+ * new run after the previous one has consumed it, so one buffer can serve every layer (at the
+ * cost of a launch pair per layer).  c_k, c_v are optional (NULL = 0).  Other arguments and
+ * limits as scd_patch_align and scd_patch_kv.  Reuse layers are not touched. */
+scd_status_t scd_patch_fold(const scd_model_t* model, int32_t hidden,
+                            const void* const* w2, const void* const* b2,
+                            const void* const* w_k, const void* const* w_v,
+                            const void* const* b_k, const void* const* b_v,
+                            void* const* w_fold_k, void* const* w_fold_v,
+                            void* const* c_k, void* const* c_v, hipStream_t stream);
+scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t* batch,
+                                     const void* rope_table, int64_t max_position, int32_t hidden,
+                                     const void* const* z_h,
+                                     const void* const* w1, const void* const* b1,
+                                     const void* const* w_fold_k, const void* const* w_fold_v,
+                                     const void* const* c_k, const void* const* c_v,
+                                     void* const* act, void* const* k_cache, void* const* v_cache,
+                                     hipStream_t stream);
+
 /* ---- packed payload and streamed receipt (Algorithm 1's transmitted set; Section 4.5) ---------
  * The codes Algorithm 1 sends travel as one contiguous buffer in the layout scd_payload_bytes
  * describes: layers in order, a Reuse layer's K codes [T*g, rank_k] then its V codes

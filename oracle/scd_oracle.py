@@ -234,6 +234,25 @@ def patch_v(h_hat, w_v, b_v):
 
 
 # --------------------------------------------------------------------------------------------
+# The aligner's output layer folded into a projection.  Eq. (aligner) ends in the affine map
+# H_hat = act W2^T + b2 and Eq. (kv_from_patch) applies W_P (P = K, V) to H_hat before any
+# nonlinearity, so H_hat W_P^T + b_P = act (W_P W2)^T + (W_P b2 + b_P).
+# --------------------------------------------------------------------------------------------
+def fold_aligner(w_p, b_p, w2, b2):
+    """``(W_P @ W2, W_P @ b2 + b_P)`` with ``W_P [D, d_model]``, ``W2 [d_model, h]``; an absent
+    bias counts as zero.  Regenerating a Patch layer from the aligner's hidden activations with
+    the folded pair, ``patch_k(act, W_fold, c, ...)``, equals ``patch_k(H_hat, W_P, b_P, ...)``."""
+    w_p, w2 = _f64(w_p), _f64(w2)
+    w_fold = w_p @ w2
+    c = np.zeros(w_p.shape[0], dtype=F64)
+    if b2 is not None:
+        c = c + w_p @ _f64(b2)
+    if b_p is not None:
+        c = c + _f64(b_p)
+    return w_fold, c
+
+
+# --------------------------------------------------------------------------------------------
 # Whole-model passes in Algorithm 1's order, and a8 cache assembly (Appendix F.2 "Cache
 # Assembly": Reuse layers hold reconstructed KV, Patch layers hold regenerated KV).
 # --------------------------------------------------------------------------------------------

@@ -30,8 +30,9 @@ __all__ = [
     "Prepared", "prepare_encode", "prepare_reuse_decode", "prepare_patch_kv",
     "scd_patch_align", "prepare_patch_align", "scd_payload_views",
     "scd_reuse_decode_streamed", "prepare_reuse_decode_streamed", "PreparedStreamed",
-    "DEFAULT_LAYERS_PER_GROUP", "scd_fit_solve_noalloc", "prepare_fit_solve_noalloc",
-    "scd_fit_solve_noalloc_max_bytes",
+    "DEFAULT_LAYERS_PER_GROUP", "scd_patch_fold", "prepare_patch_fold",
+    "scd_patch_kv_from_codes", "prepare_patch_kv_from_codes", "scd_fit_solve_noalloc",
+    "prepare_fit_solve_noalloc", "scd_fit_solve_noalloc_max_bytes",
 ]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -120,6 +121,11 @@ _SIGS = {
     "scd_fit_solve": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32, ctypes.c_int64,
                                      ctypes.c_double, ctypes.c_int32] + [_PP] * 6
                       + [_VP, ctypes.c_size_t, _VP]),
+    "scd_patch_fold": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32] + [_PP] * 10
+                       + [_VP]),
+    "scd_patch_kv_from_codes": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.POINTER(_CBatch),
+                                               _VP, ctypes.c_int64, ctypes.c_int32] + [_PP] * 10
+                                + [_VP]),
     "scd_fit_solve_noalloc_max_bytes": (ctypes.c_size_t, []),
     "scd_fit_solve_noalloc": (ctypes.c_int, [ctypes.POINTER(_CModel), ctypes.c_int32,
                                              ctypes.c_int64, ctypes.c_double, ctypes.c_int32]
@@ -446,6 +452,71 @@ def prepare_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2
 def scd_patch_align(model: Model, batch: Batch, hidden: int, z_h, w1, b1, w2, b2, act, h_hat,
                     stream=None) -> None:
     prepare_patch_align(model, batch, hidden, z_h, w1, b1, w2, b2, act, h_hat)(stream)
+
+
+def prepare_patch_fold(model: Model, hidden: int, w2, b2, w_k, w_v, b_k, b_v, w_fold_k, w_fold_v,
+                       c_k, c_v) -> Prepared:
+    """Fold the aligner's output layer into the consumer's projections (once per model pair):
+    w_fold = W_P w2 [D, hidden] and c = W_P b2 + b_P [D] for P = K, V and every Patch layer."""
+    lib = load_library()
+    L, D, d = model.n_layers, model.kv_width, model.d_model
+    dt = model.torch_dtype
+    P = [l for l in range(L) if model.is_patch[l]]
+    args = [
+        _ptr_array(w2, L, "w2", {l: (d, hidden) for l in P}, dt),
+        _ptr_array(b2, L, "b2", {l: (d,) for l in P}, dt),
+        _ptr_array(w_k, L, "w_k", {l: (D, d) for l in P}, dt),
+        _ptr_array(w_v, L, "w_v", {l: (D, d) for l in P}, dt),
+        _ptr_array(b_k, L, "b_k", {l: (D,) for l in P}, dt),
+        _ptr_array(b_v, L, "b_v", {l: (D,) for l in P}, dt),
+        _ptr_array(w_fold_k, L, "w_fold_k", {l: (D, hidden) for l in P}, dt),
+        _ptr_array(w_fold_v, L, "w_fold_v", {l: (D, hidden) for l in P}, dt),
+        _ptr_array(c_k, L, "c_k", {l: (D,) for l in P}, dt),
+        _ptr_array(c_v, L, "c_v", {l: (D,) for l in P}, dt),
+    ]
+    return Prepared(lib.scd_patch_fold, (ctypes.byref(model._c), int(hidden),
+                                         *[_as_pp(a) for a in args]), (model, args))
+
+
+def scd_patch_fold(model: Model, hidden: int, w2, b2, w_k, w_v, b_k, b_v, w_fold_k, w_fold_v,
+                   c_k, c_v, stream=None) -> None:
+    prepare_patch_fold(model, hidden, w2, b2, w_k, w_v, b_k, b_v, w_fold_k, w_fold_v, c_k,
+                       c_v)(stream)
+
+
+def prepare_patch_kv_from_codes(model: Model, batch: Batch, rope: Optional[RopeTable], hidden: int,
+                                z_h, w1, b1, w_fold_k, w_fold_v, c_k, c_v, act, k_cache,
+                                v_cache) -> Prepared:
+    """Patch from the transmitted codes: act = SiLU(z_h w1^T + b1), then
+    K = RoPE(act w_fold_k^T + c_k), V = act w_fold_v^T + c_v into the cache, layer by layer
+    (act entries may repeat: one [T, hidden] buffer can serve every Patch layer)."""
+    lib = load_library()
+    L, T, D = model.n_layers, batch.n_tokens, model.kv_width
+    dt = model.torch_dtype
+    P = [l for l in range(L) if model.is_patch[l]]
+    args = [
+        _ptr_array(z_h, L, "z_h", {l: (T, model.rank_h[l]) for l in P}, dt),
+        _ptr_array(w1, L, "w1", {l: (hidden, model.rank_h[l]) for l in P}, dt),
+        _ptr_array(b1, L, "b1", {l: (hidden,) for l in P}, dt),
+        _ptr_array(w_fold_k, L, "w_fold_k", {l: (D, hidden) for l in P}, dt),
+        _ptr_array(w_fold_v, L, "w_fold_v", {l: (D, hidden) for l in P}, dt),
+        _ptr_array(c_k, L, "c_k", {l: (D,) for l in P}, dt),
+        _ptr_array(c_v, L, "c_v", {l: (D,) for l in P}, dt),
+        _ptr_array(act, L, "act", {l: (T, hidden) for l in P}, dt),
+        _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in P}, dt),
+        _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in P}, dt),
+    ]
+    tab, maxp = _rope_args(rope)
+    return Prepared(lib.scd_patch_kv_from_codes,
+                    (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp, int(hidden),
+                     *[_as_pp(a) for a in args]), (model, batch, rope, args))
+
+
+def scd_patch_kv_from_codes(model: Model, batch: Batch, rope: Optional[RopeTable], hidden: int,
+                            z_h, w1, b1, w_fold_k, w_fold_v, c_k, c_v, act, k_cache, v_cache,
+                            stream=None) -> None:
+    prepare_patch_kv_from_codes(model, batch, rope, hidden, z_h, w1, b1, w_fold_k, w_fold_v, c_k,
+                                c_v, act, k_cache, v_cache)(stream)
 
 
 def _payload_buffer(t, name: str, nbytes: int, need_cuda: bool) -> torch.Tensor:

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(PKG_DIR, "libscd.so")
 ARCH = "gfx950"
 
 SOURCES = ["scd_gemm.hip", "scd_patch.hip", "scd_decode.hip", "scd_encode.hip", "scd_fit.hip",
-           "scd_api.cpp"]
+           "scd_fold.hip", "scd_api.cpp"]
 
 FLAGS = [
     f"--offload-arch={ARCH}",

@@ -603,6 +603,52 @@ scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch
   return ok();
 }
 
+}  // extern "C"
+
+namespace {
+
+// The aligner's first product act = SiLU(z_h w1^T + b1) for `jobs` (one per Patch layer, K = r_H).
+// It is a short contraction whose time is writing act: the shape of a Reuse decode (code x basis
+// + offset), so the bf16 decode kernel takes it when it can (r_H <= 128, r_H % 32 == 0); else the
+// bf16 GEMM body when `fast` (r_H % 64 == 0 and hidden % 128 == 0), else the generic kernel.
+// *on_decode reports whether the decode kernel took it.
+scd_status_t enqueue_align_first(const scd_model_t* model, const scd_batch_t* batch, int hidden,
+                                 const std::vector<scd::GemmJob>& jobs, bool fast,
+                                 bool* on_decode, hipStream_t stream) {
+  const scd::GemmParams base = base_params(model, batch, batch->n_tokens, 1, nullptr, 0);
+  bool decode_first = model->dtype == SCD_BF16 && hidden % 128 == 0 &&
+                      (model->head_dim == 64 || model->head_dim == 128) &&
+                      batch->n_seqs <= scd::kMaxLdsSeqs;
+  for (const auto& j : jobs)
+    if (j.k % 32 != 0 || j.k > 128) decode_first = false;
+  *on_decode = decode_first;
+  if (decode_first) {
+    for (const auto& grp : group_by(jobs, [](const scd::GemmJob& j) { return j.k; })) {
+      const int nhg = scd::decode_channel_groups(grp[0].k, hidden);
+      JobPacker jp(base, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
+      for (const auto& j : grp) jp.add(j);
+      for (const auto& lp : jp.build()) {
+        const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream, true);
+        if (e != hipSuccess)
+          return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
+      }
+    }
+    return ok();
+  }
+  JobPacker jp(base, fast ? scd::kPatchBM : scd::kGenericBM, fast ? scd::kPatchBN : scd::kGenericBN);
+  for (const auto& j : jobs) jp.add(j);
+  if (!fast) return run(scd::Op::kPatchAlign, jp.build(), model->dtype, stream);
+  for (const auto& p : jp.build()) {
+    const hipError_t e = scd::launch_align_bf16(p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
 scd_status_t scd_patch_kv(const scd_model_t* model, const scd_batch_t* batch,
                           const void* rope_table, int64_t max_position,
                           const void* const* h_hat,
@@ -692,50 +738,162 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
 
   const int64_t T = batch->n_tokens;
   const int d = model->d_model;
-  scd::GemmParams base = base_params(model, batch, T, 1, nullptr, 0);
+  const scd::GemmParams base = base_params(model, batch, T, 1, nullptr, 0);
   // act = SiLU(z_h w1^T + b1) for every Patch layer, then h_hat = act w2^T + b2
   std::vector<scd::GemmJob> first_jobs;
-  JobPacker first(base, fast1 ? scd::kPatchBM : scd::kGenericBM,
-                  fast1 ? scd::kPatchBN : scd::kGenericBN);
   JobPacker second(base, fast2 ? scd::kPatchBM : scd::kGenericBM,
                    fast2 ? scd::kPatchBN : scd::kGenericBN);
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
-    const scd::GemmJob j1{z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
-                          scd::kVecOut | scd::kSiluOut, 0};
-    first_jobs.push_back(j1);
-    first.add(j1);
+    first_jobs.push_back({z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
+                          scd::kVecOut | scd::kSiluOut, 0});
     second.add({act[l], w2[l], h_hat[l], b2 ? b2[l] : nullptr, d, hidden, scd::kVecOut, 0});
   }
-  // The first product is a short contraction (K = r_H) whose time is writing act: the shape of a
-  // Reuse decode (code x basis + offset), so the bf16 decode kernel takes it when it can.
-  bool decode_first = model->dtype == SCD_BF16 && hidden % 128 == 0 &&
-                      (model->head_dim == 64 || model->head_dim == 128) &&
-                      batch->n_seqs <= scd::kMaxLdsSeqs;
-  for (const auto& j : first_jobs)
-    if (j.k % 32 != 0 || j.k > 128) decode_first = false;
-  if (decode_first) {
-    for (const auto& grp : group_by(first_jobs, [](const scd::GemmJob& j) { return j.k; })) {
-      const int nhg = scd::decode_channel_groups(grp[0].k, hidden);
-      JobPacker jp(base, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
-      for (const auto& j : grp) jp.add(j);
-      for (const auto& lp : jp.build()) {
-        const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream, true);
-        if (e != hipSuccess)
-          return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
-      }
-    }
+  bool on_decode = false;
+  SCD_TRY(enqueue_align_first(model, batch, hidden, first_jobs, fast1, &on_decode, stream));
+  if (!fast2) return run(scd::Op::kPatchAlign, second.build(), model->dtype, stream);
+  for (const auto& p : second.build()) {
+    const hipError_t e = scd::launch_align_bf16(p, stream);
+    if (e != hipSuccess)
+      return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
   }
-  for (JobPacker* jp : {&first, &second}) {
-    if (jp == &first && decode_first) continue;
-    if (!(jp == &first ? fast1 : fast2)) {
-      SCD_TRY(run(scd::Op::kPatchAlign, jp->build(), model->dtype, stream));
+  return ok();
+}
+
+// A per-layer output that must not repeat across the listed layers.
+static scd_status_t distinct_layer_outputs(const std::vector<int>& layers, const void* const* arr,
+                                           const char* name) {
+  for (size_t i = 0; i < layers.size(); ++i)
+    for (size_t j = 0; j < i; ++j)
+      if (arr[layers[i]] == arr[layers[j]])
+        return fail(SCD_ERR_SHAPE, "%s[%d] repeats layer %d's buffer", name, layers[i], layers[j]);
+  return SCD_OK;
+}
+
+scd_status_t scd_patch_fold(const scd_model_t* model, int32_t hidden,
+                            const void* const* w2, const void* const* b2,
+                            const void* const* w_k, const void* const* w_v,
+                            const void* const* b_k, const void* const* b_v,
+                            void* const* w_fold_k, void* const* w_fold_v,
+                            void* const* c_k, void* const* c_v, hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  if (hidden < 16 || hidden % 16 != 0)
+    return fail(SCD_ERR_SHAPE, "aligner width %d must be a positive multiple of 16", hidden);
+  std::vector<int> layers;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    layers.push_back(l);
+    const void* tmp;
+    SCD_TRY(need_ptr(w2, l, "w2"));
+    SCD_TRY(opt_ptr(b2, l, "b2", &tmp));
+    SCD_TRY(need_ptr(w_k, l, "w_k"));
+    SCD_TRY(need_ptr(w_v, l, "w_v"));
+    SCD_TRY(opt_ptr(b_k, l, "b_k", &tmp));
+    SCD_TRY(opt_ptr(b_v, l, "b_v", &tmp));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(w_fold_k), l, "w_fold_k"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(w_fold_v), l, "w_fold_v"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(c_k), l, "c_k"));
+    SCD_TRY(need_ptr(reinterpret_cast<const void* const*>(c_v), l, "c_v"));
+    if (w_fold_k[l] == w_fold_v[l] || c_k[l] == c_v[l])
+      return fail(SCD_ERR_SHAPE, "layer %d's key and value outputs share a buffer", l);
+  }
+  if (layers.empty()) return ok();
+  SCD_TRY(distinct_layer_outputs(layers, reinterpret_cast<const void* const*>(w_fold_k), "w_fold_k"));
+  SCD_TRY(distinct_layer_outputs(layers, reinterpret_cast<const void* const*>(w_fold_v), "w_fold_v"));
+  SCD_TRY(distinct_layer_outputs(layers, reinterpret_cast<const void* const*>(c_k), "c_k"));
+  SCD_TRY(distinct_layer_outputs(layers, reinterpret_cast<const void* const*>(c_v), "c_v"));
+
+  std::vector<scd::FoldJob> jobs;
+  for (int l : layers) {
+    jobs.push_back({w_k[l], w2[l], b2 ? b2[l] : nullptr, b_k ? b_k[l] : nullptr, w_fold_k[l], c_k[l]});
+    jobs.push_back({w_v[l], w2[l], b2 ? b2[l] : nullptr, b_v ? b_v[l] : nullptr, w_fold_v[l], c_v[l]});
+  }
+  for (size_t done = 0; done < jobs.size(); done += scd::kMaxJobs) {
+    scd::FoldParams p{};
+    p.n_jobs = 0;
+    for (size_t i = done; i < jobs.size() && i < done + scd::kMaxJobs; ++i) p.jobs[p.n_jobs++] = jobs[i];
+    p.n = static_cast<int32_t>(kv_width(model));
+    p.d_model = model->d_model;
+    p.hidden = hidden;
+    const hipError_t e = scd::launch_patch_fold(model->dtype == SCD_BF16, p, stream);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "fold launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t* batch,
+                                     const void* rope_table, int64_t max_position, int32_t hidden,
+                                     const void* const* z_h,
+                                     const void* const* w1, const void* const* b1,
+                                     const void* const* w_fold_k, const void* const* w_fold_v,
+                                     const void* const* c_k, const void* const* c_v,
+                                     void* const* act, void* const* k_cache, void* const* v_cache,
+                                     hipStream_t stream) {
+  SCD_TRY(check_model(model));
+  SCD_TRY(check_batch(batch));
+  if (hidden < 16 || hidden % 16 != 0)
+    return fail(SCD_ERR_SHAPE, "aligner width %d must be a positive multiple of 16", hidden);
+  const int rh_max = model->d_model < 256 ? model->d_model : 256;
+  const int64_t T = batch->n_tokens;
+  bool any = false, rh64 = true;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    any = true;
+    const void* tmp;
+    SCD_TRY(check_rank("rank_h", l, model->rank_h[l], rh_max));
+    SCD_TRY(need_tok_ptr(z_h, l, "z_h", T));
+    SCD_TRY(need_ptr(w1, l, "w1"));
+    SCD_TRY(opt_ptr(b1, l, "b1", &tmp));
+    SCD_TRY(need_ptr(w_fold_k, l, "w_fold_k"));
+    SCD_TRY(need_ptr(w_fold_v, l, "w_fold_v"));
+    SCD_TRY(opt_ptr(c_k, l, "c_k", &tmp));
+    SCD_TRY(opt_ptr(c_v, l, "c_v", &tmp));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(act), l, "act", T));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache", T));
+    SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache", T));
+    if (model->rank_h[l] % 64 != 0) rh64 = false;
+  }
+  if (any && T > 0) SCD_TRY(check_rope(rope_table, max_position));
+  if (!any || T == 0) return ok();
+
+  const int D = static_cast<int>(kv_width(model));
+  const bool fast_first = model->dtype == SCD_BF16 && hidden % 128 == 0 && rh64;
+  const bool fast = model->dtype == SCD_BF16 && hidden % 64 == 0 &&
+                    (model->head_dim == 64 || model->head_dim == 128) && D % 128 == 0;
+  const scd::GemmParams base = base_params(model, batch, T, 1, rope_table, max_position);
+  // Patch layers in order, grouped: a group is a run of consecutive Patch layers whose act buffers
+  // are all distinct; each group is one launch of the hidden layer and one of the folded product.
+  // A buffer that repeats starts a new group, so a shared act buffer is overwritten only after the
+  // product that reads it (stream order).
+  std::vector<std::vector<int>> groups;
+  for (int l = 0; l < model->n_layers; ++l) {
+    if (!model->is_patch[l]) continue;
+    bool clash = groups.empty();
+    if (!clash)
+      for (int m : groups.back())
+        if (act[m] == act[l]) clash = true;
+    if (clash) groups.emplace_back();
+    groups.back().push_back(l);
+  }
+  for (const auto& grp : groups) {
+    std::vector<scd::GemmJob> first;
+    JobPacker jp(base, fast ? scd::kPatchBM : scd::kGenericBM, fast ? scd::kPatchBN : scd::kGenericBN);
+    for (int l : grp) {
+      first.push_back({z_h[l], w1[l], act[l], b1 ? b1[l] : nullptr, hidden, model->rank_h[l],
+                       scd::kVecOut | scd::kSiluOut, 0});
+      jp.add({act[l], w_fold_k[l], k_cache[l], c_k ? c_k[l] : nullptr, D, hidden,
+              scd::kRopeOut | scd::kVecOut, 0});
+      jp.add({act[l], w_fold_v[l], v_cache[l], c_v ? c_v[l] : nullptr, D, hidden, scd::kVecOut, 0});
+    }
+    bool on_decode = false;
+    SCD_TRY(enqueue_align_first(model, batch, hidden, first, fast_first, &on_decode, stream));
+    if (!fast) {
+      SCD_TRY(run(scd::Op::kPatchKV, jp.build(), model->dtype, stream));
       continue;
     }
-    for (const auto& p : jp->build()) {
-      const hipError_t e = scd::launch_align_bf16(p, stream);
-      if (e != hipSuccess)
-        return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
+    for (const auto& p : jp.build()) {
+      const hipError_t e = scd::launch_patch_bf16(p, stream);
+      if (e != hipSuccess) return fail(SCD_ERR_HIP, "patch launch failed: %s", hipGetErrorString(e));
     }
   }
   return ok();

@@ -138,8 +138,8 @@ __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch&
             if (c.silu) {
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
-                a[r] = a[r] / (1.f + __expf(-a[r]));
-                b[r] = b[r] / (1.f + __expf(-b[r]));
+                a[r] = silu_bf16(a[r]);
+                b[r] = silu_bf16(b[r]);
               }
             }
           }

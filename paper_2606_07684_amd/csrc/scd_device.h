@@ -93,6 +93,12 @@ __device__ inline int row_of_lds(int rho) {
   return (rho & ~31) | (16 * ((o >> 2) & 1) + 4 * (o >> 3) + (o & 3));
 }
 
+// SiLU x / (1 + e^-x) for outputs rounded to bf16 next: the hardware exponential and reciprocal
+// (each within about an ulp of fp32, far inside that rounding) instead of an IEEE division, which
+// costs about ten instructions per element.  For very negative x, e^-x overflows to inf and its
+// reciprocal is 0, so the result is the limit -0.
+__device__ inline float silu_bf16(float x) { return x * __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+
 __device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ inline uint32_t pack_bf16x2(float a, float b) {

@@ -68,6 +68,26 @@ hipError_t launch_patch_bf16(const GemmParams& p, hipStream_t stream);
 // act = SiLU on jobs flagged kSiluOut; no RoPE.
 hipError_t launch_align_bf16(const GemmParams& p, hipStream_t stream);
 
+// Fold of the aligner's output layer into a projection (one-time, weights only):
+// wf = wp w2 [n, hidden] and c = wp b2 + bp [n], fp32 accumulation, one rounding.
+struct FoldJob {
+  const void* wp;  // [n, d_model]  consumer projection W_K or W_V
+  const void* w2;  // [d_model, hidden]  aligner output layer
+  const void* b2;  // [d_model] or null
+  const void* bp;  // [n] or null (projection bias)
+  void* wf;        // [n, hidden] out
+  void* c;         // [n] out
+};
+struct FoldParams {
+  FoldJob jobs[kMaxJobs];
+  int32_t n_jobs;
+  int32_t n;        // D
+  int32_t d_model;  // multiple of 32
+  int32_t hidden;   // multiple of 16
+};
+static_assert(sizeof(FoldParams) <= 4096, "kernel argument block");
+hipError_t launch_patch_fold(bool bf16, const FoldParams& p, hipStream_t stream);
+
 // Reuse decode on the bf16 path: workgroups own a channel chunk of 128 * nhg and a share of the
 // launch's row tiles (decode_tile_rows(nhg) rows each); basis_width % (128 * nhg) == 0, one rank
 // (% 32 == 0, <= 256) and one branch per launch, head_dim 64 or 128.

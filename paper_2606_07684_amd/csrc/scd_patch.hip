@@ -33,9 +33,15 @@ constexpr int kLDK = kBK;                   // LDS row (bf16 elements): 8 16-byt
 constexpr int kChunks = kBK / 8;
 constexpr int kSlot = kBN * kLDK;           // elements per ring slot (one operand tile of a step)
 constexpr int kRing = 5;                    // slots
-constexpr int kThreads = 256;
+#ifndef SCD_PATCH_WAVES
+#define SCD_PATCH_WAVES 4
+#endif
+constexpr int kWaves = SCD_PATCH_WAVES;     // 4: one wave per SIMD; 8: two
+constexpr int kThreads = 64 * kWaves;
 constexpr int kDmaIters = kBN * kChunks / kThreads;  // copy instructions per wave per operand tile
 constexpr int kDmaPerStage = 2 * kDmaIters;          // ... per step (both operands)
+constexpr int kWaveTok = 256 * 2 / kWaves;  // tokens per wave (each wave owns 128 channels)
+constexpr int kUB = kWaveTok / 32;          // 32-token MFMA blocks per wave
 static_assert(kBN == kBM, "square tiles: both operand tiles fill one slot");
 static_assert(kRing * kSlot * 2 <= 160 * 1024, "LDS");
 // Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data format, no swizzle.
@@ -61,19 +67,31 @@ constexpr int kLgkmDone = 0xF | (0x3 << 14) | (0x7 << 4);
 #define SCD_MFMA_THEN_READ                          \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
   __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-#define SCD_MFMA_THEN_DMA                            \
+#define SCD_MFMA_THEN_DMA(n)                         \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x020, kDmaPerStage / 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x020, n, 0);
 __device__ __forceinline__ void interleave_reads() {
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  if constexpr (kWaves == 4) {  // 16 MFMAs, 8 reads
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  } else {  // 8 MFMAs, 6 reads
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  }
 }
 __device__ __forceinline__ void interleave_reads_dma() {
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA
-  SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA SCD_MFMA_THEN_DMA
+  if constexpr (kWaves == 4) {  // 16 MFMAs, 8 reads, 16 copies
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2)
+    SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2)
+  } else {  // 8 MFMAs, 6 reads, 8 copies
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+    SCD_MFMA_THEN_DMA(4) SCD_MFMA_THEN_DMA(4)
+  }
 }
 #undef SCD_MFMA_THEN_DMA
 #undef SCD_MFMA_THEN_READ
@@ -86,7 +104,7 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wn = wave >> 1, wt = wave & 1;
+  const int wn = wave / (kWaves / 2), wt = wave % (kWaves / 2);  // channel half, token part
 
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
   const GemmJob job = p.jobs[job_of(p, unit)];
@@ -116,7 +134,7 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   uint32_t woff[kDmaIters], hoff[kDmaIters];
 #pragma unroll
   for (int j = 0; j < kDmaIters; ++j) {
-    const int slot = (4 * j + wave) * 64 + lane;
+    const int slot = (kWaves * j + wave) * 64 + lane;
     const int rho = slot / kChunks, c = (slot % kChunks) ^ swz(slot / kChunks);
     const int n = row_of_lds(rho) < N - n0 ? row_of_lds(rho) : N - n0 - 1;
     const int t = t0 + rho < M ? rho : static_cast<int>(M - 1 - t0);
@@ -130,15 +148,15 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
 #pragma unroll
     for (int j = 0; j < kDmaIters; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(tokens ? hres : wres,
-                                               (lds_void_t)(dst + 8 * ((4 * j + wave) * 64)), 16,
+                                               (lds_void_t)(dst + 8 * ((kWaves * j + wave) * 64)), 16,
                                                tokens ? hoff[j] : woff[j], kb, 0, 0);
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][kUB];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < kUB; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[s][u][e] = 0.f;
 
@@ -152,14 +170,14 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     for (int s = 0; s < 4; ++s)
       af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + co);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < kUB; ++u)
       bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + co);
   };
   auto mma = [&](const bf16x8* af, const bf16x8* bfr) {
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < kUB; ++u)
         acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
@@ -179,8 +197,8 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * kDmaIters, true));
   lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
-  const uint16_t* hrow = smem + (wt * 128 + lr) * kLDK;
-  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  const uint16_t* hrow = smem + (wt * kWaveTok + lr) * kLDK;
+  bf16x8 a0[4], b0[kUB], a1[4], b1[kUB];
   int sh = 0, sw = 1;        // slots of step kc's token and weight tiles
   frags(wrow + sw * kSlot, hrow + sh * kSlot, 0, a0, b0);
   for (int kc = 0; kc < nk; ++kc) {
@@ -284,8 +302,8 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     if (silu) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        a[r] = a[r] / (1.f + __expf(-a[r]));
-        b[r] = b[r] / (1.f + __expf(-b[r]));
+        a[r] = silu_bf16(a[r]);
+        b[r] = silu_bf16(b[r]);
       }
     }
     if (rope) {
@@ -303,8 +321,8 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   };
 
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int64_t t = t0 + wt * 128 + 32 * u + (lane & 31);
+  for (int u = 0; u < kUB; ++u) {
+    const int64_t t = t0 + wt * kWaveTok + 32 * u + (lane & 31);
     if (t >= M) continue;
     const float2* cs_row =
         rope ? p.rope + static_cast<int64_t>(row_position(p, t)) * half : nullptr;

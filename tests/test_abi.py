@@ -438,3 +438,54 @@ def test_fit_solve_noalloc_validation(lib):
     assert st == SHAPE and "w_enc[2]" in msg
     # a schedule without Reuse layers has nothing to solve and touches no device state
     assert call(_model(is_patch=[1, 1, 1]))[0] == 0
+
+
+def test_fold_and_patch_from_codes_validation(lib):
+    # Every case fails validation, so nothing touches a device (runs without a GPU).
+    m = _model()  # layer 1 is the Patch layer (rank_h 32, d_model 256, D 128)
+    b = _batch()
+    L = m.n_layers
+
+    def fold(model=m, hidden=64, **over):
+        keep, args = [], {}
+        for k, name in enumerate(("w2", "b2", "w_k", "w_v", "b_k", "b_v", "fk", "fv", "ck", "cv")):
+            if name in over:
+                args[name] = over[name]
+            elif name in ("b2", "b_k", "b_v"):
+                args[name] = None
+            else:
+                p, a = _distinct_ptrs(L, k)
+                keep.append(a)
+                args[name] = p
+        st = lib.scd_patch_fold(ctypes.byref(model._c), hidden, *args.values(), None)
+        return st, lib.scd_last_error().decode()
+
+    assert fold(hidden=8)[0] == SHAPE
+    q, keepq = _ptrs(L, skip=(1,))
+    st, msg = fold(w_k=q)
+    assert st == NULL and "w_k[1]" in msg
+    r, keepr = _ptrs(L, value=FAKE + 8)
+    assert fold(b2=r)[0] == ALIGN
+    same, keeps = _ptrs(L)
+    st, msg = fold(fk=same, fv=same)
+    assert st == SHAPE and "share" in msg
+    m2 = _model(is_patch=[1, 1, 0])
+    dup = (ctypes.c_void_p * L)(FAKE, FAKE, FAKE + 4096)
+    st, msg = fold(model=m2, ck=ctypes.cast(dup, ctypes.POINTER(ctypes.c_void_p)))
+    assert st == SHAPE and "c_k[1]" in msg
+    assert fold(model=_model(is_patch=[0, 0, 0]))[0] == OK  # no Patch layer: nothing to fold
+
+    p, keep = _ptrs(L)
+
+    def codes(model=m, batch=b, rope=FAKE, hidden=64, z=p, w1=p, b1=None, fk=p, fv=p, ck=None,
+              cv=None, act=p, kc=p, vc=p):
+        return lib.scd_patch_kv_from_codes(ctypes.byref(model._c), ctypes.byref(batch._c), rope,
+                                           100, hidden, z, w1, b1, fk, fv, ck, cv, act, kc, vc,
+                                           None)
+
+    assert codes(hidden=40) == SHAPE
+    assert codes(fv=q) == NULL and "w_fold_v[1]" in lib.scd_last_error().decode()
+    assert codes(rope=None) == WS
+    assert codes(ck=r) == ALIGN
+    assert codes(model=_model(rank_h=[32, 24, 32])) == SCHED
+    assert codes(z=q, act=q, kc=q, vc=q, batch=_batch(n_tokens=0)) == OK

@@ -116,6 +116,50 @@ def test_fit_solve_matches_oracle(wl, branch):
     U.assert_within(errs, U.TOL[wl.dtype], f"fit_solve {wl.name} {branch}")
 
 
+def _rotate_complex(x, pos, n_heads, head_dim, theta):
+    """RoPE written test-side as multiplication of (x_i + 1j x_{i+d/2}) by exp(1j p theta^(-2i/d))
+    (the rotation itself, not the oracle's code)."""
+    t, half = x.shape[0], head_dim // 2
+    xh = x.reshape(t, n_heads, head_dim)
+    z = xh[..., :half] + 1j * xh[..., half:]
+    freq = theta ** (-2.0 * np.arange(half) / head_dim)
+    zr = z * np.exp(1j * np.outer(np.asarray(pos, np.float64), freq))[:, None, :]
+    return np.concatenate([zr.real, zr.imag], axis=-1).reshape(t, n_heads * head_dim)
+
+
+@pytest.mark.parametrize("wl", [W.FIT_SMALL_BF16, W.FIT_HEAD_SHARED, W.FIT_F32, W.FIT_DH32,
+                                W.FIT_W256_BF16, W.FIT_W64_BF16], ids=lambda w: w.name)
+def test_fit_keys_from_rotated_caches(wl):
+    # Key caches as a model holds them: the shared-latent content rows rotated by each token's
+    # position (test-side), stored once in the model's dtype.  The fit de-rotates them back to the
+    # low-rank content, so the key encoder and decoder are unique and compared directly.
+    dev = torch.device("cuda")
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    L, lam = wl.n_layers, _lam(wl)
+    pos = U.host_positions(wl)
+    R = [l for l in range(L) if not wl.is_patch[l]]
+    a_in, b_in = [None] * L, [None] * L
+    for l in R:
+        a_c, b_c = W.fit_pair(wl, l, "k", "cpu")
+        rot = lambda x: torch.from_numpy(_rotate_complex(U.f64(x), pos, wl.n_kv_heads,  # noqa
+                                                         wl.head_dim, wl.rope_theta))
+        a_in[l] = rot(a_c).to(device=dev, dtype=wl.torch_dtype).contiguous()
+        b_in[l] = rot(b_c).to(device=dev, dtype=wl.torch_dtype).contiguous()
+    rope = scd.scd_rope_table(model, wl.max_position)
+    print(f"[fit rotated keys] {wl.name} lambda={lam}", flush=True)
+    w_enc, w_dec, mu_enc, mu_dec, _, _ = scd.fit_reuse(model, batch, rope, scd.FIT_KEYS, a_in,
+                                                       b_in, lam, center=True)
+    torch.cuda.synchronize()
+    errs = {}
+    for l in R:
+        e_o, d_o, ma_o, mb_o = _oracle_fit(wl, "k", a_in, b_in, l, lam)
+        errs[("w_enc", l)] = U.max_abs_rel(U.f64(w_enc[l]), e_o)
+        errs[("w_dec", l)] = U.max_abs_rel(U.f64(w_dec[l]), d_o)
+        errs[("mu_enc", l)] = U.max_abs_rel(U.f64(mu_enc[l]), ma_o)
+        errs[("mu_dec", l)] = U.max_abs_rel(U.f64(mu_dec[l]), mb_o)
+    U.assert_within(errs, U.TOL[wl.dtype], f"fit rotated keys {wl.name}")
+
+
 def test_fit_solve_on_exact_gram_fp32():
     # The solve alone: the Gram and column sums computed in fp64 on the host (rounded once to
     # fp32), the fit's outputs in fp32 against the oracle's.

@@ -126,11 +126,49 @@ def test_empty_batch_and_reuse_only():
     assert all(c.numel() == 0 for c in out_e["k_cache"])
 
 
-@pytest.mark.parametrize("wl", [W.LLAMA3_8B, W.QWEN2_7B, W.BATCHED, W.LLAMA3_70B,
-                                *W.MODEL_SCALE_EXTRA], ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [W.LLAMA3_8B, W.BATCHED], ids=lambda w: w.name)
+def test_full_size_full_tensors(wl):
+    """The Llama-3-8B-shaped and the batched ragged workloads at full size, launched as the
+    benchmark launches them, compared with the oracle on every token of every layer (streamed
+    layer by layer in chunks of 8192 tokens): caches per tensor, codes per column.  The caches
+    start as NaN with guard rows past the batch: every routed slot must be written once by the
+    Reuse decode or the Patch and no guard row touched."""
+    print(f"case {wl.name}: T={wl.n_tokens} L={wl.n_layers} (full tensors)", flush=True)
+    dev = torch.device("cuda")
+    inp = U.Inputs(wl, dev)
+    rope = _rope_for(wl)
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    T, D, guard = wl.n_tokens, wl.kv_width, 5
+    big_k = [torch.full((T + guard, D), float("nan"), dtype=wl.torch_dtype, device=dev)
+             for _ in range(wl.n_layers)]
+    big_v = [torch.full((T + guard, D), float("nan"), dtype=wl.torch_dtype, device=dev)
+             for _ in range(wl.n_layers)]
+    kc = [b[:T] for b in big_k]
+    vc = [b[:T] for b in big_v]
+    z_k, z_v, z_h = U.alloc_codes(wl, dev)
+    scd.scd_encode(model, batch, rope, inp.k_in, inp.v_in, inp.h_in, inp.w_enc_k, inp.w_enc_v,
+                   inp.w_enc_h, inp.mu_k, inp.mu_v, z_k, z_v, z_h)
+    scd.scd_reuse_decode(model, batch, rope, inp.z_k, inp.z_v, inp.w_dec_k, inp.w_dec_v,
+                         inp.mu_k, inp.mu_v, kc, vc)
+    scd.scd_patch_kv(model, batch, rope, inp.h_hat, inp.w_k, inp.w_v, inp.b_k, inp.b_v, kc, vc)
+    torch.cuda.synchronize()
+    for l in range(wl.n_layers):
+        for big in (big_k[l], big_v[l]):
+            assert int(torch.isnan(big[:T]).sum()) == 0, f"layer {l}: slots left unwritten"
+            assert bool(torch.isnan(big[T:]).all()), f"guard rows of layer {l} were written"
+    out = {"k_cache": kc, "v_cache": vc, "z_k": z_k, "z_v": z_v, "z_h": z_h}
+    errs = U.compare_full_chunked(wl, inp, out, label=wl.name)
+    U.assert_within(errs, U.TOL[wl.dtype], wl.name + " full tensors")
+    del out, inp, big_k, big_v, kc, vc, z_k, z_v, z_h
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("wl", [W.QWEN2_7B, W.LLAMA3_70B, *W.MODEL_SCALE_EXTRA],
+                         ids=lambda w: w.name)
 def test_full_size_sampled(wl):
-    """Full-size configurations, launched exactly as the benchmark launches them; the oracle checks
-    sampled token rows (random rows, request boundaries and tile edges) of every layer."""
+    """The other full-size configurations, launched exactly as the benchmark launches them; the
+    oracle checks sampled token rows (random rows, request boundaries and tile edges) of every
+    layer."""
     print(f"case {wl.name}: T={wl.n_tokens} L={wl.n_layers}", flush=True)
     inp = U.Inputs(wl, "cuda")
     rope = _rope_for(wl)

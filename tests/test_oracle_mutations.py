@@ -21,6 +21,41 @@ _align = O.align
 _silu = O.silu
 _fit_rows = O.fit_rows
 _sign_fix = O.sign_fix
+_payload_bytes = O.payload_bytes
+_fold = O.fold_aligner
+
+
+def payload_patch_term_g(is_patch, n_tokens, n, dh, w, rk, rv, rh, eb):
+    # counts a Patch layer's code as g rows per token, like a Reuse layer's
+    g = n * dh // w
+    offs = [0]
+    for l, p in enumerate(is_patch):
+        m = n_tokens * g * rh[l] if p else n_tokens * g * (rk[l] + rv[l])
+        offs.append(offs[-1] + m * eb)
+    return offs[-1], offs
+
+
+def payload_v_only(is_patch, n_tokens, n, dh, w, rk, rv, rh, eb):
+    # forgets the key codes of Reuse layers
+    return _payload_bytes(is_patch, n_tokens, n, dh, w, [0] * len(rk), rv, rh, eb)
+
+
+def payload_patch_as_reuse(is_patch, n_tokens, n, dh, w, rk, rv, rh, eb):
+    # sends K/V codes for Patch layers too
+    return _payload_bytes([0] * len(is_patch), n_tokens, n, dh, w, rk, rv, rh, eb)
+
+
+def fold_proj_bias_sign(w_p, b_p, w2, b2):
+    # subtracts the projection bias instead of adding it
+    return _fold(w_p, None if b_p is None else -np.asarray(b_p, F64), w2, b2)
+
+
+def fold_bias_dropped(w_p, b_p, w2, b2):
+    return _fold(w_p, b_p, w2, None)
+
+
+def fold_proj_bias_dropped(w_p, b_p, w2, b2):
+    return _fold(w_p, None, w2, b2)
 
 
 def rope_wrong_sign(x, pos, n, dh, theta, inverse=False):
@@ -197,6 +232,12 @@ MUTATIONS = [
     ("fit_reuse", fit_unscaled_latents),
     ("fit_reuse", fit_decoder_without_ridge),
     ("fit_reuse", fit_encoder_on_consumer),
+    ("payload_bytes", payload_patch_term_g),
+    ("payload_bytes", payload_v_only),
+    ("payload_bytes", payload_patch_as_reuse),
+    ("fold_aligner", fold_proj_bias_sign),
+    ("fold_aligner", fold_bias_dropped),
+    ("fold_aligner", fold_proj_bias_dropped),
 ]
 
 PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]

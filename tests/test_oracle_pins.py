@@ -106,13 +106,46 @@ def test_payload_is_linear_in_tokens_and_rank():
     assert twice_t == 2 * base and twice_r == 2 * base
 
 
-def test_paper_table2_payload_accounting():
-    # Table 2 prints raw BF16 and group-INT4 payloads for the same requests; 4-bit storage is a
-    # quarter of 16-bit storage, and SCD sits between Reuse-only and raw.
-    with open(os.path.join(GOLDEN, "table2_payload.json")) as f:
-        t2 = json.load(f)
-    assert round(t2["raw_bf16_mb"] / t2["int4_mb"], 2) == 4.00
-    assert t2["reuse_only_mb"] < t2["scd_mb"] < t2["raw_bf16_mb"]
+def test_payload_equals_the_encoded_code_set():
+    # Algorithm 1 transmits exactly the producer's codes: {Z_K, Z_V} of every Reuse layer and Z_H
+    # of every Patch layer, in layer order, K before V.  Encode a tiny model with the oracle and
+    # lay its actual outputs end to end: their byte sizes must be the payload's offsets, for the
+    # full-width basis and the head-shared one, with Patch layers and ranks that differ by layer
+    # and branch.
+    rng = np.random.default_rng(7)
+    T, H, dh, d, theta = 13, 2, 8, 24, 1e4
+    D = H * dh
+    flags = [0, 1, 0, 0, 1]
+    pos = np.arange(T)
+    for w in (D, dh):
+        g = D // w
+        rk = [int(v) for v in rng.integers(1, w + 1, len(flags))]
+        rv = [int(v) for v in rng.integers(1, w + 1, len(flags))]
+        rh = [int(v) for v in rng.integers(1, d + 1, len(flags))]
+        L = len(flags)
+        k_a = [rng.standard_normal((T, D)) for _ in range(L)]
+        v_a = [rng.standard_normal((T, D)) for _ in range(L)]
+        h_a = [rng.standard_normal((T, d)) for _ in range(L)]
+        e_k = [rng.standard_normal((rk[l], w)) for l in range(L)]
+        e_v = [rng.standard_normal((rv[l], w)) for l in range(L)]
+        e_h = [rng.standard_normal((rh[l], d)) for l in range(L)]
+        z_k, z_v, z_h = O.encode_all(flags, pos, H, dh, theta, k_a, v_a, h_a, e_k, e_v, e_h)
+        sent = []
+        for l in range(L):
+            sent += [z_h[l]] if flags[l] else [z_k[l], z_v[l]]
+        assert all(z is not None for z in sent), "a routed branch produced no code"
+        for eb in (2, 4):
+            total, offs = O.payload_bytes(flags, T, H, dh, w, rk, rv, rh, eb)
+            ends = np.cumsum([0] + [z.size * eb for z in sent])
+            per_layer = [0]
+            i = 0
+            for l in range(L):
+                i += 1 if flags[l] else 2
+                per_layer.append(int(ends[i]))
+            assert offs == per_layer and total == int(ends[-1])
+            assert all(z.shape[0] == (T if flags[l] else T * g)
+                       for l, z in zip([l for l in range(L) for _ in range(1 if flags[l] else 2)],
+                                       sent))
 
 
 # ------------------------------------------------------------------------------------------
@@ -476,6 +509,50 @@ def test_align_linear_limit_and_zero_output_layer():
     w1 = rng.standard_normal((6, r))
     y, _ = O.align(z, w1, rng.standard_normal(6), np.zeros((d, 6)), b2)
     np.testing.assert_array_equal(y, np.tile(b2, (t, 1)))
+
+
+def test_fold_brute_force_and_identity_output_layer():
+    rng = np.random.default_rng(47)
+    D, d, h = 5, 4, 3
+    w_p, b_p = rng.standard_normal((D, d)), rng.standard_normal(D)
+    w2, b2 = rng.standard_normal((d, h)), rng.standard_normal(d)
+    wf, c = O.fold_aligner(w_p, b_p, w2, b2)
+    for n in range(D):
+        for j in range(h):
+            s = 0.0
+            for i in range(d):
+                s += w_p[n, i] * w2[i, j]
+            assert abs(wf[n, j] - s) < 1e-12
+        s = b_p[n]
+        for i in range(d):
+            s += w_p[n, i] * b2[i]
+        assert abs(c[n] - s) < 1e-12
+    # an identity output layer with no bias leaves the projection as it is
+    wf, c = O.fold_aligner(w_p, None, np.eye(d), None)
+    np.testing.assert_array_equal(wf, w_p)
+    np.testing.assert_array_equal(c, np.zeros(D))
+
+
+def test_fold_reproduces_the_literal_aligner_then_patch_chain():
+    # Eq. aligner -> Eq. kv_from_patch through H_hat, against the same maps with the output layer
+    # folded into the projections and applied to the hidden activations directly.
+    rng = np.random.default_rng(53)
+    t, r, hid, d, H, dh, theta = 9, 6, 10, 12, 2, 8, 1e4
+    D = H * dh
+    pos = rng.integers(0, 5000, t)
+    z = rng.standard_normal((t, r))
+    w1, b1 = rng.standard_normal((hid, r)), rng.standard_normal(hid)
+    w2, b2 = rng.standard_normal((d, hid)), rng.standard_normal(d)
+    w_k, b_k = rng.standard_normal((D, d)), rng.standard_normal(D)
+    w_v, b_v = rng.standard_normal((D, d)), rng.standard_normal(D)
+    h_hat, act = O.align(z, w1, b1, w2, b2)
+    k_ref = O.patch_k(h_hat, w_k, b_k, pos, H, dh, theta)
+    v_ref = O.patch_v(h_hat, w_v, b_v)
+    fk, ck = O.fold_aligner(w_k, b_k, w2, b2)
+    fv, cv = O.fold_aligner(w_v, b_v, w2, b2)
+    np.testing.assert_allclose(O.patch_k(act, fk, ck, pos, H, dh, theta), k_ref, rtol=1e-11,
+                               atol=1e-11)
+    np.testing.assert_allclose(O.patch_v(act, fv, cv), v_ref, rtol=1e-11, atol=1e-11)
 
 
 # ------------------------------------------------------------------------------------------
