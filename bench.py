@@ -446,8 +446,9 @@ class Codec:
         self.fold = scd.prepare_patch_fold(self.model, h, w2, b2, inp.w_k, inp.w_v, inp.b_k,
                                            inp.b_v, fk, fv, ck, cv)
         self.folded = (fk, fv, ck, cv)
-        act_buf = torch.empty((T, h), dtype=dt, device=dev) if wl.patch_layers else None
-        self.act = [act_buf if wl.is_patch[l] else None for l in range(L)]
+        # one act buffer per Patch layer: the layers then run as one launch of each product
+        self.act = [torch.empty((T, h), dtype=dt, device=dev) if wl.is_patch[l] else None
+                    for l in range(L)]
         w1 = [a[0] if a is not None else None for a in self.aligner]
         b1 = [a[1] if a is not None else None for a in self.aligner]
         self.enc = scd.prepare_encode(self.model, self.batch, self.rope, inp.k_in, inp.v_in,

@@ -26,10 +26,13 @@ import statistics
 import bench
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
+# kernel-name fragment -> step (first match wins: the aligner's hidden layer inside the Patch step
+# before the unfolded aligner timed beside it)
 PHASES = {"encode_bf16_kernel": "encode", "reuse_decode": "reuse_decode",
-          "patch_kv": "patch_kv", "patch_align": "aligner", "EncodeKV": "encode",
-          "EncodeH": "encode", "ReuseDecode": "reuse_decode", "PatchKV": "patch_kv",
-          "PatchAlign": "aligner", "fit_gram": "fit_gram", "fit_solve": "fit_solve"}
+          "patch_kv": "patch", "patch_align_act": "patch", "patch_align": "aligner",
+          "patch_fold": "fold", "EncodeKV": "encode", "EncodeH": "encode",
+          "ReuseDecode": "reuse_decode", "PatchKV": "patch", "PatchAlign": "patch",
+          "fit_gram": "fit_gram", "fit_solve": "fit_solve"}
 
 
 def phase_of(name: str):
@@ -171,7 +174,8 @@ def main():
             for line in open(args.bench_log):
                 if line.startswith("{"):
                     rec = json.loads(line)
-                    aligner_calls = rec["steps"] + rec["warmup"] if "aligner" in rec else 0
+                    aligner_calls = (rec["steps"] + rec["warmup"]
+                                     if "aligner_unfolded" in rec else 0)
                     break
         tab = kernel_table(args.trace, args.warmup_launches, aligner_calls)
         lines = [f"# Codec kernels, {wl.name} (T={wl.n_tokens}, L={wl.n_layers}, d={wl.d_model}, "
@@ -193,8 +197,10 @@ def main():
                 if line.startswith("{"):
                     rec = json.loads(line)
                     events = rec.get("phase_ms", {})
-                    if "aligner" in rec:  # timed beside the step, with its own figures
-                        al = rec["aligner"]
+                    events = {k: (v["mean"] if isinstance(v, dict) else v)
+                              for k, v in events.items()}
+                    if "aligner_unfolded" in rec:  # timed beside the step, with its own figures
+                        al = rec["aligner_unfolded"]
                         alg["aligner"] = (al["alg_bytes"], al["alg_flops"])
                         events["aligner"] = al["ms_per_call"]
                     break
@@ -231,7 +237,7 @@ def main():
         fs, ws = calibration(frows, true_bytes), calibration(wrows, true_bytes)
         fb, wb = per_phase_bytes(frows, fs), per_phase_bytes(wrows, ws)
         steps = {}
-        for ph in ("encode", "reuse_decode", "patch_kv"):
+        for ph in bench.PHASES:
             if ph in fb and ph in wb:
                 tot = fb[ph] + wb[ph]
                 steps[ph] = {"fetch_bytes": round(fb[ph]), "write_bytes": round(wb[ph]),
@@ -282,8 +288,10 @@ def write_mfma(args, wl, alg, digest):
         lines.append(f"| `{r['kernel']}` | {r['phase']} | {r['grid']} | {r['us']:.1f} | "
                      f"{r['gflop']:.1f} | {r['busy']:.3f} | {r['ghz']:.2f} | {frac:.3f} | "
                      f"{frac_clk:.3f} | {r['wait']:.2f} | {r['valu']:.2f} |")
-    if "patch_kv" in alg:
-        lines += ["", f"Algorithmic Patch flops per call: {alg['patch_kv'][1] / 1e9:.1f} GFLOP."]
+    if "patch" in alg:
+        lines += ["", f"Algorithmic Patch flops per call: {alg['patch'][1] / 1e9:.1f} GFLOP "
+                  f"(hidden layer {alg['patch_act'][1] / 1e9:.1f}, folded product "
+                  f"{alg['patch_gemm'][1] / 1e9:.1f})."]
     path = os.path.join(ROOT, "profiles", f"mfma_{wl.name}.md")
     open(path, "w").write("\n".join(lines) + "\n")
     print("wrote", path)

@@ -609,35 +609,37 @@ namespace {
 
 // The aligner's first product act = SiLU(z_h w1^T + b1) for `jobs` (one per Patch layer, K = r_H).
 // It is a short contraction whose time is writing act: the shape of a Reuse decode (code x basis
-// + offset), so the bf16 decode kernel takes it when it can (r_H <= 128, r_H % 32 == 0); else the
-// bf16 GEMM body when `fast` (r_H % 64 == 0 and hidden % 128 == 0), else the generic kernel.
-// *on_decode reports whether the decode kernel took it.
+// + offset), so the bf16 decode kernel takes every job it can (r_H % 32 == 0, r_H <= 256), one
+// launch per rank; the other jobs take the bf16 GEMM body when `fast` (r_H % 64 == 0 and
+// hidden % 128 == 0), else the generic kernel.
 scd_status_t enqueue_align_first(const scd_model_t* model, const scd_batch_t* batch, int hidden,
                                  const std::vector<scd::GemmJob>& jobs, bool fast,
-                                 bool* on_decode, hipStream_t stream) {
+                                 hipStream_t stream) {
   const scd::GemmParams base = base_params(model, batch, batch->n_tokens, 1, nullptr, 0);
-  bool decode_first = model->dtype == SCD_BF16 && hidden % 128 == 0 &&
-                      (model->head_dim == 64 || model->head_dim == 128) &&
-                      batch->n_seqs <= scd::kMaxLdsSeqs;
+  const bool decode_ok = model->dtype == SCD_BF16 && hidden % 128 == 0 &&
+                         (model->head_dim == 64 || model->head_dim == 128) &&
+                         batch->n_seqs <= scd::kMaxLdsSeqs;
+  std::vector<scd::GemmJob> on_decode, rest;
   for (const auto& j : jobs)
-    if (j.k % 32 != 0 || j.k > 128) decode_first = false;
-  *on_decode = decode_first;
-  if (decode_first) {
-    for (const auto& grp : group_by(jobs, [](const scd::GemmJob& j) { return j.k; })) {
-      const int nhg = scd::decode_channel_groups(grp[0].k, hidden);
-      JobPacker jp(base, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
-      for (const auto& j : grp) jp.add(j);
-      for (const auto& lp : jp.build()) {
-        const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream, true);
-        if (e != hipSuccess)
-          return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
-      }
+    (decode_ok && j.k % 32 == 0 && j.k <= 256 ? on_decode : rest).push_back(j);
+  for (const auto& grp : group_by(on_decode, [](const scd::GemmJob& j) { return j.k; })) {
+    const int nhg = scd::decode_channel_groups(grp[0].k, hidden);
+    JobPacker jp(base, scd::decode_tile_rows(nhg, grp[0].k), 128 * nhg);
+    for (const auto& j : grp) jp.add(j);
+    for (const auto& lp : jp.build()) {
+      const hipError_t e = scd::launch_decode_bf16(nhg, lp, stream, true);
+      if (e != hipSuccess)
+        return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
     }
-    return ok();
   }
-  JobPacker jp(base, fast ? scd::kPatchBM : scd::kGenericBM, fast ? scd::kPatchBN : scd::kGenericBN);
-  for (const auto& j : jobs) jp.add(j);
-  if (!fast) return run(scd::Op::kPatchAlign, jp.build(), model->dtype, stream);
+  if (rest.empty()) return ok();
+  bool gemm_ok = fast;
+  for (const auto& j : rest)
+    if (j.k % 64 != 0) gemm_ok = false;
+  JobPacker jp(base, gemm_ok ? scd::kPatchBM : scd::kGenericBM,
+               gemm_ok ? scd::kPatchBN : scd::kGenericBN);
+  for (const auto& j : rest) jp.add(j);
+  if (!gemm_ok) return run(scd::Op::kPatchAlign, jp.build(), model->dtype, stream);
   for (const auto& p : jp.build()) {
     const hipError_t e = scd::launch_align_bf16(p, stream);
     if (e != hipSuccess) return fail(SCD_ERR_HIP, "aligner launch failed: %s", hipGetErrorString(e));
@@ -709,9 +711,8 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
   const int rh_max = model->d_model < 256 ? model->d_model : 256;
   bool any = false;
   // The second product (K = hidden) takes the bf16 GEMM body whenever the widths allow; the first
-  // (K = r_H) needs r_H % 64 == 0 there, unless the decode body takes it (below).
+  // (K = r_H) goes where enqueue_align_first sends it.
   const bool fast2 = model->dtype == SCD_BF16 && hidden % 128 == 0 && model->d_model % 128 == 0;
-  bool fast1 = fast2;
   std::vector<const void*> acts;
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
@@ -732,7 +733,6 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
           return fail(SCD_ERR_SHAPE, "act[%d] repeats an earlier Patch layer's buffer", l);
       acts.push_back(act[l]);
     }
-    if (model->rank_h[l] % 64 != 0) fast1 = false;
   }
   if (!any || batch->n_tokens == 0) return ok();
 
@@ -749,8 +749,8 @@ scd_status_t scd_patch_align(const scd_model_t* model, const scd_batch_t* batch,
                           scd::kVecOut | scd::kSiluOut, 0});
     second.add({act[l], w2[l], h_hat[l], b2 ? b2[l] : nullptr, d, hidden, scd::kVecOut, 0});
   }
-  bool on_decode = false;
-  SCD_TRY(enqueue_align_first(model, batch, hidden, first_jobs, fast1, &on_decode, stream));
+  SCD_TRY(enqueue_align_first(model, batch, hidden, first_jobs,
+                              model->dtype == SCD_BF16 && hidden % 128 == 0, stream));
   if (!fast2) return run(scd::Op::kPatchAlign, second.build(), model->dtype, stream);
   for (const auto& p : second.build()) {
     const hipError_t e = scd::launch_align_bf16(p, stream);
@@ -835,7 +835,7 @@ scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t
     return fail(SCD_ERR_SHAPE, "aligner width %d must be a positive multiple of 16", hidden);
   const int rh_max = model->d_model < 256 ? model->d_model : 256;
   const int64_t T = batch->n_tokens;
-  bool any = false, rh64 = true;
+  bool any = false;
   for (int l = 0; l < model->n_layers; ++l) {
     if (!model->is_patch[l]) continue;
     any = true;
@@ -851,13 +851,12 @@ scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t
     SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(act), l, "act", T));
     SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(k_cache), l, "k_cache", T));
     SCD_TRY(need_tok_ptr(reinterpret_cast<const void* const*>(v_cache), l, "v_cache", T));
-    if (model->rank_h[l] % 64 != 0) rh64 = false;
   }
   if (any && T > 0) SCD_TRY(check_rope(rope_table, max_position));
   if (!any || T == 0) return ok();
 
   const int D = static_cast<int>(kv_width(model));
-  const bool fast_first = model->dtype == SCD_BF16 && hidden % 128 == 0 && rh64;
+  const bool fast_first = model->dtype == SCD_BF16 && hidden % 128 == 0;
   const bool fast = model->dtype == SCD_BF16 && hidden % 64 == 0 &&
                     (model->head_dim == 64 || model->head_dim == 128) && D % 128 == 0;
   const scd::GemmParams base = base_params(model, batch, T, 1, rope_table, max_position);
@@ -885,8 +884,7 @@ scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t
               scd::kRopeOut | scd::kVecOut, 0});
       jp.add({act[l], w_fold_v[l], v_cache[l], c_v ? c_v[l] : nullptr, D, hidden, scd::kVecOut, 0});
     }
-    bool on_decode = false;
-    SCD_TRY(enqueue_align_first(model, batch, hidden, first, fast_first, &on_decode, stream));
+    SCD_TRY(enqueue_align_first(model, batch, hidden, first, fast_first, stream));
     if (!fast) {
       SCD_TRY(run(scd::Op::kPatchKV, jp.build(), model->dtype, stream));
       continue;

@@ -281,10 +281,18 @@ hipError_t launch_align_kch(int kch, const GemmParams& p, int grid_size, size_t 
                        dim3(64 * waves_for(NHG, KC)), lds, stream, p);                        \
     return hipGetLastError();
     SCD_ALIGN_CASE(1) SCD_ALIGN_CASE(2) SCD_ALIGN_CASE(3) SCD_ALIGN_CASE(4)
-#undef SCD_ALIGN_CASE
     default:
       break;
   }
+  // ranks above 128 use at most two channel groups per workgroup (decode_channel_groups)
+  if constexpr (NHG <= 2) {
+    switch (kch) {
+      SCD_ALIGN_CASE(5) SCD_ALIGN_CASE(6) SCD_ALIGN_CASE(7) SCD_ALIGN_CASE(8)
+      default:
+        break;
+    }
+  }
+#undef SCD_ALIGN_CASE
   return hipErrorInvalidValue;
 }
 
@@ -385,7 +393,7 @@ hipError_t launch_decode_bf16(int nhg, const GemmParams& p, hipStream_t stream, 
   int64_t shares = static_cast<int64_t>(cus) * per_cu / n_nc;
   shares = shares < 1 ? 1 : (shares > row_tiles ? row_tiles : shares);
   const int grid_size = static_cast<int>(shares * n_nc);
-  if (align && (rope || kch > 4)) return hipErrorInvalidValue;
+  if (align && rope) return hipErrorInvalidValue;
 #define SCD_DECODE_DISPATCH(NHG, DH)                                                    \
   if (nhg == NHG && p.head_dim == DH)                                                   \
     return align  ? launch_align_kch<NHG, DH>(kch, p, grid_size, lds, stream)           \

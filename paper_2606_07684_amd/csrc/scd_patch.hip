@@ -1,24 +1,31 @@
 // Patch KV regeneration (Section 4.4.2, Eq. kv_from_patch) as a bf16 MFMA GEMM for gfx950:
 //   K = RoPE(H_hat W_K^T + b_K),  V = H_hat W_V^T + b_V   written straight into the KV cache.
+// The same body regenerates a Patch layer from the aligner's hidden activations through the folded
+// projections (act W_fold^T + c) and runs the aligner's own products.
 //
 // One workgroup computes a 256 (channels n) x 256 (tokens t) tile of C^T = W * H_hat^T with four
 // waves, each owning 128 channels x 128 tokens as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.
 // The weight tile is the MFMA A operand, so an accumulator register holds one token's channels;
 // weight rows are placed in LDS in a permuted order that gives each lane 16 consecutive channels
 // of one token.  A wave's 128 channels are whole heads, so every RoPE pair (i, i + d_h/2) meets in
-// one lane and the epilogue needs no LDS: bias, rotation and bf16 rounding happen in registers and
-// each lane stores two 16-byte vectors per block.
+// one lane: bias, rotation and bf16 rounding happen in registers and each lane stores two 16-byte
+// vectors per block.
 //
 // K advances 64 at a time.  An operand tile of one 64-wide step (256 rows x 64 bf16 = 32 KiB, its
 // 16-byte chunks XOR-swizzled so MFMA operand reads are conflict-free) fills one slot of a ring of
 // five, the whole 160 KiB of LDS.  Both operand tiles travel global -> LDS directly
 // (buffer_load_dwordx4 ... lds), eight lanes of a copy instruction reading one row's whole 128-byte
 // line.  Each step is four 16-wide k-slices; the workgroup barrier sits before the last one, so
-// the operand reads of the next step's first slice run under MFMAs, and right after it the two
-// slots the current step has released receive the weight tile of step k + 2 and the token tile of
-// step k + 3.  Token tiles, the operand that misses L2 more often, thus get two steps of MFMAs to
-// land and weight tiles one; five slots hold one and a half steps of copies in flight, against
-// one for a ring of two whole steps.
+// the operand reads of the next step's first slice run under MFMAs.  The copies are spread over
+// the whole step, a few between MFMAs: the token tile of step k + 2 over the first three slices
+// (into the slot the previous barrier released) and the weight tile of step k + 2 over the last
+// (into the slot this step's barrier released).  Issued in one burst, the 64 copies of a step
+// (64 KiB per CU) queue behind the texture path for about as long as the burst of MFMAs they sit
+// between, and each stalled copy holds up the MFMAs behind it in the wave's instruction stream.
+//
+// The epilogue first stages the tile's RoPE factors (256 tokens x d_h/2 pairs, fp32) and bias in
+// the then free LDS, so its stores never queue behind global loads (on this part loads and stores
+// share one counter: a load issued after stores can only be waited for together with them).
 #include "scd_device.h"
 
 namespace scd {
@@ -33,17 +40,14 @@ constexpr int kLDK = kBK;                   // LDS row (bf16 elements): 8 16-byt
 constexpr int kChunks = kBK / 8;
 constexpr int kSlot = kBN * kLDK;           // elements per ring slot (one operand tile of a step)
 constexpr int kRing = 5;                    // slots
-#ifndef SCD_PATCH_WAVES
-#define SCD_PATCH_WAVES 4
-#endif
-constexpr int kWaves = SCD_PATCH_WAVES;     // 4: one wave per SIMD; 8: two
+constexpr int kWaves = 4;                   // one wave per SIMD
 constexpr int kThreads = 64 * kWaves;
 constexpr int kDmaIters = kBN * kChunks / kThreads;  // copy instructions per wave per operand tile
-constexpr int kDmaPerStage = 2 * kDmaIters;          // ... per step (both operands)
-constexpr int kWaveTok = 256 * 2 / kWaves;  // tokens per wave (each wave owns 128 channels)
+constexpr int kWaveTok = 128;               // tokens per wave (each wave owns 128 channels)
 constexpr int kUB = kWaveTok / 32;          // 32-token MFMA blocks per wave
 static_assert(kBN == kBM, "square tiles: both operand tiles fill one slot");
 static_assert(kRing * kSlot * 2 <= 160 * 1024, "LDS");
+static_assert(kBM * 32 * 16 + kBN * 2 <= kRing * kSlot * 2, "epilogue staging fits the ring");
 // Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data format, no swizzle.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -60,40 +64,32 @@ constexpr int vmcnt_imm(int n, bool lds_done = false) {
 }
 constexpr int kLgkmDone = 0xF | (0x3 << 14) | (0x7 << 4);
 
-// Scheduling groups for one block of 16 MFMAs and 8 LDS reads that do not feed them: one read
-// after each of the first eight MFMAs.  interleave_reads_dma also spreads the stage's LDS-DMA
-// copies over the last eight MFMAs (the compiler cannot tell that the copies and the reads touch
-// different LDS buffers, so it keeps them in program order: reads first).
+// Scheduling groups for one slice of 16 MFMAs: after each of the first eight MFMAs one LDS read
+// (operands of the next slice, which do not feed these MFMAs), then up to eight copies, one per
+// MFMA.  (The compiler cannot tell that the copies and the reads touch different LDS slots, so it
+// keeps them in program order: reads first.)
 #define SCD_MFMA_THEN_READ                          \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
   __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-#define SCD_MFMA_THEN_DMA(n)                         \
+#define SCD_MFMA_THEN_COPY                           \
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x020, n, 0);
-__device__ __forceinline__ void interleave_reads() {
-  if constexpr (kWaves == 4) {  // 16 MFMAs, 8 reads
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  } else {  // 8 MFMAs, 6 reads
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-  }
+  __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+template <int C>
+__device__ __forceinline__ void interleave_reads_copies() {
+  static_assert(C >= 0 && C <= 8, "at most one copy per MFMA of the second half");
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
+  if constexpr (C >= 1) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 2) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 3) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 4) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 5) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 6) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 7) { SCD_MFMA_THEN_COPY }
+  if constexpr (C >= 8) { SCD_MFMA_THEN_COPY }
+  if constexpr (C < 8) __builtin_amdgcn_sched_group_barrier(0x008, 8 - C, 0);
 }
-__device__ __forceinline__ void interleave_reads_dma() {
-  if constexpr (kWaves == 4) {  // 16 MFMAs, 8 reads, 16 copies
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2)
-    SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2) SCD_MFMA_THEN_DMA(2)
-  } else {  // 8 MFMAs, 6 reads, 8 copies
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-    SCD_MFMA_THEN_DMA(4) SCD_MFMA_THEN_DMA(4)
-  }
-}
-#undef SCD_MFMA_THEN_DMA
+#undef SCD_MFMA_THEN_COPY
 #undef SCD_MFMA_THEN_READ
 
 // The product C = A B^T of one launch (both operands row-major with the contraction contiguous,
@@ -104,7 +100,7 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wn = wave / (kWaves / 2), wt = wave % (kWaves / 2);  // channel half, token part
+  const int wn = wave >> 1, wt = wave & 1;  // channel half, token half
 
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
   const GemmJob job = p.jobs[job_of(p, unit)];
@@ -142,15 +138,17 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
     hoff[j] = static_cast<uint32_t>((t * K + 8 * c) * 2);
   }
   constexpr bool kTokens = true, kWeights = false;
-  auto copy_tile = [&](bool tokens, int kc, int slot) {
+  // copies j0 .. j1-1 of an operand tile (the whole tile is 0 .. kDmaIters-1)
+  auto copy_part = [&](bool tokens, int kc, int slot, int j0, int j1) {
     uint16_t* dst = smem + slot * kSlot;
     const int kb = kc * kBK * 2;
 #pragma unroll
-    for (int j = 0; j < kDmaIters; ++j)
+    for (int j = j0; j < j1; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(tokens ? hres : wres,
                                                (lds_void_t)(dst + 8 * ((kWaves * j + wave) * 64)), 16,
                                                tokens ? hoff[j] : woff[j], kb, 0, 0);
   };
+  auto copy_tile = [&](bool tokens, int kc, int slot) { copy_part(tokens, kc, slot, 0, kDmaIters); };
 
   f32x16 acc[4][kUB];
 #pragma unroll
@@ -188,63 +186,67 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   // discarded look-ahead of the final step), so every step issues the same number of copies and
   // one vmcnt threshold holds throughout.
   auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
+  // Copies in issue order: T0 W0 T1 W1 T2 W2 ...; the i-th goes to slot i mod 5.  Step kc spreads
+  // the copies of token tile kc + 2 over its first three slices (into the slot of weight tile
+  // kc - 1, released at the previous barrier) and issues weight tile kc + 2 in its last slice
+  // (into the slot of token tile kc, released at its own barrier).  At the barrier of step kc
+  // only token tile kc + 2 may still be in flight.  A step index past the end re-copies the last
+  // step into a slot that is never read for data, so every step issues the same copies and one
+  // counter threshold holds throughout.
+  constexpr int kC0 = (kDmaIters + 2) / 3, kC1 = (kDmaIters + 1) / 3;
   copy_tile(kTokens, 0, 0);
   copy_tile(kWeights, 0, 1);
   copy_tile(kTokens, clamp(1), 2);
   copy_tile(kWeights, clamp(1), 3);
-  copy_tile(kTokens, clamp(2), 4);
-  // step 0's two tiles have landed once at most the last three copies are pending
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * kDmaIters, true));
+  // step 0's two tiles have landed once at most the last two copies are pending
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kDmaIters, true));
   lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
   const uint16_t* hrow = smem + (wt * kWaveTok + lr) * kLDK;
   bf16x8 a0[4], b0[kUB], a1[4], b1[kUB];
-  int sh = 0, sw = 1;        // slots of step kc's token and weight tiles
+  int sh = 0, sw = 1, sfree = 4;  // slots of step kc's token and weight tiles; slot for T(kc+2)
   frags(wrow + sw * kSlot, hrow + sh * kSlot, 0, a0, b0);
   for (int kc = 0; kc < nk; ++kc) {
     const int next_h = sh + 2 >= kRing ? sh + 2 - kRing : sh + 2;
     const int next_w = sw + 2 >= kRing ? sw + 2 - kRing : sw + 2;
     const uint16_t* wb = wrow + sw * kSlot;
     const uint16_t* hb = hrow + sh * kSlot;
-    // Slice 0's operands were read between the previous MFMAs; retiring them here keeps the waits
-    // inside this block from covering the reads it issues itself.
+    const int tk = clamp(kc + 2);
     __builtin_amdgcn_s_waitcnt(kLgkmDone);
     __builtin_amdgcn_sched_barrier(0);
-    // The first three slices' MFMAs, each with the next slice's reads between them.
     mma(a0, b0);
     frags(wb, hb, 1, a1, b1);
-    interleave_reads();
+    copy_part(kTokens, tk, sfree, 0, kC0);
+    interleave_reads_copies<kC0>();
     __builtin_amdgcn_sched_barrier(0);
     mma(a1, b1);
     frags(wb, hb, 2, a0, b0);
-    interleave_reads();
+    copy_part(kTokens, tk, sfree, kC0, kC0 + kC1);
+    interleave_reads_copies<kC1>();
     __builtin_amdgcn_sched_barrier(0);
     mma(a0, b0);
     frags(wb, hb, 3, a1, b1);
-    interleave_reads();
+    copy_part(kTokens, tk, sfree, kC0 + kC1, kDmaIters);
+    interleave_reads_copies<kDmaIters - kC0 - kC1>();
     __builtin_amdgcn_sched_barrier(0);
-    // Step kc + 1's tiles have landed for this wave once at most the last copy (the token tile
-    // of step kc + 2) is pending, and its reads of step kc are complete once no LDS access is
-    // pending; the barrier makes both true for every wave.  (A plain s_barrier: a fenced one would
-    // wait for every copy in flight.)
+    // Step kc + 1's tiles have landed once at most token tile kc + 2's copies are pending.
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaIters, true));
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // The last slice's MFMAs, with the next step's slice-0 reads and then the two copies into the
-    // slots step kc has released (every wave's reads of them completed before the barrier).
     mma(a1, b1);
     frags(wrow + next_w * kSlot, hrow + next_h * kSlot, 0, a0, b0);
     copy_tile(kWeights, clamp(kc + 2), sh);
-    copy_tile(kTokens, clamp(kc + 3), sw);
-    interleave_reads_dma();
+    interleave_reads_copies<kDmaIters>();
     __builtin_amdgcn_sched_barrier(0);
+    sfree = sw;
     sh = next_h;
     sw = next_w;
   }
-  // drain the look-ahead copies before the workgroup's LDS is released
+  // drain the look-ahead copies and every wave's operand reads: the ring is free from here on
   wait_vmem();
+  lds_barrier();
 
-  // Epilogue.  Lane l holds, for block (s, u), token t0 + wt*128 + 32u + l%32 and channels
+  // Epilogue.  Lane l holds, for block (s, u), token t0 + wt*kWaveTok + 32u + l%32 and channels
   // n0 + wn*128 + 32s + 16*(l/32) + r, r = 0..15.
   const bool rope = (job.flags & kRopeOut) != 0;
   const bool silu = (job.flags & kSiluOut) != 0;
@@ -257,9 +259,36 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   const int nw = n0 + wn * 128;
   const int hl = 16 * (lane >> 5);
 
+  // The tile's RoPE factors and bias are staged in the (now free) LDS first, so the epilogue's
+  // stores never wait behind global loads.  Factors: 16-byte chunk c (pairs 2c, 2c + 1) of token
+  // r's table row at byte (c * 256 + r) * 16, so the lanes of a read (consecutive tokens) hit
+  // consecutive chunks; one DMA instruction fills 64 consecutive chunk slots, and a lane always
+  // fetches the same token (its row position is looked up once).  Bias: 256 bf16 after them.
+  unsigned char* stage = reinterpret_cast<unsigned char*>(smem);
+  uint16_t* sbias = reinterpret_cast<uint16_t*>(stage + kBM * 32 * 16);
+  if (rope) {
+    const int nchunk = half / 2;  // chunks per token row
+    const int r = ((wave % (kBM / 64)) * 64) + lane;
+    const int64_t tr = t0 + r < M ? t0 + r : M - 1;
+    const float2* src = p.rope + static_cast<int64_t>(row_position(p, tr)) * half;
+    for (int j = 0; j < nchunk * kBM / (64 * kWaves); ++j) {
+      const int slot = (j * kWaves + wave) * 64;  // first chunk slot of this instruction
+      const int c = slot / kBM;
+      __builtin_amdgcn_global_load_lds(src + 2 * c, (lds_void_t)(stage + 16 * slot), 16, 0, 0);
+    }
+  }
+  if (add_vec && tid < kBN / 8) {
+    const int nb = n0 + 8 * tid;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (nb < N) v = *reinterpret_cast<const uint4*>(bias + nb);
+    *reinterpret_cast<uint4*>(sbias + 8 * tid) = v;
+  }
+  wait_vmem();
+  lds_barrier();
+
   auto load16 = [&](int nb, float* v) {
-    if (add_vec && nb < N) {
-      const uint4* src = reinterpret_cast<const uint4*>(bias + nb);
+    if (add_vec) {
+      const uint4* src = reinterpret_cast<const uint4*>(sbias + (nb - n0));
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const uint4 x = src[h];
@@ -286,8 +315,8 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   };
 
   // One pair of blocks (S, S + PS) holds channels (i, i + d_h/2); S and PS are compile-time so the
-  // accumulators stay in registers.
-  auto finish_pair = [&](auto s_c, auto ps_c, int u, int64_t t, const float2* cs_row) {
+  // accumulators stay in registers.  rl is the token's row within the tile.
+  auto finish_pair = [&](auto s_c, auto ps_c, int u, int64_t t, int rl) {
     constexpr int S = decltype(s_c)::value;
     constexpr int SP = S + decltype(ps_c)::value;
     const int nb = nw + 32 * S + hl, nbp = nw + 32 * SP + hl;
@@ -307,13 +336,15 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
       }
     }
     if (rope) {
-      const int i0 = (32 * S + hl) & (half - 1);  // pair index of channel r = 0
+      const int c0 = ((32 * S + hl) & (half - 1)) >> 1;  // chunk of the pair of channel r = 0
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float2 c = cs_row[i0 + r];
-        const float x = a[r], y = b[r];
-        a[r] = x * c.x - y * c.y;
-        b[r] = y * c.x + x * c.y;
+      for (int q = 0; q < 8; ++q) {
+        const float4 cs = *reinterpret_cast<const float4*>(stage + ((c0 + q) * kBM + rl) * 16);
+        const float x0 = a[2 * q], y0 = b[2 * q], x1 = a[2 * q + 1], y1 = b[2 * q + 1];
+        a[2 * q] = x0 * cs.x - y0 * cs.y;
+        b[2 * q] = y0 * cs.x + x0 * cs.y;
+        a[2 * q + 1] = x1 * cs.z - y1 * cs.w;
+        b[2 * q + 1] = y1 * cs.z + x1 * cs.w;
       }
     }
     store16(t, nb, a);
@@ -322,16 +353,15 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
 
 #pragma unroll
   for (int u = 0; u < kUB; ++u) {
-    const int64_t t = t0 + wt * kWaveTok + 32 * u + (lane & 31);
+    const int rl = wt * kWaveTok + 32 * u + (lane & 31);
+    const int64_t t = t0 + rl;
     if (t >= M) continue;
-    const float2* cs_row =
-        rope ? p.rope + static_cast<int64_t>(row_position(p, t)) * half : nullptr;
     if (pstride == 2) {
-      finish_pair(IntC<0>{}, IntC<2>{}, u, t, cs_row);
-      finish_pair(IntC<1>{}, IntC<2>{}, u, t, cs_row);
+      finish_pair(IntC<0>{}, IntC<2>{}, u, t, rl);
+      finish_pair(IntC<1>{}, IntC<2>{}, u, t, rl);
     } else {
-      finish_pair(IntC<0>{}, IntC<1>{}, u, t, cs_row);
-      finish_pair(IntC<2>{}, IntC<1>{}, u, t, cs_row);
+      finish_pair(IntC<0>{}, IntC<1>{}, u, t, rl);
+      finish_pair(IntC<2>{}, IntC<1>{}, u, t, rl);
     }
   }
 }

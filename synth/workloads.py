@@ -196,6 +196,11 @@ SMALL_RING7 = Workload("small_ring7_bf16", 2, 448, 2, 64, (257,), (32, 64), (1,)
 SMALL_ALIGN_RING = Workload("small_align_ring_bf16", 2, 256, 2, 64, (300,), (64, 192), (0, 1),
                             1e4, "bf16", aligner_hidden=640)
 
+# More requests than the decode body stages in LDS with a Patch code of rank 64: the aligner's
+# first product takes the bf16 GEMM body.
+SMALL_MANY_REQUESTS_ALIGN = SMALL_MANY_REQUESTS.replace(name="small_many_requests_align_bf16",
+                                                        ranks=(64, 64), aligner_hidden=256)
+
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
                   SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS, SMALL_RING5,
                   SMALL_RING7, SMALL_ALIGN_RING)

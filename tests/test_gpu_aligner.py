@@ -55,7 +55,8 @@ def _compare(wl, inp, act, hh, tokens):
     return errs
 
 
-@pytest.mark.parametrize("wl", [W.SMALL_ALIGN, W.SMALL_BF16, W.SMALL_F32, W.SMALL_ALIGN_RING],
+@pytest.mark.parametrize("wl", [W.SMALL_ALIGN, W.SMALL_BF16, W.SMALL_F32, W.SMALL_ALIGN_RING,
+                                W.SMALL_MANY_REQUESTS_ALIGN],
                          ids=lambda w: w.name)
 def test_aligner_matches_oracle(wl):
     inp, act, hh = _run(wl, fill=float("nan"))

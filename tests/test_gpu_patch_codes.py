@@ -23,7 +23,7 @@ from tests import parity_util as U
 pytestmark = pytest.mark.gpu
 
 SMALL = [W.SMALL_ALIGN, W.SMALL_ALIGN_RING, W.SMALL_F32, W.SMALL_RING5, W.SMALL_HEAD_SHARED,
-         W.SMALL_DEGENERATE, W.SMALL_BF16]
+         W.SMALL_DEGENERATE, W.SMALL_BF16, W.SMALL_MANY_REQUESTS_ALIGN]
 
 
 @pytest.fixture(scope="module", autouse=True)
