@@ -139,6 +139,108 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) accm[i][e] = 0.f;
 
+  // One chunk's MFMAs for input registers x (8 loads of this lane's row) against weight buffer buf.
+  // Each weight fragment of k-step s + 1 (and the offset's) is read into the register its MFMA of
+  // step s has just consumed, one read after each MFMA, so each LDS read has most of a step of
+  // MFMAs to land instead of stalling the MFMA that needs it, with no second register set.
+  // B operands come in (first half, second half) pairs: deRoPE in fp32 and one bf16 rounding
+  // (keys), or the loaded values themselves.  Both operands visit the chunk's columns in the same
+  // order, so the contraction is unchanged.  Every wave computes kMuBlocks offset blocks (blocks
+  // past RB repeat block 0 and are never used), so every step has the same instructions.
+  // The read-ahead keeps a step's fragments live across the next step's deRoPE; the key kernels
+  // with four or more code blocks would then need more than half a SIMD's registers and drop to one
+  // wave per SIMD, which costs more than the reads' latency (the second wave hides it), so they
+  // read each step's fragments right before its MFMAs.
+  constexpr bool kReadAhead = !(DEROPE && RB >= 4);
+  constexpr int kStepMfma = RB + (MU ? kMuBlocks : 0);
+  constexpr int kStepReads = RB + (MU ? kMuBlocks + 1 : 0);
+  constexpr int kPairs = kStepMfma < kStepReads ? kStepMfma : kStepReads;
+  auto compute_chunk = [&](int c, int buf, const uint4* x) {
+    const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
+    bf16x8 f[RB], m[kMuBlocks], mu;
+    auto read_step = [&](int s) {
+      const int col = chunk_col<DH>(s, h, derope);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) f[b] = efrag(eb, b, col);
+      if constexpr (MU) {
+#pragma unroll
+        for (int i = 0; i < kMuBlocks; ++i) {
+          const int b = wave + 4 * i;
+          m[i] = efrag(eb, b < RB ? b : 0, col);
+        }
+        mu = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + col);
+      }
+    };
+    if constexpr (kReadAhead) read_step(0);
+    bf16x8 bu, bv;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      if ((s & 1) == 0) {
+        if constexpr (DEROPE) {
+          float u[8], v[8];
+          unpack8(x[s], u);
+          unpack8(x[s + 1], v);
+          constexpr int spH = DH / 16;
+          const int o = (s % spH) >> 1;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float cc = cs_c[o][e], sn = cs_s[o][e];
+            const float a = u[e], b = v[e];
+            u[e] = a * cc + b * sn;
+            v[e] = b * cc - a * sn;
+          }
+          bu = __builtin_bit_cast(bf16x8, pack8(u));
+          bv = __builtin_bit_cast(bf16x8, pack8(v));
+        } else {
+          bu = __builtin_bit_cast(bf16x8, x[s]);
+          bv = __builtin_bit_cast(bf16x8, x[s + 1]);
+        }
+      }
+      const bf16x8 bx = (s & 1) ? bv : bu;
+      if constexpr (!kReadAhead) {
+        // each fragment read right before its MFMA (short-lived registers)
+        const int col = chunk_col<DH>(s, h, derope);
+#pragma unroll
+        for (int b = 0; b < RB; ++b)
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(efrag(eb, b, col), bx, acc[b], 0, 0, 0);
+        if constexpr (MU) {
+          const bf16x8 mu_s = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + col);
+#pragma unroll
+          for (int i = 0; i < kMuBlocks; ++i) {
+            const int b = wave + 4 * i;
+            if (b < RB)
+              accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(efrag(eb, b, col), mu_s, accm[i],
+                                                                0, 0, 0);
+          }
+        }
+        continue;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int b = 0; b < RB; ++b)
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[b], bx, acc[b], 0, 0, 0);
+      if constexpr (MU) {
+        // E mu for this wave's offset blocks: mu (same columns as the inputs) in every B column
+#pragma unroll
+        for (int i = 0; i < kMuBlocks; ++i)
+          accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(m[i], mu, accm[i], 0, 0, 0);
+      }
+      if (kReadAhead && s + 1 < 8) {
+        read_step(s + 1);
+#pragma unroll
+        for (int i = 0; i < kPairs; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        if constexpr (kStepMfma > kPairs)
+          __builtin_amdgcn_sched_group_barrier(0x008, kStepMfma - kPairs, 0);
+        if constexpr (kStepReads > kPairs)
+          __builtin_amdgcn_sched_group_barrier(0x100, kStepReads - kPairs, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
   if constexpr (DEPTH == 1) {
   uint4 xc[8], xn[8];
   stage_weights(0, 0);
@@ -152,58 +254,7 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       stage_weights(c + 1, buf ^ 1);
       load_x(c + 1, xn);
     }
-    // B operands, one (first half, second half) pair of k-steps at a time: deRoPE in fp32 and one
-    // bf16 rounding (keys), or the loaded values themselves, then the MFMAs of both steps.
-    const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
-#pragma unroll
-    for (int s = 0; s < 8; s += 2) {
-      bf16x8 bu, bv;
-      if constexpr (DEROPE) {
-        float u[8], v[8];
-        unpack8(xc[s], u);
-        unpack8(xc[s + 1], v);
-        constexpr int spH = DH / 16;
-        const int o = (s % spH) >> 1;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float cc = cs_c[o][e], sn = cs_s[o][e];
-          const float a = u[e], b = v[e];
-          u[e] = a * cc + b * sn;
-          v[e] = b * cc - a * sn;
-        }
-        bu = __builtin_bit_cast(bf16x8, pack8(u));
-        bv = __builtin_bit_cast(bf16x8, pack8(v));
-      } else {
-        bu = __builtin_bit_cast(bf16x8, xc[s]);
-        bv = __builtin_bit_cast(bf16x8, xc[s + 1]);
-      }
-      const int colu = chunk_col<DH>(s, h, derope), colv = chunk_col<DH>(s + 1, h, derope);
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = efrag(eb, b, colu);
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bu, acc[b], 0, 0, 0);
-      }
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = efrag(eb, b, colv);
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
-      }
-      if constexpr (MU) {
-        // E mu for this wave's offset blocks: mu (same columns as the inputs) in every B column
-        const bf16x8 mu_u = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colu);
-        const bf16x8 mu_v = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colv);
-#pragma unroll
-        for (int i = 0; i < kMuBlocks; ++i) {
-          const int b = wave + 4 * i;
-          if (b < RB) {
-            const bf16x8 au = efrag(eb, b, colu);
-            const bf16x8 av = efrag(eb, b, colv);
-            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(au, mu_u, accm[i], 0, 0, 0);
-            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, mu_v, accm[i], 0, 0, 0);
-          }
-        }
-      }
-    }
+    compute_chunk(c, buf, xc);
     wait_vmem();
     lds_barrier();
 #pragma unroll
@@ -230,60 +281,7 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
     __builtin_amdgcn_sched_barrier(0);
     load_x(c + 2 < last ? c + 2 : last, xfar);
     __builtin_amdgcn_sched_barrier(0);
-    if (c < nchunks) {
-    // B operands, one (first half, second half) pair of k-steps at a time: deRoPE in fp32 and one
-    // bf16 rounding (keys), or the loaded values themselves, then the MFMAs of both steps.
-    const uint16_t* eb = Es + buf * RB * 32 * kLdc + (lane & 31) * kLdc;
-#pragma unroll
-    for (int s = 0; s < 8; s += 2) {
-      bf16x8 bu, bv;
-      if constexpr (DEROPE) {
-        float u[8], v[8];
-        unpack8(xcur[s], u);
-        unpack8(xcur[s + 1], v);
-        constexpr int spH = DH / 16;
-        const int o = (s % spH) >> 1;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float cc = cs_c[o][e], sn = cs_s[o][e];
-          const float a = u[e], b = v[e];
-          u[e] = a * cc + b * sn;
-          v[e] = b * cc - a * sn;
-        }
-        bu = __builtin_bit_cast(bf16x8, pack8(u));
-        bv = __builtin_bit_cast(bf16x8, pack8(v));
-      } else {
-        bu = __builtin_bit_cast(bf16x8, xcur[s]);
-        bv = __builtin_bit_cast(bf16x8, xcur[s + 1]);
-      }
-      const int colu = chunk_col<DH>(s, h, derope), colv = chunk_col<DH>(s + 1, h, derope);
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = efrag(eb, b, colu);
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bu, acc[b], 0, 0, 0);
-      }
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const bf16x8 ae = efrag(eb, b, colv);
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ae, bv, acc[b], 0, 0, 0);
-      }
-      if constexpr (MU) {
-        // E mu for this wave's offset blocks: mu (same columns as the inputs) in every B column
-        const bf16x8 mu_u = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colu);
-        const bf16x8 mu_v = *reinterpret_cast<const bf16x8*>(mus + c * kChunk + colv);
-#pragma unroll
-        for (int i = 0; i < kMuBlocks; ++i) {
-          const int b = wave + 4 * i;
-          if (b < RB) {
-            const bf16x8 au = efrag(eb, b, colu);
-            const bf16x8 av = efrag(eb, b, colv);
-            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(au, mu_u, accm[i], 0, 0, 0);
-            accm[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, mu_v, accm[i], 0, 0, 0);
-          }
-        }
-      }
-    }
-    }
+    if (c < nchunks) compute_chunk(c, buf, xcur);
     // chunk c + 1's weights and inputs have landed once only chunk c + 2's 8 input loads are
     // pending; the barrier makes that true for every wave and retires this chunk's LDS reads.  The
     // scheduling fences keep each step's loads on their side of the count.
@@ -334,23 +332,24 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 
 template <int RB, bool DEROPE, bool MU>
 hipError_t launch_rb(int head_dim, const GemmParams& p, size_t lds, hipStream_t stream) {
-  // long rows (many chunks per unit, few units) prefetch two chunks ahead
-  const bool deep = !DEROPE && !MU && p.jobs[0].k >= 2048;
-  if (head_dim == 128) {
-    if (deep)
-      hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 2>), dim3(p.total_tiles),
-                         dim3(kThreads), lds, stream, p);
-    else
-      hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 1>), dim3(p.total_tiles),
-                         dim3(kThreads), lds, stream, p);
-  } else {
-    if (deep)
-      hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 2>), dim3(p.total_tiles),
-                         dim3(kThreads), lds, stream, p);
-    else
-      hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 1>), dim3(p.total_tiles),
-                         dim3(kThreads), lds, stream, p);
+  // long rows without deRoPE or offset (the H branch) prefetch two chunks ahead
+  if constexpr (!DEROPE && !MU) {
+    if (p.jobs[0].k >= 2048) {
+      if (head_dim == 128)
+        hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 2>), dim3(p.total_tiles),
+                           dim3(kThreads), lds, stream, p);
+      else
+        hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 2>), dim3(p.total_tiles),
+                           dim3(kThreads), lds, stream, p);
+      return hipGetLastError();
+    }
   }
+  if (head_dim == 128)
+    hipLaunchKernelGGL((encode_bf16_kernel<RB, 128, DEROPE, MU, 1>), dim3(p.total_tiles),
+                       dim3(kThreads), lds, stream, p);
+  else
+    hipLaunchKernelGGL((encode_bf16_kernel<RB, 64, DEROPE, MU, 1>), dim3(p.total_tiles),
+                       dim3(kThreads), lds, stream, p);
   return hipGetLastError();
 }
 
