@@ -239,7 +239,8 @@ def time_fit(dev, steps, warmup, stream):
     and ``scd_fit_solve`` for keys and values, HIP events on the stream they run on.  The Gram is
     HBM-bound (2w = 256 columns: about 128 flops per byte of the symmetric product); algorithmic
     bytes read both caches once and write the Gram and column sums once.  The solve is the
-    O(w^3) fp64 step, one workgroup per layer, reported as time per call."""
+    O(w^3) fp64 step (each stage one launch over all layers; the tridiagonalisation and the
+    Cholesky one launch per column), reported as time per call."""
     import torch
 
     import paper_2606_07684_amd as scd
@@ -305,8 +306,9 @@ def time_fit(dev, steps, warmup, stream):
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                      "alg_bytes": nbytes, "alg_flops": flops,
                      "tflops": round(flops / (gram_ms * 1e-3) / 1e12, 2)},
-            "solve": {"kernel": "fit_solve_kernel", "ms_per_call": round(solve_ms / 2, 3),
-                      "calls": 2, "layers_per_call": len(R)}}
+            "solve": {"kernels": "fit_prep/tridiag/bisect/inverse/back/project/normal/chol/out",
+                      "ms_per_call": round(solve_ms / 2, 3), "calls": 2,
+                      "layers_per_call": len(R), "launches_per_call": n2 + w + 6}}
 
 
 def time_receive(wl, dev, steps, warmup, stream, model, batch, rope, inp, z_k, z_v, z_h,

@@ -902,8 +902,6 @@ scd_status_t scd_patch_kv_from_codes(const scd_model_t* model, const scd_batch_t
 // ---- Offline Reuse fit ------------------------------------------------------------------------
 namespace {
 
-constexpr int kFitMaxSweeps = 40;
-
 // Slices of the row axis for a Gram launch of n_jobs jobs: about two rounds of workgroups (the
 // whole-Gram kernel fits one workgroup per CU, the tile kernels two) when the tiles allow, at
 // least 512 rows per slice, slice lengths a multiple of the kernels' k-step.
@@ -944,8 +942,7 @@ size_t fit_gram_ws(const scd_model_t* m, int64_t n_rows) {
 size_t fit_solve_ws(const scd_model_t* m) {
   const int R = count_reuse(m);
   const size_t jobs = R < scd::kMaxJobs ? R : scd::kMaxJobs;
-  const size_t n = 2 * static_cast<size_t>(m->basis_width);
-  return jobs * 3 * n * n * sizeof(double);
+  return jobs * static_cast<size_t>(scd::fit_solve_layer_doubles(m->basis_width)) * sizeof(double);
 }
 
 // Per-layer output buffers of the fit must be distinct: the layers of a launch are written
@@ -1101,7 +1098,6 @@ scd_status_t enqueue_fit_solve(const scd_model_t* model, int32_t branch, int64_t
     p.lambda = ridge_lambda;
     p.center = center;
     p.bf16 = model->dtype == SCD_BF16 ? 1 : 0;
-    p.max_sweeps = kFitMaxSweeps;
     p.work = work;
     const hipError_t e = scd::launch_fit_solve(p, stream);
     if (e != hipSuccess) return fail(SCD_ERR_HIP, "fit solve launch failed: %s", hipGetErrorString(e));
@@ -1143,8 +1139,8 @@ scd_status_t scd_fit_solve_noalloc(const scd_model_t* model, int32_t branch, int
   SCD_TRY(check_fit_solve(model, branch, n_rows, ridge_lambda, center, gram, colsum, w_enc, w_dec,
                           mu_enc, mu_dec, &layers));
   if (layers.empty()) return ok();
-  const size_t n = 2 * static_cast<size_t>(model->basis_width);
-  const size_t per_layer = 3 * n * n * sizeof(double);
+  const size_t per_layer =
+      static_cast<size_t>(scd::fit_solve_layer_doubles(model->basis_width)) * sizeof(double);
   if (per_layer > scd::kFitScratchBytes)
     return fail(SCD_ERR_WORKSPACE,
                 "basis_width %d needs %zu bytes of solve scratch per layer; the allocation-free "

@@ -10,7 +10,8 @@
 //   * the ridge decoder F = (Z^T Z + lam I)^-1 Z^T B needs Z^T Z = V_r^T G V_r and
 //     Z^T B = (G[w:2w, :] V_r)^T.
 // The O(N w^2) part (the Gram) streams the caches once on the matrix cores; the O(w^3) part runs in
-// fp64 in one workgroup per layer (parallel cyclic Jacobi, then Cholesky solves).
+// fp64 as a sequence of launches over all layers at once (Householder tridiagonalisation,
+// bisection and inverse iteration for the top r eigenpairs, Cholesky solves).
 #include "scd_device.h"
 
 #include <mutex>
@@ -20,7 +21,7 @@ namespace scd {
 using namespace dev;
 
 // Device-resident scratch of the allocation-free solve (scd_fit_solve_noalloc): the solve's fp64
-// Jacobi and solve matrices for as many layers as fit, reused launch after launch.  Each GPU the
+// matrices for as many layers as fit, reused launch after launch.  Each GPU the
 // library runs on holds its own copy for the life of the process.  Host code must never pass this
 // name to a kernel (in host code it is a stand-in, not a device address): fit_scratch() looks up
 // the device address once per device.
@@ -607,65 +608,108 @@ __global__ __launch_bounds__(256) void fit_gram_reduce_kernel(const FitGramParam
 }
 
 // ---------------------------------------------------------------------------------------------
-// fp64 solve, one workgroup of 1024 threads per layer.
+// fp64 solve.  Every stage is one launch over all layers of the call (the last grid dimension is
+// the layer), so each stage spreads over the whole GPU:
+//   prep      the centred Gram G_c and the offsets;
+//   tridiag   Householder reduction Q^T G_c Q = T (tridiagonal), one launch per column: the launch
+//             for column k + 1 applies reflector k to the trailing block, forms reflector k + 1
+//             from the updated column and the product p = tau A v that the next launch needs.  Two
+//             matrix copies take turns as source and destination, so no workgroup reads what
+//             another workgroup of the same launch writes;
+//   bisect    the r largest eigenvalues of T by bisection on Sturm counts;
+//   inverse   their eigenvectors of T by inverse iteration (three solves with T - lambda I under
+//             partial pivoting); eigenvalues closer than 1e-7 ||T|| form a cluster, whose vectors
+//             one thread computes in turn, each orthogonalised against the cluster's earlier ones;
+//   back      V_r = Q Y, each column's largest-magnitude entry then made positive;
+//   project   P = G_c V_r;
+//   normal    Z^T Z + lam I = V_r^T P + lam I and A^T A + lam I;
+//   chol      right-looking Cholesky of both, one launch per column;
+//   out       the triangular solves for E and F and the outputs, rounded once.
 // ---------------------------------------------------------------------------------------------
-constexpr int kSolveThreads = 1024;
+constexpr int kSolveThreads = 256;
+constexpr int kSolveRows = 16;  // rows per workgroup of a tridiagonal or a Cholesky step
+constexpr int kBackCols = 8;    // columns of Y per workgroup of the back-transformation
+constexpr int kMaxN = 2 * kFitMaxSolveWidth;
+constexpr int kInverseSolves = 3;
+constexpr double kEps = 2.220446049250313e-16;  // 2^-52
+constexpr double kClusterTol = 1e-7;            // relative to ||T||: eigenvalues closer cluster
+constexpr double kNaN = __builtin_nan("");
 
-// Pair k of round `round` of the cyclic ("round-robin") ordering of n indices: the n/2 pairs of a
-// round are disjoint and the n - 1 rounds visit every pair once.
-__device__ inline void jacobi_pair(int round, int k, int n, int& lo, int& hi) {
-  // round < m and k < n / 2 <= m, so both sums lie in [0, 2m): one conditional subtraction
-  // replaces the modulo
-  const int m = n - 1;
-  int a, b;
-  if (k == 0) {
-    a = m;
-    b = round;
-  } else {
-    a = round + k;
-    a = a >= m ? a - m : a;
-    b = round - k + m;
-    b = b >= m ? b - m : b;
-  }
-  lo = a < b ? a : b;
-  hi = a < b ? b : a;
+// Per-layer table that the prep launch writes into the layer's workspace for the later launches
+// (whose argument block stays small).
+struct SolveJob {
+  const float* gram;
+  const float* colsum;
+  void* w_enc;
+  void* w_dec;
+  void* mu_enc;
+  void* mu_dec;
+  int64_t rank;
+  double tnorm;  // Gershgorin bound of ||T||, written by the bisection launch
+};
+
+struct SolveArgs {
+  double* work;
+  double rows;
+  double lambda;
+  int32_t w;
+  int32_t step;
+  int32_t center;
+  int32_t bf16;
+};
+
+// One layer's workspace (fp64, n = 2w): four n x n matrices Z, X, Y, M, then 8n scalars.
+struct Slots {
+  double *z, *x, *y, *m;
+  double *d, *e, *tau, *p0, *p1, *lam, *ldiag;
+  SolveJob* job;
+};
+
+__device__ inline Slots slots(double* work, int w, int layer) {
+  const int64_t n = 2 * w, n2 = n * n;
+  double* b = work + layer * fit_solve_layer_doubles(w);
+  Slots s;
+  s.z = b;
+  s.x = b + n2;
+  s.y = b + 2 * n2;
+  s.m = b + 3 * n2;
+  double* v = b + 4 * n2;
+  s.d = v;
+  s.e = v + n;
+  s.tau = v + 2 * n;
+  s.p0 = v + 3 * n;
+  s.p1 = v + 4 * n;
+  s.lam = v + 5 * n;
+  s.ldiag = v + 6 * n;  // Cholesky diagonals: A^T A block [w], then Z^T Z block [r]
+  s.job = reinterpret_cast<SolveJob*>(v + 7 * n);
+  return s;
 }
 
-// In-place Cholesky factor (lower triangle) of the dim x dim matrix at a (row stride ld).  A
-// non-positive pivot leaves NaN, which then reaches every output of the solve.
-__device__ void cholesky(double* a, int dim, int ld, double* piv) {
-  const int tid = threadIdx.x;
-  for (int k = 0; k < dim; ++k) {
-    if (tid == 0) {
-      const double d = a[k * ld + k];
-      *piv = d > 0.0 ? sqrt(d) : __longlong_as_double(0x7ff8000000000000ll);
-      a[k * ld + k] = *piv;
-    }
-    __syncthreads();
-    const double pv = *piv;
-    for (int i = k + 1 + tid; i < dim; i += kSolveThreads) a[i * ld + k] /= pv;
-    __syncthreads();
-    const int rem = dim - k - 1;
-    for (int e = tid; e < rem * rem; e += kSolveThreads) {
-      const int i = k + 1 + e / rem, j = k + 1 + e % rem;
-      if (j <= i) a[i * ld + j] -= a[i * ld + k] * a[j * ld + k];
-    }
-    __syncthreads();
-  }
+// Centred Gram entry G[i][j] - s_i s_j / N in fp64; every stage that needs G_c evaluates it with
+// this one expression, so all see the same values.
+__device__ inline double centred(const float* gram, const float* cs, int n, int i, int j, double rows,
+                                 bool center) {
+  double g = static_cast<double>(gram[static_cast<int64_t>(i) * n + j]);
+  if (center) g -= static_cast<double>(cs[i]) * static_cast<double>(cs[j]) / rows;
+  return g;
 }
 
-// Solves (L L^T) x = b for one right-hand side held at x[0], x[xs], ... (in place).
-__device__ void chol_solve(const double* l, int dim, int ld, double* x, int xs) {
-  for (int i = 0; i < dim; ++i) {
-    double s = x[i * xs];
-    for (int j = 0; j < i; ++j) s -= l[i * ld + j] * x[j * xs];
-    x[i * xs] = s / l[i * ld + i];
-  }
-  for (int i = dim - 1; i >= 0; --i) {
-    double s = x[i * xs];
-    for (int j = i + 1; j < dim; ++j) s -= l[j * ld + i] * x[j * xs];
-    x[i * xs] = s / l[i * ld + i];
-  }
+__device__ inline double wave_sum(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Sum over the workgroup (kSolveThreads), the same value returned to every thread.  `red` holds
+// one double per wave; the trailing barrier lets the caller reuse it at once.
+__device__ inline double block_sum(double v, double* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  v = wave_sum(v);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int q = 0; q < kSolveThreads / 64; ++q) s += red[q];
+  __syncthreads();
+  return s;
 }
 
 __device__ inline void store_out(void* dst, int64_t i, double v, bool bf16) {
@@ -673,172 +717,522 @@ __device__ inline void store_out(void* dst, int64_t i, double v, bool bf16) {
   else static_cast<float*>(dst)[i] = static_cast<float>(v);
 }
 
-__global__ __launch_bounds__(kSolveThreads) void fit_solve_kernel(const FitSolveParams p) {
-  const int job = blockIdx.x;
-  const FitSolveJob& jb = p.jobs[job];
-  const int w = p.w, n = 2 * w, r = jb.rank, half = n / 2;
-  const int tid = threadIdx.x;
-  const bool bf16 = p.bf16 != 0;
-  double* gc = p.work + static_cast<int64_t>(job) * 3 * n * n;  // centred Gram (kept)
-  double* mj = gc + static_cast<int64_t>(n) * n;                 // Jacobi matrix, then V_r
-  double* vj = mj + static_cast<int64_t>(n) * n;                 // eigenvectors, then G V_r
+// Reflector j lives in row j of X (j odd) or Y (j even), entries j+1 .. n-1 (the first one 1).
+__device__ inline double* reflector_rows(const Slots& s, int j) { return (j & 1) ? s.x : s.y; }
+
+// ---- prep: G_c into Z, the offsets, the job table --------------------------------------------
+__global__ __launch_bounds__(kSolveThreads) void fit_prep_kernel(const FitSolveParams p) {
+  const int layer = blockIdx.y, n = 2 * p.w;
+  const FitSolveJob& jb = p.jobs[layer];
+  const Slots s = slots(p.work, p.w, layer);
   const double rows = static_cast<double>(p.n_rows);
-
-  __shared__ double rot_c[kFitMaxSolveWidth], rot_s[kFitMaxSolveWidth];
-  __shared__ int sel[2 * kFitMaxSolveWidth];
-  __shared__ int changed;
-  __shared__ double piv, trace;
-
-  // centred Gram G - s s^T / N (the Gram of the rows minus their mean), V = I, offsets
-  for (int e = tid; e < n * n; e += kSolveThreads) {
-    const int i = e / n, j = e % n;
-    double g = jb.gram[e];
-    if (p.center) g -= static_cast<double>(jb.colsum[i]) * static_cast<double>(jb.colsum[j]) / rows;
-    gc[e] = g;
-    mj[e] = g;
-    vj[e] = i == j ? 1.0 : 0.0;
+  const bool center = p.center != 0, bf16 = p.bf16 != 0;
+  const int i0 = blockIdx.x * kSolveRows;
+  for (int e = threadIdx.x; e < kSolveRows * n; e += kSolveThreads) {
+    const int i = i0 + e / n, j = e % n;
+    if (i < n) s.z[static_cast<int64_t>(i) * n + j] = centred(jb.gram, jb.colsum, n, i, j, rows, center);
   }
-  if (p.center) {
-    for (int i = tid; i < w; i += kSolveThreads) {
+  if (blockIdx.x != 0) return;
+  if (threadIdx.x == 0)
+    *s.job = SolveJob{jb.gram, jb.colsum, jb.w_enc, jb.w_dec, jb.mu_enc, jb.mu_dec, jb.rank, 0.0};
+  if (center) {
+    for (int i = threadIdx.x; i < p.w; i += kSolveThreads) {
       store_out(jb.mu_enc, i, static_cast<double>(jb.colsum[i]) / rows, bf16);
-      store_out(jb.mu_dec, i, static_cast<double>(jb.colsum[w + i]) / rows, bf16);
+      store_out(jb.mu_dec, i, static_cast<double>(jb.colsum[p.w + i]) / rows, bf16);
     }
   }
-  if (tid == 0) {
-    trace = 0.0;
-    changed = 0;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    double t = 0.0;
-    for (int i = 0; i < n; ++i) t += fabs(gc[i * n + i]);
-    trace = t;
-  }
-  __syncthreads();
-  // Rotations below these thresholds change the eigenvectors far below fp32 precision; lower
-  // thresholds would keep rotating on roundoff (off-diagonal entries of about eps * lambda_max)
-  // and never report convergence.
-  const double floor_abs = 1e-15 * trace;
+}
 
-  // parallel cyclic Jacobi: every round applies n/2 disjoint rotations at once
-  for (int sweep = 0; sweep < p.max_sweeps; ++sweep) {
-    for (int round = 0; round < n - 1; ++round) {
-      for (int k = tid; k < half; k += kSolveThreads) {
-        int a, b;
-        jacobi_pair(round, k, n, a, b);
-        const double app = mj[a * n + a], aqq = mj[b * n + b], apq = mj[a * n + b];
-        double cr = 1.0, sr = 0.0;
-        if (fabs(apq) > floor_abs && fabs(apq) > 1e-12 * sqrt(fabs(app * aqq))) {
-          // zero the (a, b) entry of J^T M J with J = [[c, s], [-s, c]] on (a, b)
-          const double th = (aqq - app) / (2.0 * apq);
-          const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(th * th + 1.0));
-          cr = 1.0 / sqrt(t * t + 1.0);
-          sr = t * cr;
-          changed = 1;
+// ---- one Householder step ----------------------------------------------------------------------
+// Launch k (k = -1 .. n-3), with A^(k) the matrix after reflectors 0 .. k-1 (A^(0) = G_c):
+//   w_k = p_k - (tau_k / 2)(p_k . v_k) v_k;  A^(k+1) = A^(k) - v_k w_k^T - w_k v_k^T on the block
+//   [k+1, n)^2 (launch -1 has no reflector to apply);
+//   column k+1 of A^(k+1) gives d_{k+1}, and its part below the diagonal, x, gives reflector k+1:
+//   beta = -sign(x_0) ||x||, tau = (beta - x_0) / beta, v = x / (x_0 - beta) with v_0 = 1, so that
+//   (I - tau v v^T) x = beta e_0 (e_{k+1} = beta; x with nothing below x_0 takes tau = 0);
+//   p_{k+1} = tau_{k+1} A^(k+1) v_{k+1} on rows [k+2, n), this workgroup's rows only.
+// Source A^(k): G_c (Z) for k <= 0, else the previous launch's destination; destination: X for even
+// k, Y for odd k.  Reflector k+1 goes into row k+1 of the destination, a row no later launch
+// writes; p alternates between two vectors.
+__global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveArgs a) {
+  __shared__ double vk[kMaxN], wk[kMaxN], vn[kMaxN];
+  __shared__ double red[kSolveThreads / 64];
+  const int layer = blockIdx.y, n = 2 * a.w, k = a.step, tid = threadIdx.x;
+  const Slots s = slots(a.work, a.w, layer);
+  const double* src = k <= 0 ? s.z : ((k - 1) & 1 ? s.y : s.x);
+  double* dst = (k & 1) ? s.y : s.x;  // k = -1 is odd: Y (only its reflector row is written)
+  double* p_next = ((k + 1) & 1) ? s.p1 : s.p0;
+  // w_k (zero for launch -1)
+  if (k >= 0) {
+    const double* vrow = reflector_rows(s, k) + static_cast<int64_t>(k) * n;
+    const double* p_cur = (k & 1) ? s.p1 : s.p0;
+    double dot = 0.0;
+    for (int i = k + 1 + tid; i < n; i += kSolveThreads) {
+      const double v = vrow[i], pv = p_cur[i];
+      vk[i] = v;
+      wk[i] = pv;
+      dot += pv * v;
+    }
+    const double kk = 0.5 * s.tau[k] * block_sum(dot, red);
+    for (int i = k + 1 + tid; i < n; i += kSolveThreads) wk[i] -= kk * vk[i];
+  } else {
+    for (int i = tid; i < n; i += kSolveThreads) vk[i] = wk[i] = 0.0;
+  }
+  __syncthreads();
+  // column k+1 of A^(k+1), read as row k+1 (the matrix is symmetric)
+  const double vk1 = vk[k + 1], wk1 = wk[k + 1];
+  const double* row = src + static_cast<int64_t>(k + 1) * n;
+  double sig = 0.0;
+  for (int i = k + 1 + tid; i < n; i += kSolveThreads) {
+    const double c = row[i] - vk1 * wk[i] - wk1 * vk[i];
+    vn[i] = c;
+    if (i >= k + 3) sig += c * c;
+  }
+  const double sigma = block_sum(sig, red);  // its barrier also publishes vn
+  const double d_next = vn[k + 1], alpha = vn[k + 2];
+  __syncthreads();  // every thread has read alpha before v_0 = 1 replaces it
+  double tau = 0.0, beta = alpha, scale = 0.0;
+  if (!(sigma == 0.0)) {
+    const double norm = sqrt(alpha * alpha + sigma);
+    beta = alpha >= 0.0 ? -norm : norm;
+    tau = (beta - alpha) / beta;
+    scale = 1.0 / (alpha - beta);
+  }
+  for (int i = k + 3 + tid; i < n; i += kSolveThreads) vn[i] *= scale;
+  if (tid == 0) vn[k + 2] = 1.0;
+  __syncthreads();
+  // this workgroup's rows of A^(k+1) and of p_{k+1}
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r0 = k + 2 + blockIdx.x * kSolveRows;
+  for (int i = r0 + wave; i < r0 + kSolveRows && i < n; i += kSolveThreads / 64) {
+    const double* arow = src + static_cast<int64_t>(i) * n;
+    double* orow = dst + static_cast<int64_t>(i) * n;
+    const double vi = vk[i], wi = wk[i];
+    double acc = 0.0;
+    for (int j = k + 2 + lane; j < n; j += 64) {
+      const double v = arow[j] - vi * wk[j] - wi * vk[j];
+      if (k >= 0) orow[j] = v;
+      if (k == n - 3) s.d[n - 1] = v;  // the last launch: i = j = n - 1
+      acc += v * vn[j];
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) p_next[i] = tau * acc;
+  }
+  if (blockIdx.x == 0) {
+    double* vrow = dst + static_cast<int64_t>(k + 1) * n;
+    for (int i = k + 2 + tid; i < n; i += kSolveThreads) vrow[i] = vn[i];
+    if (tid == 0) {
+      s.d[k + 1] = d_next;
+      s.e[k + 1] = beta;
+      s.tau[k + 1] = tau;
+    }
+  }
+}
+
+// ---- bisection -------------------------------------------------------------------------------
+// Number of eigenvalues of T below x (Sturm count of the LDL^T pivots of T - x I); a pivot smaller
+// in magnitude than pivmin counts as -pivmin.
+__device__ inline int sturm_count(const double* d, const double* e2, int n, double x, double pivmin) {
+  double q = d[0] - x;
+  if (fabs(q) < pivmin) q = -pivmin;
+  int c = q < 0.0 ? 1 : 0;
+  for (int i = 1; i < n; ++i) {
+    q = (d[i] - x) - e2[i - 1] / q;
+    if (fabs(q) < pivmin) q = -pivmin;
+    c += q < 0.0 ? 1 : 0;
+  }
+  return c;
+}
+
+// Gershgorin interval of T, over the workgroup (64 threads, one wave).
+__device__ inline void gershgorin(const double* d, const double* ae, int n, double& lo, double& hi) {
+  lo = INFINITY;
+  hi = -INFINITY;
+  for (int i = threadIdx.x; i < n; i += 64) {
+    const double rad = (i > 0 ? ae[i - 1] : 0.0) + (i < n - 1 ? ae[i] : 0.0);
+    lo = fmin(lo, d[i] - rad);
+    hi = fmax(hi, d[i] + rad);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = fmin(lo, __shfl_xor(lo, o, 64));
+    hi = fmax(hi, __shfl_xor(hi, o, 64));
+  }
+}
+
+// One wave per workgroup, one eigenvalue per thread: lam[j] = the (j+1)-th largest, found to an
+// absolute 2^-52 ||T|| plus a relative 2^-51.
+__global__ __launch_bounds__(64) void fit_bisect_kernel(const SolveArgs a) {
+  __shared__ double d[kMaxN], e2[kMaxN], ae[kMaxN];
+  const int layer = blockIdx.y, n = 2 * a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  for (int i = threadIdx.x; i < n; i += 64) {
+    d[i] = s.d[i];
+    const double e = i < n - 1 ? s.e[i] : 0.0;
+    e2[i] = e * e;
+    ae[i] = fabs(e);
+  }
+  __syncthreads();
+  double lo0, hi0;
+  gershgorin(d, ae, n, lo0, hi0);
+  // a floor keeps the tolerances positive for an all-zero matrix
+  const double tnorm = fmax(fmax(fabs(lo0), fabs(hi0)), 1e-280);
+  if (blockIdx.x == 0 && threadIdx.x == 0) s.job->tnorm = tnorm;
+  const int j = blockIdx.x * 64 + threadIdx.x;
+  if (j >= r) return;
+  const double atol = kEps * tnorm, pivmin = kEps * tnorm;
+  const int t = n - 1 - j;  // ascending index
+  double lo = lo0 - atol, hi = hi0 + atol;
+  for (int it = 0; it < 128; ++it) {
+    if (hi - lo <= atol + 2.0 * kEps * fmax(fabs(lo), fabs(hi))) break;
+    const double mid = 0.5 * (lo + hi);
+    if (sturm_count(d, e2, n, mid, pivmin) <= t) lo = mid;
+    else hi = mid;
+  }
+  s.lam[j] = 0.5 * (lo + hi);
+}
+
+// ---- inverse iteration --------------------------------------------------------------------------
+__device__ inline double start_entry(int i, int m) {
+  uint32_t x = static_cast<uint32_t>(i) * 0x9E3779B1u ^ (static_cast<uint32_t>(m) + 0x7F4A7C15u) * 0x85EBCA77u;
+  x ^= x >> 16;
+  x *= 0x7FEB352Du;
+  x ^= x >> 15;
+  x *= 0x846CA68Bu;
+  x ^= x >> 16;
+  return static_cast<double>(x >> 8) * (1.0 / 16777216.0) - 0.5;
+}
+
+// A pivot smaller than tol in magnitude becomes +-tol (NaN stays NaN).
+__device__ inline double guard_pivot(double c, double tol) {
+  return !(fabs(c) <= tol) ? c : (c >= 0.0 ? tol : -tol);
+}
+
+// Vector m of the layer: Y[i][m] (Z[0, n r)), with the LU factors of T - sigma I in U0 (Z[n r,
+// 2 n r)), U1 and U2 (M[0, n r) and M[n r, 2 n r)), all indexed [i][m].
+__global__ __launch_bounds__(64) void fit_inverse_kernel(const SolveArgs a) {
+  __shared__ double d[kMaxN], e[kMaxN];
+  const int layer = blockIdx.y, n = 2 * a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  for (int i = threadIdx.x; i < n; i += 64) {
+    d[i] = s.d[i];
+    e[i] = i < n - 1 ? s.e[i] : 0.0;
+  }
+  __syncthreads();
+  const int j = blockIdx.x * 64 + threadIdx.x;
+  if (j >= r) return;
+  const double tnorm = s.job->tnorm;
+  const double ctol = kClusterTol * tnorm, pert = 10.0 * kEps * tnorm, ptol = kEps * tnorm;
+  const double* lam = s.lam;
+  // only the first thread of a cluster works; it takes the whole cluster in order
+  if (j > 0 && !(lam[j - 1] - lam[j] > ctol)) return;
+  int last = j;
+  while (last + 1 < r && !(lam[last] - lam[last + 1] > ctol)) ++last;
+  const int64_t nr = static_cast<int64_t>(n) * r;
+  double* yv = s.z;
+  double* u0 = s.z + nr;
+  double* u1 = s.m;
+  double* u2 = s.m + nr;
+  double sigma = 0.0;
+  for (int m = j; m <= last; ++m) {
+    // shifts inside a cluster step down by at least pert, so the solves stay independent
+    sigma = m == j ? lam[m] : fmin(lam[m], sigma - pert);
+    for (int i = 0; i < n; ++i) yv[static_cast<int64_t>(i) * r + m] = start_entry(i, m);
+    double sc = 2.0;  // the start vector's entries lie in [-1/2, 1/2)
+    for (int it = 0; it < kInverseSolves; ++it) {
+      // forward elimination of (T - sigma I) y = b / max|b| with partial pivoting; rows hold
+      // (c0, c1) on the diagonal and the superdiagonal, the right-hand side rides along
+      double c0 = d[0] - sigma, c1 = n > 1 ? e[0] : 0.0;
+      double y = yv[m] * sc;
+      for (int i = 0; i < n - 1; ++i) {
+        const int64_t at = static_cast<int64_t>(i) * r + m;
+        const double sub = e[i], a1 = d[i + 1] - sigma, b1 = i + 1 < n - 1 ? e[i + 1] : 0.0;
+        const double nb = yv[at + r] * sc;
+        if (fabs(c0) >= fabs(sub)) {
+          const double piv = guard_pivot(c0, ptol);
+          const double mult = sub / piv;
+          u0[at] = piv;
+          u1[at] = c1;
+          u2[at] = 0.0;
+          yv[at] = y;
+          y = nb - mult * y;
+          c0 = a1 - mult * c1;
+          c1 = b1;
+        } else {
+          const double mult = c0 / sub;
+          u0[at] = sub;
+          u1[at] = a1;
+          u2[at] = b1;
+          yv[at] = nb;
+          y = y - mult * nb;
+          c0 = c1 - mult * a1;
+          c1 = -mult * b1;
         }
-        rot_c[k] = cr;
-        rot_s[k] = sr;
       }
-      __syncthreads();
-      for (int e = tid; e < half * half; e += kSolveThreads) {
-        const int P = e / half, Q = e % half;
-        int p0, q0, p1, q1;
-        jacobi_pair(round, P, n, p0, q0);
-        jacobi_pair(round, Q, n, p1, q1);
-        const double cP = rot_c[P], sP = rot_s[P], cQ = rot_c[Q], sQ = rot_s[Q];
-        const double m00 = mj[p0 * n + p1], m01 = mj[p0 * n + q1];
-        const double m10 = mj[q0 * n + p1], m11 = mj[q0 * n + q1];
-        const double r0a = cP * m00 - sP * m10, r0b = cP * m01 - sP * m11;
-        const double r1a = sP * m00 + cP * m10, r1b = sP * m01 + cP * m11;
-        mj[p0 * n + p1] = cQ * r0a - sQ * r0b;
-        mj[p0 * n + q1] = sQ * r0a + cQ * r0b;
-        mj[q0 * n + p1] = cQ * r1a - sQ * r1b;
-        mj[q0 * n + q1] = sQ * r1a + cQ * r1b;
+      {
+        const int64_t at = static_cast<int64_t>(n - 1) * r + m;
+        u0[at] = guard_pivot(c0, ptol);
+        yv[at] = y;
       }
-      for (int e = tid; e < n * half; e += kSolveThreads) {
-        const int i = e / half, Q = e % half;
-        int p1, q1;
-        jacobi_pair(round, Q, n, p1, q1);
-        const double cQ = rot_c[Q], sQ = rot_s[Q];
-        const double a = vj[i * n + p1], b = vj[i * n + q1];
-        vj[i * n + p1] = cQ * a - sQ * b;
-        vj[i * n + q1] = sQ * a + cQ * b;
+      // back substitution, in place
+      double x1 = 0.0, x2 = 0.0;
+      for (int i = n - 1; i >= 0; --i) {
+        const int64_t at = static_cast<int64_t>(i) * r + m;
+        double v = yv[at];
+        if (i + 1 < n) v -= u1[at] * x1;
+        if (i + 2 < n) v -= u2[at] * x2;
+        v /= u0[at];
+        yv[at] = v;
+        x2 = x1;
+        x1 = v;
       }
-      __syncthreads();
+      // orthogonalise against the cluster's earlier vectors, then normalise
+      for (int q = j; q < m; ++q) {
+        double dot = 0.0;
+        for (int i = 0; i < n; ++i)
+          dot += yv[static_cast<int64_t>(i) * r + q] * yv[static_cast<int64_t>(i) * r + m];
+        for (int i = 0; i < n; ++i)
+          yv[static_cast<int64_t>(i) * r + m] -= dot * yv[static_cast<int64_t>(i) * r + q];
+      }
+      double ss = 0.0, mx = 0.0;
+      for (int i = 0; i < n; ++i) {
+        const double v = yv[static_cast<int64_t>(i) * r + m];
+        ss += v * v;
+        mx = fmax(mx, fabs(v));
+      }
+      const double inv = 1.0 / sqrt(ss);
+      for (int i = 0; i < n; ++i) yv[static_cast<int64_t>(i) * r + m] *= inv;
+      sc = mx > 0.0 ? 1.0 / (mx * inv) : 1.0;  // 1 / max|y| of the normalised vector
     }
-    const int any = changed;
-    __syncthreads();
-    if (!any) break;
-    if (tid == 0) changed = 0;
-    __syncthreads();
   }
+}
 
-  // the r largest eigenvalues in decreasing order.  The order is total (NaN counts as -inf and
-  // ties go to the lower index), so the ranks are a permutation of [0, n) and every sel[k], k < r,
-  // is written even when non-finite inputs reached the matrix.
-  for (int i = tid; i < n; i += kSolveThreads) {
-    const double di = mj[i * n + i];
-    const double li = isnan(di) ? -INFINITY : di;
-    int cnt = 0;
-    for (int j = 0; j < n; ++j) {
-      const double dj = mj[j * n + j];
-      const double lj = isnan(dj) ? -INFINITY : dj;
-      cnt += (lj > li || (lj == li && j < i)) ? 1 : 0;
+// ---- back-transformation and sign ---------------------------------------------------------------
+// kBackCols columns of Y per workgroup, held in LDS while the reflectors n-3 .. 0 are applied in
+// turn (Y <- (I - tau_j v_j v_j^T) Y); thread t keeps rows i = t / kBackCols (mod 32) of column
+// t % kBackCols.  Then each column's first entry of largest magnitude is made positive.
+__global__ __launch_bounds__(kSolveThreads) void fit_back_kernel(const SolveArgs a) {
+  __shared__ double yc[kMaxN * kBackCols];
+  __shared__ double vb[kMaxN];
+  __shared__ double red[kSolveThreads / 64][kBackCols];
+  __shared__ int redi[kSolveThreads / 64][kBackCols];
+  const int layer = blockIdx.y, n = 2 * a.w, tid = threadIdx.x;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  const int c0 = blockIdx.x * kBackCols;
+  if (c0 >= r) return;
+  constexpr int kGroups = kSolveThreads / kBackCols;  // 32 row groups
+  const int c = tid % kBackCols, g = tid / kBackCols, lane = tid & 63, wave = tid >> 6;
+  const bool live = c0 + c < r;
+  for (int e = tid; e < n * kBackCols; e += kSolveThreads) {
+    const int i = e / kBackCols, cc = e % kBackCols;
+    yc[e] = c0 + cc < r ? s.z[static_cast<int64_t>(i) * r + c0 + cc] : 0.0;
+  }
+  for (int jr = n - 3; jr >= 0; --jr) {
+    const double t = s.tau[jr];
+    if (t == 0.0) continue;
+    const double* vrow = reflector_rows(s, jr) + static_cast<int64_t>(jr) * n;
+    __syncthreads();  // the previous reflector's vb and red reads are done
+    for (int i = jr + 1 + tid; i < n; i += kSolveThreads) vb[i] = vrow[i];
+    __syncthreads();
+    double part = 0.0;
+    for (int i = jr + 1 + g; i < n; i += kGroups) part += vb[i] * yc[i * kBackCols + c];
+    // the 8 row groups of a wave that share column c sit kBackCols lanes apart
+    for (int o = kBackCols; o < 64; o <<= 1) part += __shfl_xor(part, o, 64);
+    if (lane < kBackCols) red[wave][lane] = part;
+    __syncthreads();
+    double dot = 0.0;
+    for (int q = 0; q < kSolveThreads / 64; ++q) dot += red[q][c];
+    const double f = t * dot;
+    for (int i = jr + 1 + g; i < n; i += kGroups) yc[i * kBackCols + c] -= f * vb[i];
+  }
+  // sign: the first entry of largest magnitude of each column made positive
+  __syncthreads();  // the last reflector's red reads and Y updates are done
+  double best = -1.0;
+  int bi = 0;
+  for (int i = g; i < n; i += kGroups) {
+    const double v = fabs(yc[i * kBackCols + c]);
+    if (v > best) {
+      best = v;
+      bi = i;
     }
-    if (cnt < r) sel[cnt] = i;
+  }
+  for (int o = kBackCols; o < 64; o <<= 1) {
+    const double ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ob > best || (ob == best && oi < bi)) {
+      best = ob;
+      bi = oi;
+    }
+  }
+  if (lane < kBackCols) {
+    red[wave][lane] = best;
+    redi[wave][lane] = bi;
   }
   __syncthreads();
-  // V_r [n, r] (into the Jacobi matrix's storage), each column's largest-magnitude entry positive
-  double* vr = mj;
-  for (int k = tid; k < r; k += kSolveThreads) {
-    const int col = sel[k];
-    int imax = 0;
-    double best = -1.0;
-    for (int i = 0; i < n; ++i) {
-      const double a = fabs(vj[i * n + col]);
-      if (a > best) {
-        best = a;
-        imax = i;
+  best = red[0][c];
+  bi = redi[0][c];
+  for (int q = 1; q < kSolveThreads / 64; ++q) {
+    if (red[q][c] > best || (red[q][c] == best && redi[q][c] < bi)) {
+      best = red[q][c];
+      bi = redi[q][c];
+    }
+  }
+  const double sg = yc[bi * kBackCols + c] < 0.0 ? -1.0 : 1.0;
+  if (live)
+    for (int i = g; i < n; i += kGroups)
+      s.z[static_cast<int64_t>(i) * r + c0 + c] = sg * yc[i * kBackCols + c];
+}
+
+// ---- fp64 tiled products ------------------------------------------------------------------------
+// 64 x 64 output tile per workgroup, 4 x 4 per thread, k-steps of 16 through LDS.  ta(kk, i) and
+// tb(kk, j) give the operands' entries for reduction index kk (0 outside the matrix).
+template <typename FA, typename FB, typename FC>
+__device__ inline void tile_product(int kdim, FA ta, FB tb, FC out) {
+  __shared__ double as[16][64 + 1], bs[16][64 + 1];
+  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
+  double acc[4][4] = {};
+  for (int k0 = 0; k0 < kdim; k0 += 16) {
+    for (int e = tid; e < 16 * 64; e += kSolveThreads) {
+      const int kk = e / 64, x = e % 64;
+      as[kk][x] = k0 + kk < kdim ? ta(k0 + kk, x) : 0.0;
+      bs[kk][x] = k0 + kk < kdim ? tb(k0 + kk, x) : 0.0;
+    }
+    __syncthreads();
+    for (int kk = 0; kk < 16; ++kk) {
+      double av[4], bv[4];
+      for (int q = 0; q < 4; ++q) {
+        av[q] = as[kk][ty + 16 * q];
+        bv[q] = bs[kk][tx + 16 * q];
       }
+      for (int q = 0; q < 4; ++q)
+        for (int u = 0; u < 4; ++u) acc[q][u] += av[q] * bv[u];
     }
-    const double sg = vj[imax * n + col] < 0.0 ? -1.0 : 1.0;
-    for (int i = 0; i < n; ++i) vr[i * r + k] = sg * vj[i * n + col];
+    __syncthreads();
   }
-  __syncthreads();
-  // P = G_c V_r [n, r]: rows [0, w) are A^T Z, rows [w, 2w) are (Z^T B)^T
-  double* pm = vj;
-  for (int e = tid; e < n * r; e += kSolveThreads) {
-    const int i = e / r, k = e % r;
-    double s = 0.0;
-    for (int j = 0; j < n; ++j) s += gc[i * n + j] * vr[j * r + k];
-    pm[e] = s;
+  for (int q = 0; q < 4; ++q)
+    for (int u = 0; u < 4; ++u) out(ty + 16 * q, tx + 16 * u, acc[q][u]);
+}
+
+// P = G_c V_r [n, r] into M (grid: n / 64 x ceil(r_max / 64) tiles, layers)
+__global__ __launch_bounds__(kSolveThreads) void fit_project_kernel(const SolveArgs a) {
+  const int layer = blockIdx.z, n = 2 * a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const SolveJob jb = *s.job;
+  const int r = static_cast<int>(jb.rank);
+  const int i0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
+  if (m0 >= r) return;
+  const bool center = a.center != 0;
+  tile_product(
+      n,
+      // G_c is symmetric: its column i0 + x read as a row, so the loads run along rows
+      [&](int kk, int x) { return centred(jb.gram, jb.colsum, n, kk, i0 + x, a.rows, center); },
+      [&](int kk, int x) {
+        return m0 + x < r ? s.z[static_cast<int64_t>(kk) * r + m0 + x] : 0.0;
+      },
+      [&](int x, int y, double v) {
+        if (m0 + y < r) s.m[static_cast<int64_t>(i0 + x) * r + m0 + y] = v;
+      });
+}
+
+// Z^T Z + lam I = V_r^T P + lam I [r, r] into Y (grid.x = tiles of it), and A^T A + lam I [w, w]
+// into X (grid.y = 1: w / 64 x w / 64 tiles over grid.x)
+__global__ __launch_bounds__(kSolveThreads) void fit_normal_kernel(const SolveArgs a) {
+  const int layer = blockIdx.z, n = 2 * a.w, w = a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const SolveJob jb = *s.job;
+  const int r = static_cast<int>(jb.rank);
+  if (blockIdx.y == 0) {
+    const int nt = (r + 63) / 64;
+    if (static_cast<int>(blockIdx.x) >= nt * nt) return;
+    const int k0 = (blockIdx.x / nt) * 64, l0 = (blockIdx.x % nt) * 64;
+    tile_product(
+        n,
+        [&](int i, int x) { return k0 + x < r ? s.z[static_cast<int64_t>(i) * r + k0 + x] : 0.0; },
+        [&](int i, int x) { return l0 + x < r ? s.m[static_cast<int64_t>(i) * r + l0 + x] : 0.0; },
+        [&](int x, int y, double v) {
+          const int k = k0 + x, l = l0 + y;
+          if (k < r && l < r) s.y[static_cast<int64_t>(k) * r + l] = v + (k == l ? a.lambda : 0.0);
+        });
+  } else {
+    const int nt = w / 64;
+    if (static_cast<int>(blockIdx.x) >= nt * nt) return;
+    const int i0 = (blockIdx.x / nt) * 64, j0 = (blockIdx.x % nt) * 64;
+    const bool center = a.center != 0;
+    for (int e = threadIdx.x; e < 64 * 64; e += kSolveThreads) {
+      const int i = i0 + e / 64, j = j0 + e % 64;
+      s.x[static_cast<int64_t>(i) * w + j] =
+          centred(jb.gram, jb.colsum, n, i, j, a.rows, center) + (i == j ? a.lambda : 0.0);
+    }
   }
+}
+
+// ---- Cholesky, one column per launch --------------------------------------------------------------
+// grid.y = 0: A^T A + lam I (X, size w), 1: Z^T Z + lam I (Y, size r).  Step k reads column k on and
+// below the diagonal, updates rows (k, s) of the lower triangle (a workgroup's kSolveRows rows), and
+// stores L[i][k] at [k][i] in the upper triangle, which nothing reads before the solves; L[k][k]
+// goes to ldiag.  A non-positive pivot leaves NaN, which reaches every output of the layer.
+__global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs a) {
+  __shared__ double lc[kFitMaxSolveWidth];
+  const int layer = blockIdx.z, w = a.w, k = a.step, tid = threadIdx.x;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  const bool zz = blockIdx.y == 1;
+  const int sz = zz ? r : w;
+  if (k >= sz) return;
+  double* mat = zz ? s.y : s.x;
+  double* ldiag = s.ldiag + (zz ? w : 0);
+  const double piv = mat[static_cast<int64_t>(k) * sz + k];
+  const double lkk = piv > 0.0 ? sqrt(piv) : kNaN;
+  for (int i = k + 1 + tid; i < sz; i += kSolveThreads) lc[i] = mat[static_cast<int64_t>(i) * sz + k] / lkk;
   __syncthreads();
-  // Z^T Z + lam I = V_r^T P + lam I (r x r, in the centred Gram's lower-right block) and
-  // A^T A + lam I (its upper-left block)
-  double* c2 = gc + static_cast<int64_t>(w) * n + w;
-  for (int e = tid; e < r * r; e += kSolveThreads) {
-    const int k = e / r, l = e % r;
-    double s = 0.0;
-    for (int i = 0; i < n; ++i) s += vr[i * r + k] * pm[i * r + l];
-    c2[k * n + l] = s + (k == l ? p.lambda : 0.0);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r0 = k + 1 + blockIdx.x * kSolveRows;
+  for (int i = r0 + wave; i < r0 + kSolveRows && i < sz; i += kSolveThreads / 64) {
+    const double li = lc[i];
+    double* row = mat + static_cast<int64_t>(i) * sz;
+    for (int j = k + 1 + lane; j <= i; j += 64) row[j] -= li * lc[j];
+    if (lane == 0) mat[static_cast<int64_t>(k) * sz + i] = li;
   }
-  for (int i = tid; i < w; i += kSolveThreads) gc[i * n + i] += p.lambda;
-  __syncthreads();
-  cholesky(gc, w, n, &piv);
-  cholesky(c2, r, n, &piv);
-  // encoder E = (A^T A + lam I)^-1 A^T Z: column k of P's first w rows, in place
-  for (int k = tid; k < r; k += kSolveThreads) chol_solve(gc, w, n, pm + k, r);
-  // decoder F = (Z^T Z + lam I)^-1 Z^T B: column j of F is row w + j of P, in place
-  for (int j = tid; j < w; j += kSolveThreads) chol_solve(c2, r, n, pm + static_cast<int64_t>(w + j) * r, 1);
-  __syncthreads();
-  // W_enc [r, w] = E^T and W_dec [w, r] = F^T, each rounded once
-  for (int e = tid; e < r * w; e += kSolveThreads) {
-    const int k = e / w, cc = e % w;
-    store_out(jb.w_enc, e, pm[cc * r + k], bf16);
+  if (blockIdx.x == 0 && tid == 0) ldiag[k] = lkk;
+}
+
+// ---- triangular solves and outputs --------------------------------------------------------------
+// Solves (L L^T) x = b in place for one right-hand side at x[0], x[xs], ...; L[i][j] (j < i) sits
+// at l[j * sz + i], L[i][i] at diag[i].
+__device__ inline void chol_solve(const double* l, const double* diag, int sz, double* x, int64_t xs) {
+  for (int i = 0; i < sz; ++i) {
+    double v = x[i * xs];
+    for (int j = 0; j < i; ++j) v -= l[static_cast<int64_t>(j) * sz + i] * x[j * xs];
+    x[i * xs] = v / diag[i];
   }
-  for (int e = tid; e < w * r; e += kSolveThreads)
-    store_out(jb.w_dec, e, pm[static_cast<int64_t>(w) * r + e], bf16);
+  for (int i = sz - 1; i >= 0; --i) {
+    double v = x[i * xs];
+    for (int j = i + 1; j < sz; ++j) v -= l[static_cast<int64_t>(i) * sz + j] * x[j * xs];
+    x[i * xs] = v / diag[i];
+  }
+}
+
+// Threads [0, r): encoder column m, E[:, m] = (A^T A + lam I)^-1 P[0:w, m] -> w_enc[m, :];
+// threads [r, r + w): decoder row j, F[:, j] = (Z^T Z + lam I)^-1 P[w + j, :]^T -> w_dec[j, :].
+__global__ __launch_bounds__(64) void fit_out_kernel(const SolveArgs a) {
+  const int layer = blockIdx.y, w = a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const SolveJob jb = *s.job;
+  const int r = static_cast<int>(jb.rank);
+  const bool bf16 = a.bf16 != 0;
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  if (t < r) {
+    double* x = s.m + t;
+    chol_solve(s.x, s.ldiag, w, x, r);
+    for (int i = 0; i < w; ++i) store_out(jb.w_enc, static_cast<int64_t>(t) * w + i, x[static_cast<int64_t>(i) * r], bf16);
+  } else if (t < r + w) {
+    const int j = t - r;
+    double* x = s.m + static_cast<int64_t>(w + j) * r;
+    chol_solve(s.y, s.ldiag + w, r, x, 1);
+    for (int l = 0; l < r; ++l) store_out(jb.w_dec, static_cast<int64_t>(j) * r + l, x[l], bf16);
+  }
 }
 
 template <int DH>
@@ -911,7 +1305,38 @@ hipError_t fit_scratch(double** ptr) {
 }
 
 hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(fit_solve_kernel, dim3(p.n_jobs), dim3(kSolveThreads), 0, stream, p);
+  const int n = 2 * p.w, layers = p.n_jobs;
+  int rmax = 0;
+  for (int l = 0; l < layers; ++l) rmax = p.jobs[l].rank > rmax ? p.jobs[l].rank : rmax;
+  const dim3 block(kSolveThreads), wave(64);
+  SolveArgs a{p.work, static_cast<double>(p.n_rows), p.lambda, p.w, 0, p.center, p.bf16};
+  hipLaunchKernelGGL(fit_prep_kernel, dim3((n + kSolveRows - 1) / kSolveRows, layers), block, 0,
+                     stream, p);
+  for (int k = -1; k <= n - 3; ++k) {
+    a.step = k;
+    const int rows = n - k - 2;
+    hipLaunchKernelGGL(fit_tridiag_kernel, dim3((rows + kSolveRows - 1) / kSolveRows, layers),
+                       block, 0, stream, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned rt = static_cast<unsigned>((rmax + 63) / 64);
+  hipLaunchKernelGGL(fit_bisect_kernel, dim3(rt, layers), wave, 0, stream, a);
+  hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
+  hipLaunchKernelGGL(fit_back_kernel, dim3((rmax + kBackCols - 1) / kBackCols, layers), block, 0,
+                     stream, a);
+  hipLaunchKernelGGL(fit_project_kernel, dim3(n / 64, rt, layers), block, 0, stream, a);
+  const unsigned tw = static_cast<unsigned>(p.w / 64);
+  hipLaunchKernelGGL(fit_normal_kernel, dim3(rt * rt > tw * tw ? rt * rt : tw * tw, 2, layers),
+                     block, 0, stream, a);
+  const int sz = p.w > rmax ? p.w : rmax;
+  for (int k = 0; k < sz; ++k) {
+    a.step = k;
+    const int rows = sz - k - 1;
+    const int gx = rows > 0 ? (rows + kSolveRows - 1) / kSolveRows : 1;
+    hipLaunchKernelGGL(fit_chol_kernel, dim3(gx, 2, layers), block, 0, stream, a);
+  }
+  hipLaunchKernelGGL(fit_out_kernel, dim3((rmax + p.w + 63) / 64, layers), wave, 0, stream, a);
   return hipGetLastError();
 }
 

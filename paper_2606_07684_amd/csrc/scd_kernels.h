@@ -158,14 +158,16 @@ struct FitSolveParams {
   double lambda;
   int32_t center;
   int32_t bf16;
-  int32_t max_sweeps;
-  int32_t reserved;
-  double* work;  // [n_jobs][3][2w][2w] fp64
+  double* work;  // n_jobs x fit_solve_layer_doubles(w) fp64
 };
 static_assert(sizeof(FitSolveParams) <= 4096, "kernel argument block");
 
-// Largest basis width the solve takes (its Jacobi matrix is 2w x 2w in one workgroup).
-constexpr int kFitMaxSolveWidth = 256;
+// Largest basis width the solve takes (w = D = 1024 for a model with 8 KV heads of 128).
+constexpr int kFitMaxSolveWidth = 1024;
+// fp64 workspace of the solve per layer: four 2w x 2w matrices and 8 vectors of 2w.
+__host__ __device__ constexpr int64_t fit_solve_layer_doubles(int w) {
+  return 4 * (2 * static_cast<int64_t>(w)) * (2 * w) + 8 * (2 * static_cast<int64_t>(w));
+}
 
 int64_t fit_upper_tiles(int w);  // upper 128 x 128 tiles of the 2w x 2w Gram
 // bf16 with 2w = 256: one workgroup per (job, slice) computes the whole Gram

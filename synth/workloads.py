@@ -180,6 +180,10 @@ FIT_W64_BF16 = Workload("fit_w64_bf16", 2, 128, 4, 64, (150, 211), (16, 16), (0,
                         basis_width=64, ranks_v=(32, 32))
 FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KEYS, FIT_W256_BF16,
                  FIT_W64_BF16)
+# The widest basis the solve takes: w = D = 1024 (8 KV heads of 128, one basis over all heads), a
+# 2048 x 2048 Gram over 2,600 calibration rows of one Reuse layer.
+FIT_W1024_BF16 = Workload("fit_w1024_bf16", 1, 256, 8, 128, (1400, 1200), (64,), (), 5e5, "bf16",
+                          pos0=(0, 9), ranks_v=(64,))
 # Calibration at the Llama-3-8B shape with the head-shared basis: 8192 tokens x 8 heads = 65,536
 # rows of 128 channels per layer (the paper calibrates on 100-500 prefixes of ~600 tokens).
 FIT_LLAMA3_8B = LLAMA3_8B_HEAD_SHARED.replace(name="fit_llama3_8b_head_shared_bf16")

@@ -368,7 +368,7 @@ def test_fit_validation(lib):
     assert _fit_solve(lib, m, center=2)[0] == SHAPE
     assert _fit_solve(lib, _model(rank_v=[32, 32, 24]), branch=1)[0] == SCHED
     assert _fit_solve(lib, _model(rank_k=[144, 32, 32]))[0] == SCHED  # > basis width 128
-    wide = _model(n_kv_heads=6, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 384 > 256
+    wide = _model(n_kv_heads=18, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 1152 > 1024
     assert _fit_solve(lib, wide)[0] == UNSUP
     pm, keepm = _ptrs(3, skip=(0,))
     st, msg = _fit_solve(lib, m, mu_dec=pm)
@@ -379,14 +379,14 @@ def test_fit_validation(lib):
     assert st == SHAPE and "gram[2]" in msg
     st, msg = _fit_solve(lib, m, w_dec=ctypes.cast(same, ctypes.POINTER(ctypes.c_void_p)))
     assert st == SHAPE and "w_dec[2]" in msg
-    solve_need = 2 * 3 * 256 * 256 * 8  # two Reuse layers, w = 128
+    solve_need = 2 * (4 * 256 * 256 + 8 * 256) * 8  # two Reuse layers, w = 128
     st, msg = _fit_solve(lib, m, ws_bytes=solve_need - 8)
     assert st == SHAPE and "workspace" in msg
 
 
 def test_fit_workspace_bytes_cover_both_calls(lib):
     # Gram partials: jobs x slices x upper tiles x (128^2 + 128) floats, slices = 1024 // units
-    # capped by one per 512 rows; solve: 3 (2w)^2 doubles
+    # capped by one per 512 rows; solve: 4 (2w)^2 + 8 (2w) doubles
     # per job.  One Reuse-only model, w = 128 (one 256 x 256 Gram = 3 upper tiles).
     # bf16 with w = 128 takes the whole-Gram kernel: one workgroup per (layer, slice), 512 // jobs
     m = _model(is_patch=[0, 0, 0])
@@ -397,7 +397,7 @@ def test_fit_workspace_bytes_cover_both_calls(lib):
         sr = -(-sr // 64) * 64
         ns = -(-T // sr)
         gram = 3 * ns * 3 * (128 * 128 + 128) * 4
-        solve = 3 * 3 * 256 * 256 * 8
+        solve = 3 * (4 * 256 * 256 + 8 * 256) * 8
         assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), T) == max(gram, solve)
     assert lib.scd_fit_workspace_bytes(ctypes.byref(m._c), 0) == 0
 
@@ -428,8 +428,12 @@ def test_fit_solve_noalloc_validation(lib):
     assert call(m, lam=float("inf"))[0] == SHAPE
     assert call(m, center=3)[0] == SHAPE
     assert call(_model(rank_k=[144, 32, 32]))[0] == SCHED
-    wide = _model(n_kv_heads=6, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 384
+    wide = _model(n_kv_heads=18, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)  # w = 1152
     assert call(wide)[0] == UNSUP
+    # w = 768: 4 (2w)^2 + 8 (2w) doubles per layer (75.6 MB) exceed the 64 MiB scratch array
+    big = _model(n_kv_heads=12, head_dim=64, rank_k=[32] * 3, rank_v=[32] * 3)
+    st, msg = call(big)
+    assert st == WS and "scratch" in msg
     pm, keepm = _ptrs(3, skip=(2,))
     st, msg = call(m, gram=pm)
     assert st == NULL and "gram[2]" in msg

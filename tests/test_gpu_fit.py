@@ -94,7 +94,7 @@ def _well_conditioned(wl, branch):
 
 
 @pytest.mark.parametrize("branch", ["k", "v"])
-@pytest.mark.parametrize("wl", W.FIT_WORKLOADS, ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [*W.FIT_WORKLOADS, W.FIT_W1024_BF16], ids=lambda w: w.name)
 def test_fit_solve_matches_oracle(wl, branch):
     dev = torch.device("cuda")
     model, batch = U.model_of(wl), U.batch_of(wl, dev)

@@ -54,8 +54,8 @@ def _gpu():
 def test_noalloc_solve_matches_workspace_solve_twice():
     dev = torch.device("cuda")
     assert scd.scd_fit_solve_noalloc_max_bytes() == 64 << 20
-    # (layers, heads, head_dim, rank, rows): 11 layers at w = 256 need 6 MiB each, so the scratch
-    # array takes 10 per launch and the call makes two launches; the second call is smaller.
+    # (layers, heads, head_dim, rank, rows): 11 layers at w = 256 need 8.4 MB each, so the
+    # scratch array takes 7 per launch and the call makes two launches; the second call is smaller.
     cases = [(11, 2, 128, 64, 2000), (3, 2, 64, 32, 700)]
     for i, (L, heads, hd, rank, n_rows) in enumerate(cases):
         model = _model(L, heads, hd, rank)
