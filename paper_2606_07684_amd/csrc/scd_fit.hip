@@ -754,43 +754,73 @@ __global__ __launch_bounds__(kSolveThreads) void fit_prep_kernel(const FitSolveP
 // Source A^(k): G_c (Z) for k <= 0, else the previous launch's destination; destination: X for even
 // k, Y for odd k.  Reflector k+1 goes into row k+1 of the destination, a row no later launch
 // writes; p alternates between two vectors.
-__global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveArgs a) {
+// Every global load of a launch is issued at its start (the reflector and p of the previous launch,
+// row k+1 and, for n <= 64 PRE, this workgroup's rows of the source), so the launch waits on one
+// round of loads rather than three.
+template <int PRE>
+__device__ __forceinline__ void tridiag_step(const SolveArgs& a) {
   __shared__ double vk[kMaxN], wk[kMaxN], vn[kMaxN];
-  __shared__ double red[kSolveThreads / 64];
+  __shared__ double red[2][kSolveThreads / 64];
   const int layer = blockIdx.y, n = 2 * a.w, k = a.step, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  constexpr int kWaves = kSolveThreads / 64, kRowsPerWave = kSolveRows / kWaves;
   const Slots s = slots(a.work, a.w, layer);
   const double* src = k <= 0 ? s.z : ((k - 1) & 1 ? s.y : s.x);
   double* dst = (k & 1) ? s.y : s.x;  // k = -1 is odd: Y (only its reflector row is written)
   double* p_next = ((k + 1) & 1) ? s.p1 : s.p0;
-  // w_k (zero for launch -1)
+  const int r0 = k + 2 + blockIdx.x * kSolveRows;
+  // loads: reflector k and p_k into vk / wk, row k+1 of the source into vn, own rows to registers
   if (k >= 0) {
     const double* vrow = reflector_rows(s, k) + static_cast<int64_t>(k) * n;
     const double* p_cur = (k & 1) ? s.p1 : s.p0;
-    double dot = 0.0;
     for (int i = k + 1 + tid; i < n; i += kSolveThreads) {
-      const double v = vrow[i], pv = p_cur[i];
-      vk[i] = v;
-      wk[i] = pv;
-      dot += pv * v;
+      vk[i] = vrow[i];
+      wk[i] = p_cur[i];
     }
-    const double kk = 0.5 * s.tau[k] * block_sum(dot, red);
-    for (int i = k + 1 + tid; i < n; i += kSolveThreads) wk[i] -= kk * vk[i];
   } else {
     for (int i = tid; i < n; i += kSolveThreads) vk[i] = wk[i] = 0.0;
   }
+  const double* row1 = src + static_cast<int64_t>(k + 1) * n;
+  for (int i = k + 1 + tid; i < n; i += kSolveThreads) vn[i] = row1[i];
+  double pre[PRE > 0 ? kRowsPerWave : 1][PRE > 0 ? PRE : 1];
+  if constexpr (PRE > 0) {
+    for (int q = 0; q < kRowsPerWave; ++q) {
+      const int i = r0 + wave + kWaves * q;
+      for (int u = 0; u < PRE; ++u) {
+        const int j = k + 2 + lane + 64 * u;
+        pre[q][u] = (i < n && j < n) ? src[static_cast<int64_t>(i) * n + j] : 0.0;
+      }
+    }
+  }
   __syncthreads();
-  // column k+1 of A^(k+1), read as row k+1 (the matrix is symmetric)
-  const double vk1 = vk[k + 1], wk1 = wk[k + 1];
-  const double* row = src + static_cast<int64_t>(k + 1) * n;
+  // w_k = p_k - (tau_k / 2)(p_k . v_k) v_k (zero for launch -1)
+  double kk = 0.0;
+  if (k >= 0) {
+    double dot = 0.0;
+    for (int i = k + 1 + tid; i < n; i += kSolveThreads) dot += wk[i] * vk[i];
+    dot = wave_sum(dot);
+    if (lane == 0) red[0][wave] = dot;
+    __syncthreads();
+    double t = 0.0;
+    for (int q = 0; q < kWaves; ++q) t += red[0][q];
+    kk = 0.5 * s.tau[k] * t;
+  }
+  const double vk1 = vk[k + 1], wk1 = wk[k + 1] - kk * vk1;
+  // column k+1 of A^(k+1) (row k+1, the matrix being symmetric) and w_k, own entries only
   double sig = 0.0;
   for (int i = k + 1 + tid; i < n; i += kSolveThreads) {
-    const double c = row[i] - vk1 * wk[i] - wk1 * vk[i];
+    const double wi = wk[i] - kk * vk[i];
+    if (i > k + 1) wk[i] = wi;  // entry k+1 stays p_k's: every thread reads it above
+    const double c = vn[i] - vk1 * wi - wk1 * vk[i];
     vn[i] = c;
     if (i >= k + 3) sig += c * c;
   }
-  const double sigma = block_sum(sig, red);  // its barrier also publishes vn
+  sig = wave_sum(sig);
+  if (lane == 0) red[1][wave] = sig;
+  __syncthreads();
+  double sigma = 0.0;
+  for (int q = 0; q < kWaves; ++q) sigma += red[1][q];
   const double d_next = vn[k + 1], alpha = vn[k + 2];
-  __syncthreads();  // every thread has read alpha before v_0 = 1 replaces it
   double tau = 0.0, beta = alpha, scale = 0.0;
   if (!(sigma == 0.0)) {
     const double norm = sqrt(alpha * alpha + sigma);
@@ -798,35 +828,53 @@ __global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveA
     tau = (beta - alpha) / beta;
     scale = 1.0 / (alpha - beta);
   }
+  // v_{k+1}: entries past its first scaled in place; its first entry (1) is never stored in vn,
+  // so alpha stays readable
   for (int i = k + 3 + tid; i < n; i += kSolveThreads) vn[i] *= scale;
-  if (tid == 0) vn[k + 2] = 1.0;
   __syncthreads();
   // this workgroup's rows of A^(k+1) and of p_{k+1}
-  const int lane = tid & 63, wave = tid >> 6;
-  const int r0 = k + 2 + blockIdx.x * kSolveRows;
-  for (int i = r0 + wave; i < r0 + kSolveRows && i < n; i += kSolveThreads / 64) {
+  for (int q = 0; q < kRowsPerWave; ++q) {
+    const int i = r0 + wave + kWaves * q;
+    if (i >= n || i >= r0 + kSolveRows) break;
     const double* arow = src + static_cast<int64_t>(i) * n;
     double* orow = dst + static_cast<int64_t>(i) * n;
     const double vi = vk[i], wi = wk[i];
     double acc = 0.0;
-    for (int j = k + 2 + lane; j < n; j += 64) {
-      const double v = arow[j] - vi * wk[j] - wi * vk[j];
+    auto entry = [&](int j, double x) {
+      const double v = x - vi * wk[j] - wi * vk[j];
       if (k >= 0) orow[j] = v;
       if (k == n - 3) s.d[n - 1] = v;  // the last launch: i = j = n - 1
-      acc += v * vn[j];
+      acc += v * (j == k + 2 ? 1.0 : vn[j]);
+    };
+    if constexpr (PRE > 0) {
+#pragma unroll
+      for (int u = 0; u < PRE; ++u) {
+        const int j = k + 2 + lane + 64 * u;
+        if (j < n) entry(j, pre[q][u]);
+      }
+    } else {
+      for (int j = k + 2 + lane; j < n; j += 64) entry(j, arow[j]);
     }
     acc = wave_sum(acc);
     if (lane == 0) p_next[i] = tau * acc;
   }
   if (blockIdx.x == 0) {
     double* vrow = dst + static_cast<int64_t>(k + 1) * n;
-    for (int i = k + 2 + tid; i < n; i += kSolveThreads) vrow[i] = vn[i];
+    for (int i = k + 2 + tid; i < n; i += kSolveThreads) vrow[i] = i == k + 2 ? 1.0 : vn[i];
     if (tid == 0) {
       s.d[k + 1] = d_next;
       s.e[k + 1] = beta;
       s.tau[k + 1] = tau;
     }
   }
+}
+
+constexpr int kTridiagPre = 8;  // row entries per lane held in registers: n <= 512
+__global__ __launch_bounds__(kSolveThreads) void fit_tridiag_pre_kernel(const SolveArgs a) {
+  tridiag_step<kTridiagPre>(a);
+}
+__global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveArgs a) {
+  tridiag_step<0>(a);
 }
 
 // ---- bisection -------------------------------------------------------------------------------
@@ -859,8 +907,12 @@ __device__ inline void gershgorin(const double* d, const double* ae, int n, doub
   }
 }
 
-// One wave per workgroup, one eigenvalue per thread: lam[j] = the (j+1)-th largest, found to an
-// absolute 2^-52 ||T|| plus a relative 2^-51.
+// One wave per workgroup, four eigenvalues per wave, each by 16 lanes: lam[j] = the (j+1)-th
+// largest.  Every round the 16 lanes take Sturm counts at 16 evenly spaced interior points of the
+// bracket, which then shrinks to the pair of neighbouring points (ends included) between which the
+// count passes j's ascending index: a 17-fold cut per round, until the bracket is below an absolute
+// 2^-52 ||T|| plus a relative 2^-51.
+constexpr int kSectionLanes = 16;
 __global__ __launch_bounds__(64) void fit_bisect_kernel(const SolveArgs a) {
   __shared__ double d[kMaxN], e2[kMaxN], ae[kMaxN];
   const int layer = blockIdx.y, n = 2 * a.w;
@@ -878,18 +930,30 @@ __global__ __launch_bounds__(64) void fit_bisect_kernel(const SolveArgs a) {
   // a floor keeps the tolerances positive for an all-zero matrix
   const double tnorm = fmax(fmax(fabs(lo0), fabs(hi0)), 1e-280);
   if (blockIdx.x == 0 && threadIdx.x == 0) s.job->tnorm = tnorm;
-  const int j = blockIdx.x * 64 + threadIdx.x;
-  if (j >= r) return;
+  const int lane = threadIdx.x & (kSectionLanes - 1);
+  const int j = blockIdx.x * (64 / kSectionLanes) + threadIdx.x / kSectionLanes;
+  // the 16 lanes of an eigenvalue share every branch below; whole groups past r are idle
+  const bool live = j < r;
   const double atol = kEps * tnorm, pivmin = kEps * tnorm;
   const int t = n - 1 - j;  // ascending index
   double lo = lo0 - atol, hi = hi0 + atol;
-  for (int it = 0; it < 128; ++it) {
+  for (int it = 0; it < 64; ++it) {
     if (hi - lo <= atol + 2.0 * kEps * fmax(fabs(lo), fabs(hi))) break;
-    const double mid = 0.5 * (lo + hi);
-    if (sturm_count(d, e2, n, mid, pivmin) <= t) lo = mid;
-    else hi = mid;
+    // point k = 1 .. 16 at lo + k step; the new ends are points (or the old ends), so the counts
+    // already taken there hold for them
+    const double step = (hi - lo) * (1.0 / (kSectionLanes + 1));
+    const double x = lo + step * (lane + 1);
+    const bool below = live && sturm_count(d, e2, n, x, pivmin) <= t;
+    // lanes of this group whose point lies below the eigenvalue (a prefix of the group)
+    const uint64_t m = __ballot(below);
+    const int group = threadIdx.x & ~(kSectionLanes - 1);
+    const int kb = __popcll((m >> group) & ((1ull << kSectionLanes) - 1));
+    const double nlo = kb > 0 ? lo + step * kb : lo;
+    const double nhi = kb < kSectionLanes ? lo + step * (kb + 1) : hi;
+    lo = nlo;
+    hi = nhi;
   }
-  s.lam[j] = 0.5 * (lo + hi);
+  if (live && lane == 0) s.lam[j] = 0.5 * (lo + hi);
 }
 
 // ---- inverse iteration --------------------------------------------------------------------------
@@ -1171,7 +1235,8 @@ __global__ __launch_bounds__(kSolveThreads) void fit_normal_kernel(const SolveAr
 // ---- Cholesky, one column per launch --------------------------------------------------------------
 // grid.y = 0: A^T A + lam I (X, size w), 1: Z^T Z + lam I (Y, size r).  Step k reads column k on and
 // below the diagonal, updates rows (k, s) of the lower triangle (a workgroup's kSolveRows rows), and
-// stores L[i][k] at [k][i] in the upper triangle, which nothing reads before the solves; L[k][k]
+// stores L[i][k] twice, in places nothing reads before the solves: at [k][i] in the upper triangle
+// (column k of L as a row) and at [i][k] of a row-major copy of L just past the matrix.  L[k][k]
 // goes to ldiag.  A non-positive pivot leaves NaN, which reaches every output of the layer.
 __global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs a) {
   __shared__ double lc[kFitMaxSolveWidth];
@@ -1193,45 +1258,75 @@ __global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs
     const double li = lc[i];
     double* row = mat + static_cast<int64_t>(i) * sz;
     for (int j = k + 1 + lane; j <= i; j += 64) row[j] -= li * lc[j];
-    if (lane == 0) mat[static_cast<int64_t>(k) * sz + i] = li;
+    if (lane == 0) {
+      mat[static_cast<int64_t>(k) * sz + i] = li;
+      mat[static_cast<int64_t>(sz) * sz + static_cast<int64_t>(i) * sz + k] = li;
+    }
   }
   if (blockIdx.x == 0 && tid == 0) ldiag[k] = lkk;
 }
 
 // ---- triangular solves and outputs --------------------------------------------------------------
-// Solves (L L^T) x = b in place for one right-hand side at x[0], x[xs], ...; L[i][j] (j < i) sits
-// at l[j * sz + i], L[i][i] at diag[i].
-__device__ inline void chol_solve(const double* l, const double* diag, int sz, double* x, int64_t xs) {
+__device__ inline double readlane_f64(double v, int lane) {
+  const int64_t b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), lane);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), lane);
+  return __longlong_as_double((static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo));
+}
+
+// One wave solves (L L^T) x = b for one right-hand side held in LDS (xs[i], lane i % 64 owns
+// entry i, so every LDS access is the lane's own).  Forward L y = b column by column: y_i =
+// b_i / L_ii, then b_j -= L[j][i] y_i for j > i with column i of L read as row i of the upper
+// triangle (`lu`, contiguous).  Backward L^T x = y the same way from the bottom: x_i = y_i / L_ii,
+// then y_j -= L[i][j] x_i for j < i with row i of L read from the row-major copy (`lr`).  The
+// entry of step i is broadcast from its owner lane.
+__device__ inline void wave_chol_solve(const double* lu, const double* lr, const double* diag,
+                                       int sz, double* xs) {
+  const int lane = threadIdx.x & 63;
   for (int i = 0; i < sz; ++i) {
-    double v = x[i * xs];
-    for (int j = 0; j < i; ++j) v -= l[static_cast<int64_t>(j) * sz + i] * x[j * xs];
-    x[i * xs] = v / diag[i];
+    double own = 0.0;
+    if ((i & 63) == lane) {
+      own = xs[i] / diag[i];
+      xs[i] = own;
+    }
+    const double yi = readlane_f64(own, i & 63);
+    const double* col = lu + static_cast<int64_t>(i) * sz;
+    for (int j = i + 1 + ((lane - i - 1) & 63); j < sz; j += 64) xs[j] -= col[j] * yi;
   }
   for (int i = sz - 1; i >= 0; --i) {
-    double v = x[i * xs];
-    for (int j = i + 1; j < sz; ++j) v -= l[static_cast<int64_t>(i) * sz + j] * x[j * xs];
-    x[i * xs] = v / diag[i];
+    double own = 0.0;
+    if ((i & 63) == lane) {
+      own = xs[i] / diag[i];
+      xs[i] = own;
+    }
+    const double xi = readlane_f64(own, i & 63);
+    const double* row = lr + static_cast<int64_t>(i) * sz;
+    for (int j = lane; j < i; j += 64) xs[j] -= row[j] * xi;
   }
 }
 
-// Threads [0, r): encoder column m, E[:, m] = (A^T A + lam I)^-1 P[0:w, m] -> w_enc[m, :];
-// threads [r, r + w): decoder row j, F[:, j] = (Z^T Z + lam I)^-1 P[w + j, :]^T -> w_dec[j, :].
-__global__ __launch_bounds__(64) void fit_out_kernel(const SolveArgs a) {
-  const int layer = blockIdx.y, w = a.w;
+// One wave per right-hand side, four per workgroup.  Waves [0, r): encoder column m,
+// E[:, m] = (A^T A + lam I)^-1 P[0:w, m] -> w_enc[m, :]; waves [r, r + w): decoder row j,
+// F[:, j] = (Z^T Z + lam I)^-1 P[w + j, :]^T -> w_dec[j, :].
+__global__ __launch_bounds__(kSolveThreads) void fit_out_kernel(const SolveArgs a) {
+  __shared__ double xs_all[kSolveThreads / 64][kFitMaxSolveWidth];
+  const int layer = blockIdx.y, w = a.w, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const Slots s = slots(a.work, a.w, layer);
   const SolveJob jb = *s.job;
   const int r = static_cast<int>(jb.rank);
   const bool bf16 = a.bf16 != 0;
-  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int t = blockIdx.x * (kSolveThreads / 64) + wave;
+  double* xs = xs_all[wave];
   if (t < r) {
-    double* x = s.m + t;
-    chol_solve(s.x, s.ldiag, w, x, r);
-    for (int i = 0; i < w; ++i) store_out(jb.w_enc, static_cast<int64_t>(t) * w + i, x[static_cast<int64_t>(i) * r], bf16);
+    for (int i = lane; i < w; i += 64) xs[i] = s.m[static_cast<int64_t>(i) * r + t];
+    wave_chol_solve(s.x, s.x + static_cast<int64_t>(w) * w, s.ldiag, w, xs);
+    for (int i = lane; i < w; i += 64) store_out(jb.w_enc, static_cast<int64_t>(t) * w + i, xs[i], bf16);
   } else if (t < r + w) {
     const int j = t - r;
-    double* x = s.m + static_cast<int64_t>(w + j) * r;
-    chol_solve(s.y, s.ldiag + w, r, x, 1);
-    for (int l = 0; l < r; ++l) store_out(jb.w_dec, static_cast<int64_t>(j) * r + l, x[l], bf16);
+    const double* b = s.m + static_cast<int64_t>(w + j) * r;
+    for (int l = lane; l < r; l += 64) xs[l] = b[l];
+    wave_chol_solve(s.y, s.y + static_cast<int64_t>(r) * r, s.ldiag + w, r, xs);
+    for (int l = lane; l < r; l += 64) store_out(jb.w_dec, static_cast<int64_t>(j) * r + l, xs[l], bf16);
   }
 }
 
@@ -1315,13 +1410,14 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   for (int k = -1; k <= n - 3; ++k) {
     a.step = k;
     const int rows = n - k - 2;
-    hipLaunchKernelGGL(fit_tridiag_kernel, dim3((rows + kSolveRows - 1) / kSolveRows, layers),
-                       block, 0, stream, a);
+    const dim3 grid((rows + kSolveRows - 1) / kSolveRows, layers);
+    if (n <= 64 * kTridiagPre) hipLaunchKernelGGL(fit_tridiag_pre_kernel, grid, block, 0, stream, a);
+    else hipLaunchKernelGGL(fit_tridiag_kernel, grid, block, 0, stream, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned rt = static_cast<unsigned>((rmax + 63) / 64);
-  hipLaunchKernelGGL(fit_bisect_kernel, dim3(rt, layers), wave, 0, stream, a);
+  hipLaunchKernelGGL(fit_bisect_kernel, dim3((rmax + 3) / 4, layers), wave, 0, stream, a);
   hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
   hipLaunchKernelGGL(fit_back_kernel, dim3((rmax + kBackCols - 1) / kBackCols, layers), block, 0,
                      stream, a);
@@ -1336,7 +1432,9 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
     const int gx = rows > 0 ? (rows + kSolveRows - 1) / kSolveRows : 1;
     hipLaunchKernelGGL(fit_chol_kernel, dim3(gx, 2, layers), block, 0, stream, a);
   }
-  hipLaunchKernelGGL(fit_out_kernel, dim3((rmax + p.w + 63) / 64, layers), wave, 0, stream, a);
+  constexpr int kWaves = kSolveThreads / 64;
+  hipLaunchKernelGGL(fit_out_kernel, dim3((rmax + p.w + kWaves - 1) / kWaves, layers), block, 0,
+                     stream, a);
   return hipGetLastError();
 }
 
