@@ -241,9 +241,12 @@ class Batch:
 
 @dataclasses.dataclass
 class RopeTable:
-    """Device RoPE table filled by :func:`scd_rope_table` for positions ``[0, max_position)``."""
+    """Device RoPE table filled by :func:`scd_rope_table` for positions ``[0, max_position)`` of a
+    model with ``head_dim`` and ``rope_theta``; entry points check it against their model."""
     buffer: torch.Tensor
     max_position: int
+    head_dim: int
+    rope_theta: float
 
 
 def _stream(stream) -> Optional[int]:
@@ -293,7 +296,7 @@ def scd_rope_table(model: Model, max_position: int, device=None, stream=None) ->
     buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
     _check(lib.scd_rope_table(ctypes.byref(model._c), int(max_position), buf.data_ptr(), nbytes,
                               _stream(stream)))
-    return RopeTable(buf, int(max_position))
+    return RopeTable(buf, int(max_position), int(model.head_dim), float(model.rope_theta))
 
 
 def scd_positions(batch: Batch, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
@@ -325,10 +328,23 @@ def scd_payload_bytes(model: Model, n_tokens: int):
     return total, list(offs)
 
 
-def _rope_args(rope: Optional[RopeTable]):
+def _rope_args(rope: Optional[RopeTable], model: "Model"):
+    """Device pointer and max_position of a RoPE table built for this model (its head_dim and
+    theta) and large enough for its max_position; the library reads max_position * head_dim / 2
+    (cos, sin) pairs from it."""
     if rope is None:
         return None, 0
-    return rope.buffer.data_ptr(), rope.max_position
+    if rope.head_dim != model.head_dim or rope.rope_theta != model.rope_theta:
+        raise ValueError(f"RoPE table was built for head_dim {rope.head_dim}, theta "
+                         f"{rope.rope_theta}; the model has {model.head_dim}, {model.rope_theta}")
+    buf = rope.buffer
+    if not isinstance(buf, torch.Tensor) or not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("RoPE table buffer must be a contiguous CUDA tensor")
+    need = int(load_library().scd_rope_table_bytes(ctypes.byref(model._c), int(rope.max_position)))
+    if need == 0 or buf.numel() * buf.element_size() < need:
+        raise ValueError(f"RoPE table holds {buf.numel() * buf.element_size()} bytes; "
+                         f"max_position {rope.max_position} needs {need}")
+    return buf.data_ptr(), rope.max_position
 
 
 class Prepared:
@@ -363,7 +379,7 @@ def prepare_encode(model: Model, batch: Batch, rope: Optional[RopeTable], k_in, 
         _ptr_array(z_v, L, "z_v", {l: (T * g, model.rank_v[l]) for l in R}, dt),
         _ptr_array(z_h, L, "z_h", {l: (T, model.rank_h[l]) for l in P}, dt),
     ]
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return Prepared(lib.scd_encode, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
                                      *[_as_pp(a) for a in args]), (model, batch, rope, args))
 
@@ -390,7 +406,7 @@ def prepare_reuse_decode(model: Model, batch: Batch, rope: Optional[RopeTable], 
         _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in R}, dt),
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in R}, dt),
     ]
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return Prepared(lib.scd_reuse_decode, (ctypes.byref(model._c), ctypes.byref(batch._c), tab,
                                            maxp, *[_as_pp(a) for a in args]),
                     (model, batch, rope, args))
@@ -417,7 +433,7 @@ def prepare_patch_kv(model: Model, batch: Batch, rope: Optional[RopeTable], h_ha
         _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in P}, dt),
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in P}, dt),
     ]
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return Prepared(lib.scd_patch_kv, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
                                        *[_as_pp(a) for a in args]), (model, batch, rope, args))
 
@@ -506,7 +522,7 @@ def prepare_patch_kv_from_codes(model: Model, batch: Batch, rope: Optional[RopeT
         _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in P}, dt),
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in P}, dt),
     ]
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return Prepared(lib.scd_patch_kv_from_codes,
                     (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp, int(hidden),
                      *[_as_pp(a) for a in args]), (model, batch, rope, args))
@@ -579,7 +595,7 @@ def prepare_reuse_decode_streamed(model: Model, batch: Batch, rope: Optional[Rop
         _ptr_array(k_cache, L, "k_cache", {l: (T, D) for l in R}, dt),
         _ptr_array(v_cache, L, "v_cache", {l: (T, D) for l in R}, dt),
     ]
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return PreparedStreamed(lib.scd_reuse_decode_streamed,
                             (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
                              payload_src.data_ptr(), payload_dst.data_ptr(),
@@ -634,7 +650,7 @@ def prepare_fit_gram(model: Model, batch: Batch, rope: Optional[RopeTable], bran
         _ptr_array(colsum, L, "colsum", {l: (2 * w,) for l in R}, torch.float32),
     ]
     ws, nbytes = _workspace_arg(workspace)
-    tab, maxp = _rope_args(rope)
+    tab, maxp = _rope_args(rope, model)
     return Prepared(lib.scd_fit_gram, (ctypes.byref(model._c), ctypes.byref(batch._c), tab, maxp,
                                        int(branch), *[_as_pp(a) for a in args], ws, nbytes),
                     (model, batch, rope, args, workspace))

@@ -493,3 +493,23 @@ def test_fold_and_patch_from_codes_validation(lib):
     assert codes(ck=r) == ALIGN
     assert codes(model=_model(rank_h=[32, 24, 32])) == SCHED
     assert codes(z=q, act=q, kc=q, vc=q, batch=_batch(n_tokens=0)) == OK
+
+
+def test_rope_table_is_checked_against_the_model(lib):
+    # The binding refuses a RoPE table built for another head_dim or theta, one smaller than its
+    # max_position needs, and one that is not device memory (checked before any call).
+    import torch
+
+    m = _model()  # head_dim 64, theta 1e4
+    need = int(lib.scd_rope_table_bytes(ctypes.byref(m._c), 100))
+    assert need == 100 * 32 * 8
+    cpu = scd.RopeTable(torch.empty(need, dtype=torch.uint8), 100, m.head_dim, m.rope_theta)
+    with pytest.raises(ValueError, match="CUDA"):
+        scd._rope_args(cpu, m)
+    other = scd.RopeTable(torch.empty(need, dtype=torch.uint8), 100, 128, m.rope_theta)
+    with pytest.raises(ValueError, match="head_dim 128"):
+        scd._rope_args(other, m)
+    theta = scd.RopeTable(torch.empty(need, dtype=torch.uint8), 100, m.head_dim, 5e5)
+    with pytest.raises(ValueError, match="theta"):
+        scd._rope_args(theta, m)
+    assert scd._rope_args(None, m) == (None, 0)

@@ -44,6 +44,16 @@ def test_rope_table_is_fp64_rounded_once():
     print("rope table exact fraction:", np.mean(got[..., 0] == want_c), flush=True)
 
 
+def test_rope_table_too_small_is_refused():
+    wl = W.SMALL_BF16
+    model = U.model_of(wl)
+    tab = scd.scd_rope_table(model, 64)
+    short = scd.RopeTable(tab.buffer[:-8], 64, tab.head_dim, tab.rope_theta)
+    with pytest.raises(ValueError, match="needs"):
+        scd._rope_args(short, model)
+    assert scd._rope_args(tab, model) == (tab.buffer.data_ptr(), 64)
+
+
 def test_positions_bit_exact():
     lens = [0, 5, 1, 0, 300, 17, 0]
     cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
