@@ -4,9 +4,7 @@ None of these re-type the oracle's formulas: RoPE is checked against complex mul
 a matrix exponential, closed-form points and its group properties; the linear maps against
 explicit loops, exact round trips, in-subspace recovery and the Eckart-Young tail energy.
 """
-import json
 import math
-import os
 
 import numpy as np
 import pytest
@@ -14,7 +12,6 @@ import scipy.linalg
 
 from oracle import scd_oracle as O
 
-GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 # ------------------------------------------------------------------------------------------
