@@ -365,14 +365,15 @@ scd_status_t scd_encode(const scd_model_t* model, const scd_batch_t* batch,
   };
   auto enc = [&](const scd::GemmParams& p) { return scd::launch_encode_bf16(p, stream); };
   if (fast_kv) {
-    SCD_TRY(run_groups(kv_base, scd::kEncodeRows, 256, group_by(kv_jobs, by_kind), enc, "encode"));
+    // tiles of 128 code columns: a rank above 128 takes two workgroups per row tile
+    SCD_TRY(run_groups(kv_base, scd::kEncodeRows, 128, group_by(kv_jobs, by_kind), enc, "encode"));
   } else {
     JobPacker jp(kv_base, scd::kGenericBM, scd::kGenericBN);
     for (const auto& j : kv_jobs) jp.add(j);
     SCD_TRY(run(scd::Op::kEncodeKV, jp.build(), model->dtype, stream));
   }
   if (fast_h)
-    return run_groups(h_base, scd::kEncodeRows, 256, group_by(h_jobs, by_kind), enc, "encode");
+    return run_groups(h_base, scd::kEncodeRows, 128, group_by(h_jobs, by_kind), enc, "encode");
   JobPacker hp(h_base, scd::kGenericBM, scd::kGenericBN);
   for (const auto& j : h_jobs) hp.add(j);
   return run(scd::Op::kEncodeH, hp.build(), model->dtype, stream);

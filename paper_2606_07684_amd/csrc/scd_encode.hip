@@ -2,8 +2,9 @@
 //   Z_K = (rows(deRoPE(K)) - mu_K) W_enc,K^T,   Z_V = (rows(V) - mu_V) W_enc,V^T,   Z_H = H W_enc,H^T
 // The step is bound by HBM reads of the K/V/H inputs (the codes are r/w of that traffic).
 //
-// A workgroup of 4 waves owns 128 input rows of one layer-branch and produces all RB*32 code
-// columns for them.  Every wave streams its 32 rows straight from HBM into registers, 128 input
+// A workgroup of 4 waves owns 128 input rows of one layer-branch and produces up to 128 code
+// columns for them (RB*32; a rank above 128 takes two workgroups per row tile, so every instance
+// keeps two waves per SIMD).  Every wave streams its 32 rows straight from HBM into registers, 128 input
 // columns (one chunk) at a time, one chunk ahead of use.  With deRoPE each lane loads the same
 // 8 columns of both halves of a head, so every rotation pair meets in one lane; the rotated values
 // are rounded to bf16 and used directly as the B operand of v_mfma_f32_32x32x16_bf16 (without
@@ -60,13 +61,20 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
 
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
   const GemmJob job = p.jobs[job_of(p, unit)];
-  const int R = job.n, K = job.k;
+  // A rank above RB*32 takes two workgroups per row tile, units 2i and 2i + 1, each producing
+  // RB*32 (or the remaining) code columns of the same rows: consecutive units run on one XCD at
+  // about the same time, so the second read of the rows mostly hits L2.
+  const int n_split = (job.n + RB * 32 - 1) / (RB * 32);  // 1 or 2
+  const int local = unit - job.tile_begin;
+  const int code0 = (local % n_split) * RB * 32;
+  const int R = job.n - code0 < RB * 32 ? job.n - code0 : RB * 32;  // code columns here
+  const int K = job.k;
   const int64_t M = p.m;
-  const int64_t row = static_cast<int64_t>(unit - job.tile_begin) * 128 + wave * 32 + (lane & 31);
+  const int64_t row = static_cast<int64_t>(local / n_split) * 128 + wave * 32 + (lane & 31);
   const bool valid = row < M;
   constexpr bool derope = DEROPE;
   const uint16_t* X = static_cast<const uint16_t*>(job.a);
-  const uint16_t* E = static_cast<const uint16_t*>(job.b);
+  const uint16_t* E = static_cast<const uint16_t*>(job.b) + static_cast<int64_t>(code0) * K;
   const uint16_t* mu = static_cast<const uint16_t*>(job.vec);
   const int nchunks = K / kChunk;
 
@@ -315,8 +323,8 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(GemmParams p) {
       for (int e = 0; e < 16; ++e) acc[b][e] -= emu[32 * b + 16 * h + e];
   }
   if (!valid) return;
-  // lane holds, for block b, code columns 32*b + 16*h + (0..15) of its row
-  uint16_t* Zo = static_cast<uint16_t*>(job.c) + row * R;
+  // lane holds, for block b, code columns code0 + 32*b + 16*h + (0..15) of its row
+  uint16_t* Zo = static_cast<uint16_t*>(job.c) + row * job.n + code0;
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
     const int c0 = 32 * b + 16 * h;
@@ -366,11 +374,9 @@ hipError_t launch_kind(bool derope, bool mu, int head_dim, const GemmParams& p, 
 
 }  // namespace
 
-// Code blocks of 32 the kernel instance for `max_rank` computes (a template parameter).
-int encode_code_blocks(int max_rank) {
-  const int rb = (max_rank + 31) / 32;
-  return rb <= 2 ? 2 : (rb <= 4 ? 4 : 8);
-}
+// Code blocks of 32 the kernel instance for `max_rank` computes (a template parameter); ranks
+// above 128 take two workgroups of 4 blocks per row tile.
+int encode_code_blocks(int max_rank) { return max_rank <= 64 ? 2 : 4; }
 
 size_t encode_bf16_lds_bytes(int code_blocks, int k, bool mu) {
   return static_cast<size_t>(2) * code_blocks * 32 * kLdcPad * 2 +
@@ -395,8 +401,7 @@ hipError_t launch_encode_bf16(const GemmParams& p, hipStream_t stream) {
   const int rb = encode_code_blocks(max_r);
   const size_t lds = encode_bf16_lds_bytes(rb, k, mu);
   if (rb == 2) return launch_kind<2>(derope, mu, p.head_dim, p, lds, stream);
-  if (rb == 4) return launch_kind<4>(derope, mu, p.head_dim, p, lds, stream);
-  return launch_kind<8>(derope, mu, p.head_dim, p, lds, stream);
+  return launch_kind<4>(derope, mu, p.head_dim, p, lds, stream);
 }
 
 }  // namespace scd
