@@ -60,9 +60,6 @@ __device__ inline void tile_of(int tile, int nt, int& ti, int& tj) {
   }
   tj = ti + rem;
 }
-__device__ inline int upper_index(int ti, int tj, int nt) {
-  return ti * nt - ti * (ti - 1) / 2 + (tj - ti);
-}
 
 // First column (inside a 128-column block) of chunk pair cp: VEC columns of one head's first half;
 // their RoPE partners sit d_h/2 further on.  A block holds 128 / d_h heads of d_h / (2 VEC) pairs.
@@ -697,19 +694,6 @@ __device__ inline double centred(const float* gram, const float* cs, int n, int 
 __device__ inline double wave_sum(double v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
-}
-
-// Sum over the workgroup (kSolveThreads), the same value returned to every thread.  `red` holds
-// one double per wave; the trailing barrier lets the caller reuse it at once.
-__device__ inline double block_sum(double v, double* red) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  v = wave_sum(v);
-  if (lane == 0) red[wave] = v;
-  __syncthreads();
-  double s = 0.0;
-  for (int q = 0; q < kSolveThreads / 64; ++q) s += red[q];
-  __syncthreads();
-  return s;
 }
 
 __device__ inline void store_out(void* dst, int64_t i, double v, bool bf16) {

@@ -205,9 +205,13 @@ SMALL_ALIGN_RING = Workload("small_align_ring_bf16", 2, 256, 2, 64, (300,), (64,
 SMALL_MANY_REQUESTS_ALIGN = SMALL_MANY_REQUESTS.replace(name="small_many_requests_align_bf16",
                                                         ranks=(64, 64), aligner_hidden=256)
 
+# Ranks between 128 and 256 that are not 256: the encode's two workgroups per row tile then split
+# the codes unevenly (128 + 32, 128 + 96, 128 + 64), for keys (de-rotated), values and H.
+SMALL_SPLIT_RANKS = Workload("small_split_ranks_bf16", 3, 384, 2, 128, (300, 77, 250),
+                             (160, 224, 192), (1,), 5e5, "bf16", ranks_v=(192, 96, 224))
 TEST_WORKLOADS = (SMALL_BF16, SMALL_HEAD_SHARED, SMALL_F32, SMALL_NARROW, SMALL_DEGENERATE,
                   SMALL_FULL_RANK, SMALL_MANY_REQUESTS, SMALL_ALIGN, SMALL_MANY_LAYERS, SMALL_RING5,
-                  SMALL_RING7, SMALL_ALIGN_RING)
+                  SMALL_RING7, SMALL_ALIGN_RING, SMALL_SPLIT_RANKS)
 
 
 # --------------------------------------------------------------------------------------------
