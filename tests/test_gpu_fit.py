@@ -318,3 +318,47 @@ def test_fit_without_centring_and_without_ridge(wl):
         bound = max(bound, np.linalg.cond(A.T @ A) * np.sqrt(A.shape[0]) * 2.0 ** -24)
     print(f"[fit no centring, lambda 0] tolerance {bound:.3g}", flush=True)
     U.assert_within(errs, bound, f"fit no centring, lambda 0, {wl.name}")
+
+
+def _rows_with_spectrum(n_rows, sing, seed):
+    """Rows X [n_rows, n] whose Gram X^T X is Q diag(sing^2) Q^T exactly (fp64), Q random orthogonal."""
+    g = np.random.default_rng(seed)
+    n = len(sing)
+    q, _ = np.linalg.qr(g.standard_normal((n, n)))
+    u, _ = np.linalg.qr(g.standard_normal((n_rows, n)))
+    return (u * np.asarray(sing)[None, :]) @ q.T
+
+
+@pytest.mark.parametrize("case", ["repeated_top_eigenvalues", "rank_below_r"])
+def test_fit_solve_degenerate_spectra(case):
+    # Eigenvalues that repeat inside the top r (three clusters of 8, 8 and 16), or a Gram whose rank
+    # (16) is below r = 32, so the solve's eigenvalue clusters are exercised.  Individual
+    # eigenvectors are then not unique; W_dec W_enc is (a rotation inside a degenerate subspace
+    # cancels in it, and null directions give zero latents), so that is compared with the oracle's
+    # fit on the rows themselves.
+    dev = torch.device("cuda")
+    w, r, n_rows, lam = 64, 32, 400, 0.1
+    if case == "repeated_top_eigenvalues":
+        sing = np.sqrt(np.concatenate([[10.0] * 8, [7.0] * 8, [5.0] * 16,
+                                       np.linspace(0.5, 0.05, 2 * w - r)]))
+    else:
+        sing = np.concatenate([[3.0] * 4, np.linspace(2.0, 1.0, 12), np.zeros(2 * w - 16)])
+    X = _rows_with_spectrum(n_rows, sing, 7 if case == "rank_below_r" else 5)
+    model = scd.Model(n_layers=1, d_model=64, n_kv_heads=1, head_dim=64, rope_theta=1e4,
+                      dtype="f32", is_patch=[0], rank_k=[r], rank_v=[r], rank_h=[32],
+                      basis_width=w)
+    gram = [torch.tensor(X.T @ X, dtype=torch.float32, device=dev)]
+    colsum = [torch.tensor(X.sum(0), dtype=torch.float32, device=dev)]
+    w_enc = [torch.empty((r, w), device=dev)]
+    w_dec = [torch.empty((w, r), device=dev)]
+    ws = torch.empty(scd.scd_fit_workspace_bytes(model, n_rows), dtype=torch.uint8, device=dev)
+    print(f"[fit degenerate] {case}", flush=True)
+    scd.scd_fit_solve(model, scd.FIT_VALUES, n_rows, lam, False, gram, colsum, w_enc, w_dec,
+                      [None], [None], ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(w_enc[0]).all() and torch.isfinite(w_dec[0]).all()
+    e_o, d_o, _, _ = O.fit_reuse(X[:, :w], X[:, w:], np.zeros(n_rows, dtype=np.int64), 1, 64, 1e4,
+                                 w, False, r, lam, center=False)
+    err = U.max_abs_rel(U.f64(w_dec[0]) @ U.f64(w_enc[0]), d_o @ e_o)
+    print(f"[fit degenerate] {case}: W_dec W_enc max-abs-rel {err:.2e}", flush=True)
+    assert err <= U.TOL["f32"]
