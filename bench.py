@@ -233,7 +233,7 @@ def time_aligner(wl, dev, steps, warmup, stream):
             "frac": round(ach / peak, 4), "alg_flops": flops, "alg_bytes": nbytes}
 
 
-def time_fit(dev, steps, warmup, stream):
+def time_fit(dev, steps, warmup, stream, fit_workload="fit_llama3_8b_head_shared_bf16"):
     """The offline Reuse fit at the Llama-3-8B shape with the head-shared basis (w = d_h = 128:
     8192 tokens x 8 heads = 65,536 calibration rows per layer, 28 Reuse layers): ``scd_fit_gram``
     and ``scd_fit_solve`` for keys and values, HIP events on the stream they run on.  The Gram is
@@ -246,7 +246,7 @@ def time_fit(dev, steps, warmup, stream):
     import paper_2606_07684_amd as scd
     from synth import workloads as W
 
-    wl = W.FIT_LLAMA3_8B
+    wl = {w.name: w for w in (W.FIT_LLAMA3_8B, *W.FIT_WORKLOADS, W.FIT_W1024_BF16)}[fit_workload]
     L, T, D, w, g = wl.n_layers, wl.n_tokens, wl.kv_width, wl.w, wl.g
     R = [l for l in range(L) if not wl.is_patch[l]]
     model = scd.Model(n_layers=L, d_model=wl.d_model, n_kv_heads=wl.n_kv_heads,
@@ -583,6 +583,8 @@ def main():
     ap.add_argument("--no-receive", action="store_true",
                     help="skip the receipt timing (its decode launches share the step's kernel "
                          "and grid, so kernel traces of the step leave it out)")
+    ap.add_argument("--fit-workload", default="fit_llama3_8b_head_shared_bf16",
+                    help="calibration shape of the offline fit timing (e.g. fit_w1024_bf16)")
     ap.add_argument("--no-fit", action="store_true",
                     help="skip the offline fit timing (it runs after the step's timing)")
     ap.add_argument("--no-aligner", action="store_true",
@@ -676,7 +678,7 @@ def main():
     # The offline Reuse fit (Section 4.3.1), at the head-shared calibration shape, beside the step.
     if not args.no_fit:
         print("[bench] timing the offline fit", file=sys.stderr, flush=True)
-        out["fit"] = time_fit(dev, args.steps, args.warmup, stream)
+        out["fit"] = time_fit(dev, args.steps, args.warmup, stream, args.fit_workload)
         torch.cuda.empty_cache()
 
     # Every model-shaped workload in the same run (the same step and readings; a CPU baseline with

@@ -32,7 +32,10 @@ PHASES = {"encode_bf16_kernel": "encode", "reuse_decode": "reuse_decode",
           "patch_kv": "patch", "patch_align_act": "patch", "patch_align": "aligner",
           "patch_fold": "fold", "EncodeKV": "encode", "EncodeH": "encode",
           "ReuseDecode": "reuse_decode", "PatchKV": "patch", "PatchAlign": "patch",
-          "fit_gram": "fit_gram", "fit_solve": "fit_solve"}
+          "fit_gram": "fit_gram", "fit_prep": "fit_solve", "fit_tridiag": "fit_solve",
+          "fit_bisect": "fit_solve", "fit_inverse": "fit_solve", "fit_back": "fit_solve",
+          "fit_project": "fit_solve", "fit_normal": "fit_solve", "fit_chol": "fit_solve",
+          "fit_out": "fit_solve"}
 
 
 def phase_of(name: str):
@@ -83,6 +86,36 @@ def kernel_table(trace_dir: str, warmup_launches: int, aligner_calls: int = 0):
         out.append({"kernel": short(name), "phase": phase_of(name), "grid": grid, "launches": len(d),
                     "mean_us": statistics.mean(d), "min_us": min(d), "max_us": max(d)})
     return out
+
+
+def fit_solve_table(trace_dir: str):
+    """The fp64 solve's kernels per call: launches and total microseconds per call (a call starts at
+    its one `fit_prep_kernel` launch; the first call, a warm-up, is dropped)."""
+    rows = sorted(csv.DictReader(open(one_csv(trace_dir, "kernel_trace.csv"))),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    calls, cur = [], None
+    for r in rows:
+        name = r["Kernel_Name"]
+        if phase_of(name) != "fit_solve":
+            continue
+        if "fit_prep_kernel" in name:
+            cur = {"start": int(r["Start_Timestamp"]), "k": collections.OrderedDict()}
+            calls.append(cur)
+        if cur is None:
+            continue
+        k = short(name).replace("(scd::(anonymous namespace)::SolveArgs)", "")
+        k = k.replace("(scd::FitSolveParams)", "")
+        n, t = cur["k"].get(k, (0, 0.0))
+        cur["k"][k] = (n + 1, t + (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        cur["end"] = int(r["End_Timestamp"])
+    calls = [c for c in calls if "end" in c][1:] or calls
+    names = list(calls[0]["k"].keys()) if calls else []
+    out = []
+    for k in names:
+        out.append({"kernel": k, "launches": statistics.median(c["k"].get(k, (0, 0))[0] for c in calls),
+                    "us": statistics.median(c["k"].get(k, (0, 0.0))[1] for c in calls)})
+    wall = statistics.median((c["end"] - c["start"]) / 1e3 for c in calls) if calls else 0.0
+    return out, wall, len(calls)
 
 
 def counters(folder: str, counter: str):
@@ -160,6 +193,9 @@ def main():
     ap.add_argument("--mfma", help="rocprofv3 --pmc folder with SQ_VALU_MFMA_BUSY_CYCLES, "
                     "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
     ap.add_argument("--mfma-cmd", default="")
+    ap.add_argument("--fit-md", help="also write profiles/fit_solve_<name>.md from --trace (the "
+                    "traced run timed the fit at --fit-shape)")
+    ap.add_argument("--fit-shape", default="fit_llama3_8b_head_shared_bf16")
     args = ap.parse_args()
 
     from synth import workloads as W
@@ -225,6 +261,21 @@ def main():
                 lines.append(f"| {ph} | {us:.1f} | {ev} | {f / 1e9:.1f} GFLOP | {ach:.0f} TFLOP/s | "
                              f"{ach / peak:.3f} of {peak:.0f} TFLOP/s |")
         path = os.path.join(ROOT, "profiles", f"kernels_{wl.name}.md")
+        open(path, "w").write("\n".join(lines) + "\n")
+        print("wrote", path)
+
+    if args.trace and args.fit_md:
+        tab, wall, n_calls = fit_solve_table(args.trace)
+        lines = [f"# fp64 fit solve kernels, {args.fit_shape}", "",
+                 f"Command: `{args.trace_cmd}`", "",
+                 f"Source digest of csrc/: `{digest}`. Per call (one branch, every Reuse layer), "
+                 f"medians over {n_calls} calls after a warm-up call; kernel times from the trace.",
+                 "", "| kernel | launches per call | us per call |", "|---|---|---|"]
+        for t in tab:
+            lines.append(f"| `{t['kernel']}` | {t['launches']:.0f} | {t['us']:.1f} |")
+        lines += ["", f"Sum of kernel time per call: {sum(t['us'] for t in tab):.1f} us; first "
+                  f"launch start to last launch end: {wall:.1f} us."]
+        path = os.path.join(ROOT, "profiles", f"fit_solve_{args.fit_md}.md")
         open(path, "w").write("\n".join(lines) + "\n")
         print("wrote", path)
 
