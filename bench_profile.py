@@ -66,7 +66,8 @@ def kernel_table(trace_dir: str, warmup_launches: int, aligner_calls: int = 0):
         if phase_of(r["Kernel_Name"]) is None:
             continue
         grid = r.get("Grid_Size") or r.get("Grid_Size_X") or 0
-        key = (r["Kernel_Name"], int(grid))
+        # the solve's per-column launches shrink their grids step by step: one row per kernel
+        key = (r["Kernel_Name"], 0 if phase_of(r["Kernel_Name"]) == "fit_solve" else int(grid))
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
         groups.setdefault(key, []).append(dur)
     out = []
