@@ -184,6 +184,10 @@ FIT_WORKLOADS = (FIT_SMALL_BF16, FIT_HEAD_SHARED, FIT_F32, FIT_DH32, FIT_POS0_KE
 # 2048 x 2048 Gram over 2,600 calibration rows of one Reuse layer.
 FIT_W1024_BF16 = Workload("fit_w1024_bf16", 1, 256, 8, 128, (1400, 1200), (64,), (), 5e5, "bf16",
                           pos0=(0, 9), ranks_v=(64,))
+# The model-shaped configurations' own bases: the fit at w = D = 1024 on calibration caches of the
+# Llama-3-8B shape (8192 tokens of one request, rank 128), two Reuse layers.
+FIT_CODEC_LLAMA3_8B = Workload("fit_codec_llama3_8b_bf16", 2, 4096, 8, 128, (8192,), (128, 128), (),
+                               5e5, "bf16")
 # Calibration at the Llama-3-8B shape with the head-shared basis: 8192 tokens x 8 heads = 65,536
 # rows of 128 channels per layer (the paper calibrates on 100-500 prefixes of ~600 tokens).
 FIT_LLAMA3_8B = LLAMA3_8B_HEAD_SHARED.replace(name="fit_llama3_8b_head_shared_bf16")

@@ -362,3 +362,68 @@ def test_fit_solve_degenerate_spectra(case):
     err = U.max_abs_rel(U.f64(w_dec[0]) @ U.f64(w_enc[0]), d_o @ e_o)
     print(f"[fit degenerate] {case}: W_dec W_enc max-abs-rel {err:.2e}", flush=True)
     assert err <= U.TOL["f32"]
+
+
+def test_fitted_bases_at_the_config1_shape_through_the_codec():
+    # The configs' own bases (w = D = 1024, rank 128, 8192 tokens): fit keys (caches rotated by
+    # position test-side, so the de-rotated content is low rank and the fit unique) and values
+    # on calibration rows, compare the fits with the oracle's, then carry held-out producer rows
+    # through the codec's encode and Reuse decode with the fitted translators (W_dec != W_enc^T)
+    # against the oracle's encode and decode with its own fit.
+    wl = W.FIT_CODEC_LLAMA3_8B
+    dev = torch.device("cuda")
+    model, batch = U.model_of(wl), U.batch_of(wl, dev)
+    L, lam, pos = wl.n_layers, _lam(wl), U.host_positions(wl)
+    H, dh, th, D = wl.n_kv_heads, wl.head_dim, wl.rope_theta, wl.kv_width
+    rot = lambda x: _rotate_complex(U.f64(x), pos, H, dh, th)  # noqa: E731
+    dev_t = lambda x: torch.from_numpy(x).to(device=dev, dtype=wl.torch_dtype).contiguous()  # noqa
+    cal, held = {}, {}
+    for br in ("k", "v"):
+        for store, sample in ((cal, "cal"), (held, "heldout")):
+            a, b = [None] * L, [None] * L
+            for l in range(L):
+                a_c, b_c = W.fit_pair(wl, l, br, "cpu", sample)
+                a[l] = dev_t(rot(a_c)) if br == "k" else a_c.to(dev)
+                b[l] = dev_t(rot(b_c)) if br == "k" else b_c.to(dev)
+            store[br] = (a, b)
+    rope = scd.scd_rope_table(model, wl.max_position)
+    fits, errs = {}, {}
+    for br, code in (("k", scd.FIT_KEYS), ("v", scd.FIT_VALUES)):
+        print(f"[fit codec w=1024] fitting {br}", flush=True)
+        fits[br] = scd.fit_reuse(model, batch, rope if br == "k" else None, code, *cal[br], lam,
+                                 center=True)
+    torch.cuda.synchronize()
+    fits_o = {}
+    for br in ("k", "v"):
+        for l in range(L):
+            e_o, d_o, ma_o, mb_o = _oracle_fit(wl, br, *cal[br], l, lam)
+            fits_o[(br, l)] = (e_o, d_o, ma_o, mb_o)
+            # At rank 128 the latent's scales are 0.8% apart and 8192 rows move the sample
+            # eigenvalues by about 1%, so some neighbours land within the fp32 Gram's rounding of
+            # each other and their eigenvectors are not unique; W_dec W_enc is (c19).
+            w_enc, w_dec = fits[br][0][l], fits[br][1][l]
+            errs[(br, "w_dec w_enc", l)] = U.max_abs_rel(U.f64(w_dec) @ U.f64(w_enc), d_o @ e_o)
+            errs[(br, "mu_enc", l)] = U.max_abs_rel(U.f64(fits[br][2][l]), ma_o)
+            errs[(br, "mu_dec", l)] = U.max_abs_rel(U.f64(fits[br][3][l]), mb_o)
+    z_k, z_v, z_h = W.alloc_codes(wl, dev)
+    kc, vc = W.alloc_caches(wl, dev)
+    none = [None] * L
+    print("[fit codec w=1024] encode and decode with the fitted bases", flush=True)
+    scd.scd_encode(model, batch, rope, held["k"][0], held["v"][0], none, fits["k"][0],
+                   fits["v"][0], none, fits["k"][2], fits["v"][2], z_k, z_v, z_h)
+    scd.scd_reuse_decode(model, batch, rope, z_k, z_v, fits["k"][1], fits["v"][1], fits["k"][3],
+                         fits["v"][3], kc, vc)
+    torch.cuda.synchronize()
+    for l in range(L):
+        ek, dk, mak, mbk = fits_o[("k", l)]
+        ev, dv, mav, mbv = fits_o[("v", l)]
+        want_k = O.decode_k(O.encode_k(U.f64(held["k"][0][l]), pos, ek, mak, H, dh, th), dk, mbk,
+                            pos, H, dh, th)
+        want_v = O.decode_v(O.encode_v(U.f64(held["v"][0][l]), ev, mav), dv, mbv, D)
+        errs[("k_cache", l)] = U.max_abs_rel(U.f64(kc[l]), want_k)
+        errs[("v_cache", l)] = U.max_abs_rel(U.f64(vc[l]), want_v)
+        # the fitted translator carries held-out producer rows onto the consumer's, within the noise
+        assert U.max_abs_rel(want_v, U.f64(held["v"][1][l])) < 0.2
+        assert U.max_abs_rel(want_k, U.f64(held["k"][1][l])) < 0.2
+        assert not torch.allclose(fits["v"][1][l].float(), fits["v"][0][l].float().T)
+    U.assert_within(errs, U.TOL[wl.dtype], "fitted bases at the config-1 shape")
