@@ -96,7 +96,11 @@ typedef struct {
  * Opaque device table of rotation cosines and sines for positions [0, max_position), evaluated in
  * fp64 and rounded once to fp32 (fp32-evaluated angles lose ~1e-5 absolute accuracy by position
  * 512 and ~2e-3 by 32K).  It depends only on (head_dim, rope_theta, max_position): build it once
- * per model and reuse it.  scd_rope_table_bytes returns its size; scd_rope_table fills it. */
+ * per model and reuse it.  scd_rope_table_bytes returns its size; scd_rope_table fills it.  The
+ * entry points that take a table trust the (table, max_position) pair they are given: it must be a
+ * table this model's head_dim and rope_theta built for that max_position, holding
+ * scd_rope_table_bytes(model, max_position) bytes (the C calls cannot see its size; the Python
+ * binding records head_dim, theta and max_position with the table and checks them). */
 size_t scd_rope_table_bytes(const scd_model_t* model, int64_t max_position);
 scd_status_t scd_rope_table(const scd_model_t* model, int64_t max_position, void* table,
                             size_t table_bytes, hipStream_t stream);
