@@ -956,7 +956,108 @@ __device__ inline double guard_pivot(double c, double tol) {
   return !(fabs(c) <= tol) ? c : (c >= 0.0 ? tol : -tol);
 }
 
-// Vector m of the layer: Y[i][m] (Z[0, n r)), with the LU factors of T - sigma I in U0 (Z[n r,
+// Strided view of one vector: entry i at p[i * stride].
+struct Strided {
+  double* p;
+  int64_t stride;
+  __device__ double& operator[](int i) const { return p[i * stride]; }
+};
+
+// The four vectors one eigenvector's inverse iteration works on: the vector and its LU factors.
+struct InverseWork {
+  Strided y, u0, u1, u2;
+};
+
+// Inverse iteration for the cluster of eigenvalues lam[j .. last] (one thread).  Member m works in
+// work(m); every finished vector m is stored at out(m) (Y[i][m] of the layer), which is also where
+// the orthogonalisation reads the earlier members.
+template <typename WorkFn, typename OutFn>
+__device__ inline void inverse_cluster(const double* d, const double* e, int n, const double* lam,
+                                       int j, int last, double tnorm, WorkFn work, OutFn out) {
+  const double pert = 10.0 * kEps * tnorm, ptol = kEps * tnorm;
+  double sigma = 0.0;
+  for (int m = j; m <= last; ++m) {
+    const InverseWork wk = work(m);
+    const Strided y = wk.y, u0 = wk.u0, u1 = wk.u1, u2 = wk.u2;
+    // shifts inside a cluster step down by at least pert, so the solves stay independent
+    sigma = m == j ? lam[m] : fmin(lam[m], sigma - pert);
+    for (int i = 0; i < n; ++i) y[i] = start_entry(i, m);
+    double sc = 2.0;  // the start vector's entries lie in [-1/2, 1/2)
+    for (int it = 0; it < kInverseSolves; ++it) {
+      // forward elimination of (T - sigma I) y = b / max|b| with partial pivoting; rows hold
+      // (c0, c1) on the diagonal and the superdiagonal, the right-hand side rides along
+      double c0 = d[0] - sigma, c1 = n > 1 ? e[0] : 0.0;
+      double yc = y[0] * sc;
+      for (int i = 0; i < n - 1; ++i) {
+        const double sub = e[i], a1 = d[i + 1] - sigma, b1 = i + 1 < n - 1 ? e[i + 1] : 0.0;
+        const double nb = y[i + 1] * sc;
+        if (fabs(c0) >= fabs(sub)) {
+          const double piv = guard_pivot(c0, ptol);
+          const double mult = sub / piv;
+          u0[i] = piv;
+          u1[i] = c1;
+          u2[i] = 0.0;
+          y[i] = yc;
+          yc = nb - mult * yc;
+          c0 = a1 - mult * c1;
+          c1 = b1;
+        } else {
+          const double mult = c0 / sub;
+          u0[i] = sub;
+          u1[i] = a1;
+          u2[i] = b1;
+          y[i] = nb;
+          yc = yc - mult * nb;
+          c0 = c1 - mult * a1;
+          c1 = -mult * b1;
+        }
+      }
+      u0[n - 1] = guard_pivot(c0, ptol);
+      y[n - 1] = yc;
+      // back substitution, in place
+      double x1 = 0.0, x2 = 0.0;
+      for (int i = n - 1; i >= 0; --i) {
+        double v = y[i];
+        if (i + 1 < n) v -= u1[i] * x1;
+        if (i + 2 < n) v -= u2[i] * x2;
+        v /= u0[i];
+        y[i] = v;
+        x2 = x1;
+        x1 = v;
+      }
+      // orthogonalise against the cluster's earlier vectors, then normalise
+      for (int q = j; q < m; ++q) {
+        const Strided yq = out(q);
+        double dot = 0.0;
+        for (int i = 0; i < n; ++i) dot += yq[i] * y[i];
+        for (int i = 0; i < n; ++i) y[i] -= dot * yq[i];
+      }
+      double ss = 0.0, mx = 0.0;
+      for (int i = 0; i < n; ++i) {
+        ss += y[i] * y[i];
+        mx = fmax(mx, fabs(y[i]));
+      }
+      const double inv = 1.0 / sqrt(ss);
+      for (int i = 0; i < n; ++i) y[i] *= inv;
+      sc = mx > 0.0 ? 1.0 / (mx * inv) : 1.0;  // 1 / max|y| of the normalised vector
+    }
+    const Strided o = out(m);
+    if (o.p != y.p)
+      for (int i = 0; i < n; ++i) o[i] = y[i];
+  }
+}
+
+// One thread per eigenvalue; only the first thread of a cluster works (it takes the whole
+// cluster in order).  Returns false for threads with nothing to do.
+__device__ inline bool cluster_of(const double* lam, int r, int j, double ctol, int* last) {
+  if (j >= r || (j > 0 && !(lam[j - 1] - lam[j] > ctol))) return false;
+  int l = j;
+  while (l + 1 < r && !(lam[l] - lam[l + 1] > ctol)) ++l;
+  *last = l;
+  return true;
+}
+
+// Vectors in the workspace: Y[i][m] (Z[0, n r)), the LU factors of T - sigma I in U0 (Z[n r,
 // 2 n r)), U1 and U2 (M[0, n r) and M[n r, 2 n r)), all indexed [i][m].
 __global__ __launch_bounds__(64) void fit_inverse_kernel(const SolveArgs a) {
   __shared__ double d[kMaxN], e[kMaxN];
@@ -969,91 +1070,45 @@ __global__ __launch_bounds__(64) void fit_inverse_kernel(const SolveArgs a) {
   }
   __syncthreads();
   const int j = blockIdx.x * 64 + threadIdx.x;
-  if (j >= r) return;
   const double tnorm = s.job->tnorm;
-  const double ctol = kClusterTol * tnorm, pert = 10.0 * kEps * tnorm, ptol = kEps * tnorm;
-  const double* lam = s.lam;
-  // only the first thread of a cluster works; it takes the whole cluster in order
-  if (j > 0 && !(lam[j - 1] - lam[j] > ctol)) return;
-  int last = j;
-  while (last + 1 < r && !(lam[last] - lam[last + 1] > ctol)) ++last;
+  int last;
+  if (!cluster_of(s.lam, r, j, kClusterTol * tnorm, &last)) return;
   const int64_t nr = static_cast<int64_t>(n) * r;
-  double* yv = s.z;
-  double* u0 = s.z + nr;
-  double* u1 = s.m;
-  double* u2 = s.m + nr;
-  double sigma = 0.0;
-  for (int m = j; m <= last; ++m) {
-    // shifts inside a cluster step down by at least pert, so the solves stay independent
-    sigma = m == j ? lam[m] : fmin(lam[m], sigma - pert);
-    for (int i = 0; i < n; ++i) yv[static_cast<int64_t>(i) * r + m] = start_entry(i, m);
-    double sc = 2.0;  // the start vector's entries lie in [-1/2, 1/2)
-    for (int it = 0; it < kInverseSolves; ++it) {
-      // forward elimination of (T - sigma I) y = b / max|b| with partial pivoting; rows hold
-      // (c0, c1) on the diagonal and the superdiagonal, the right-hand side rides along
-      double c0 = d[0] - sigma, c1 = n > 1 ? e[0] : 0.0;
-      double y = yv[m] * sc;
-      for (int i = 0; i < n - 1; ++i) {
-        const int64_t at = static_cast<int64_t>(i) * r + m;
-        const double sub = e[i], a1 = d[i + 1] - sigma, b1 = i + 1 < n - 1 ? e[i + 1] : 0.0;
-        const double nb = yv[at + r] * sc;
-        if (fabs(c0) >= fabs(sub)) {
-          const double piv = guard_pivot(c0, ptol);
-          const double mult = sub / piv;
-          u0[at] = piv;
-          u1[at] = c1;
-          u2[at] = 0.0;
-          yv[at] = y;
-          y = nb - mult * y;
-          c0 = a1 - mult * c1;
-          c1 = b1;
-        } else {
-          const double mult = c0 / sub;
-          u0[at] = sub;
-          u1[at] = a1;
-          u2[at] = b1;
-          yv[at] = nb;
-          y = y - mult * nb;
-          c0 = c1 - mult * a1;
-          c1 = -mult * b1;
-        }
-      }
-      {
-        const int64_t at = static_cast<int64_t>(n - 1) * r + m;
-        u0[at] = guard_pivot(c0, ptol);
-        yv[at] = y;
-      }
-      // back substitution, in place
-      double x1 = 0.0, x2 = 0.0;
-      for (int i = n - 1; i >= 0; --i) {
-        const int64_t at = static_cast<int64_t>(i) * r + m;
-        double v = yv[at];
-        if (i + 1 < n) v -= u1[at] * x1;
-        if (i + 2 < n) v -= u2[at] * x2;
-        v /= u0[at];
-        yv[at] = v;
-        x2 = x1;
-        x1 = v;
-      }
-      // orthogonalise against the cluster's earlier vectors, then normalise
-      for (int q = j; q < m; ++q) {
-        double dot = 0.0;
-        for (int i = 0; i < n; ++i)
-          dot += yv[static_cast<int64_t>(i) * r + q] * yv[static_cast<int64_t>(i) * r + m];
-        for (int i = 0; i < n; ++i)
-          yv[static_cast<int64_t>(i) * r + m] -= dot * yv[static_cast<int64_t>(i) * r + q];
-      }
-      double ss = 0.0, mx = 0.0;
-      for (int i = 0; i < n; ++i) {
-        const double v = yv[static_cast<int64_t>(i) * r + m];
-        ss += v * v;
-        mx = fmax(mx, fabs(v));
-      }
-      const double inv = 1.0 / sqrt(ss);
-      for (int i = 0; i < n; ++i) yv[static_cast<int64_t>(i) * r + m] *= inv;
-      sc = mx > 0.0 ? 1.0 / (mx * inv) : 1.0;  // 1 / max|y| of the normalised vector
-    }
+  // vector m works in place at its own column of Y, its factors in their columns of U0..U2
+  auto col = [&](double* base, int m) { return Strided{base + m, r}; };
+  inverse_cluster(
+      d, e, n, s.lam, j, last, tnorm,
+      [&](int m) { return InverseWork{col(s.z, m), col(s.z + nr, m), col(s.m, m), col(s.m + nr, m)}; },
+      [&](int m) { return col(s.z, m); });
+}
+
+// The same for n <= kInverseLdsN: each working thread keeps its vector and LU factors in LDS
+// ([i][thread], kInverseLdsThreads interleaved, so the threads' accesses fall in distinct banks)
+// and copies each finished vector to Y.
+constexpr int kInverseLdsN = 256, kInverseLdsThreads = 16;
+__global__ __launch_bounds__(64) void fit_inverse_lds_kernel(const SolveArgs a) {
+  __shared__ double d[kInverseLdsN], e[kInverseLdsN];
+  __shared__ double vec[4 * kInverseLdsN * kInverseLdsThreads];
+  const int layer = blockIdx.y, n = 2 * a.w;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  for (int i = threadIdx.x; i < n; i += 64) {
+    d[i] = s.d[i];
+    e[i] = i < n - 1 ? s.e[i] : 0.0;
   }
+  __syncthreads();
+  const int t = threadIdx.x;
+  const int j = blockIdx.x * kInverseLdsThreads + t;
+  if (t >= kInverseLdsThreads) return;
+  const double tnorm = s.job->tnorm;
+  int last;
+  if (!cluster_of(s.lam, r, j, kClusterTol * tnorm, &last)) return;
+  constexpr int64_t kPlane = static_cast<int64_t>(kInverseLdsN) * kInverseLdsThreads;
+  auto lds = [&](int q) { return Strided{vec + q * kPlane + t, kInverseLdsThreads}; };
+  inverse_cluster(
+      d, e, n, s.lam, j, last, tnorm,
+      [&](int) { return InverseWork{lds(0), lds(1), lds(2), lds(3)}; },
+      [&](int m) { return Strided{s.z + m, r}; });
 }
 
 // ---- back-transformation and sign ---------------------------------------------------------------
@@ -1402,7 +1457,12 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const unsigned rt = static_cast<unsigned>((rmax + 63) / 64);
   hipLaunchKernelGGL(fit_bisect_kernel, dim3((rmax + 3) / 4, layers), wave, 0, stream, a);
-  hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
+  if (n <= kInverseLdsN)
+    hipLaunchKernelGGL(fit_inverse_lds_kernel,
+                       dim3((rmax + kInverseLdsThreads - 1) / kInverseLdsThreads, layers), wave, 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
   hipLaunchKernelGGL(fit_back_kernel, dim3((rmax + kBackCols - 1) / kBackCols, layers), block, 0,
                      stream, a);
   hipLaunchKernelGGL(fit_project_kernel, dim3(n / 64, rt, layers), block, 0, stream, a);
