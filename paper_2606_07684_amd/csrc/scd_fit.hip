@@ -1305,6 +1305,46 @@ __global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs
   if (blockIdx.x == 0 && tid == 0) ldiag[k] = lkk;
 }
 
+// The same factorisation for sizes up to kCholLdsN, one workgroup per matrix with the matrix in
+// LDS: one launch instead of one per column, and bit-identical to it (the same operations on every
+// entry in the same order).  grid.x = 0: A^T A + lam I, 1: Z^T Z + lam I.
+constexpr int kCholLdsN = 128, kCholThreads = 1024;
+__global__ __launch_bounds__(kCholThreads) void fit_chol_lds_kernel(const SolveArgs a) {
+  constexpr int LD = kCholLdsN + 1;
+  __shared__ double m[kCholLdsN * LD];
+  __shared__ double lc[kCholLdsN];
+  const int layer = blockIdx.y, w = a.w, tid = threadIdx.x;
+  const Slots s = slots(a.work, a.w, layer);
+  const int r = static_cast<int>(s.job->rank);
+  const bool zz = blockIdx.x == 1;
+  const int sz = zz ? r : w;
+  double* mat = zz ? s.y : s.x;
+  double* ldiag = s.ldiag + (zz ? w : 0);
+  for (int e = tid; e < sz * sz; e += kCholThreads) {
+    const int i = e / sz, j = e % sz;
+    if (j <= i) m[i * LD + j] = mat[static_cast<int64_t>(i) * sz + j];
+  }
+  __syncthreads();
+  for (int k = 0; k < sz; ++k) {
+    const double piv = m[k * LD + k];
+    const double lkk = piv > 0.0 ? sqrt(piv) : kNaN;
+    for (int i = k + 1 + tid; i < sz; i += kCholThreads) lc[i] = m[i * LD + k] / lkk;
+    if (tid == 0) ldiag[k] = lkk;
+    __syncthreads();
+    // rows by wave, the row's columns by lane
+    for (int i = k + 1 + (tid >> 6); i < sz; i += kCholThreads / 64) {
+      const double li = lc[i];
+      for (int j = k + 1 + (tid & 63); j <= i; j += 64) m[i * LD + j] -= li * lc[j];
+    }
+    // column k of L, as the per-column launches store it: the upper triangle and the row-major copy
+    for (int i = k + 1 + tid; i < sz; i += kCholThreads) {
+      mat[static_cast<int64_t>(k) * sz + i] = lc[i];
+      mat[static_cast<int64_t>(sz) * sz + static_cast<int64_t>(i) * sz + k] = lc[i];
+    }
+    __syncthreads();
+  }
+}
+
 // ---- triangular solves and outputs --------------------------------------------------------------
 __device__ inline double readlane_f64(double v, int lane) {
   const int64_t b = __double_as_longlong(v);
@@ -1470,11 +1510,15 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   hipLaunchKernelGGL(fit_normal_kernel, dim3(rt * rt > tw * tw ? rt * rt : tw * tw, 2, layers),
                      block, 0, stream, a);
   const int sz = p.w > rmax ? p.w : rmax;
-  for (int k = 0; k < sz; ++k) {
-    a.step = k;
-    const int rows = sz - k - 1;
-    const int gx = rows > 0 ? (rows + kSolveRows - 1) / kSolveRows : 1;
-    hipLaunchKernelGGL(fit_chol_kernel, dim3(gx, 2, layers), block, 0, stream, a);
+  if (sz <= kCholLdsN) {
+    hipLaunchKernelGGL(fit_chol_lds_kernel, dim3(2, layers), dim3(kCholThreads), 0, stream, a);
+  } else {
+    for (int k = 0; k < sz; ++k) {
+      a.step = k;
+      const int rows = sz - k - 1;
+      const int gx = rows > 0 ? (rows + kSolveRows - 1) / kSolveRows : 1;
+      hipLaunchKernelGGL(fit_chol_kernel, dim3(gx, 2, layers), block, 0, stream, a);
+    }
   }
   constexpr int kWaves = kSolveThreads / 64;
   hipLaunchKernelGGL(fit_out_kernel, dim3((rmax + p.w + kWaves - 1) / kWaves, layers), block, 0,
