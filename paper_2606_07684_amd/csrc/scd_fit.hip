@@ -861,6 +861,108 @@ __global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveA
   tridiag_step<0>(a);
 }
 
+// The last steps, from step k0 on (trailing block of at most kTailN rows), in one launch: one
+// workgroup per layer holds the block [k0 + 1, n)^2 of A^(k0) in LDS and applies the same steps as
+// the per-column launches (the same expressions, reflectors and p in the same places), the
+// workgroup barriers standing in for the launch boundaries.  k0 = -1 starts from G_c itself.
+constexpr int kTailN = 128, kTailThreads = 1024;
+__global__ __launch_bounds__(kTailThreads) void fit_tridiag_tail_kernel(const SolveArgs a) {
+  constexpr int LD = kTailN + 1, kWaves = kTailThreads / 64;
+  __shared__ double am[kTailN * LD];
+  __shared__ double vk[kTailN], wk[kTailN], vn[kTailN], pk[kTailN];
+  __shared__ double red[2][kWaves];
+  const int layer = blockIdx.x, n = 2 * a.w, k0 = a.step, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const Slots s = slots(a.work, a.w, layer);
+  const int o = k0 + 1;  // global index of local row / column 0
+  const int m0 = n - o;  // rows of the block (<= kTailN)
+  {
+    const double* src = k0 <= 0 ? s.z : ((k0 - 1) & 1 ? s.y : s.x);
+    for (int e = tid; e < m0 * m0; e += kTailThreads) {
+      const int i = e / m0, j = e % m0;
+      am[i * LD + j] = src[static_cast<int64_t>(o + i) * n + o + j];
+    }
+    if (k0 >= 0) {
+      const double* vrow = reflector_rows(s, k0) + static_cast<int64_t>(k0) * n;
+      const double* p_cur = (k0 & 1) ? s.p1 : s.p0;
+      for (int i = tid; i < m0; i += kTailThreads) {
+        vk[i] = vrow[o + i];
+        pk[i] = p_cur[o + i];
+      }
+    } else {
+      for (int i = tid; i < m0; i += kTailThreads) vk[i] = pk[i] = 0.0;
+    }
+  }
+  __syncthreads();
+  auto block_sum = [&](double v, int slot) {
+    v = wave_sum(v);
+    if (lane == 0) red[slot][wave] = v;
+    __syncthreads();
+    double t = 0.0;
+    for (int q = 0; q < kWaves; ++q) t += red[slot][q];
+    return t;
+  };
+  double tau_k = k0 >= 0 ? s.tau[k0] : 0.0;
+  for (int k = k0; k <= n - 3; ++k) {
+    // local indices: global i is local i - o; the step touches global [k + 1, n)
+    const int b = k + 1 - o;  // local index of global k + 1
+    // w_k = p_k - (tau_k / 2)(p_k . v_k) v_k
+    double kk = 0.0;
+    if (k >= 0) {
+      double dot = 0.0;
+      for (int i = b + tid; i < m0; i += kTailThreads) dot += pk[i] * vk[i];
+      kk = 0.5 * tau_k * block_sum(dot, 0);
+    }
+    const double vk1 = vk[b], wk1 = pk[b] - kk * vk1;
+    double sig = 0.0;
+    for (int i = b + tid; i < m0; i += kTailThreads) {
+      const double wi = pk[i] - kk * vk[i];
+      wk[i] = wi;
+      const double c = am[b * LD + i] - vk1 * wi - wk1 * vk[i];
+      vn[i] = c;
+      if (i >= b + 2) sig += c * c;
+    }
+    const double sigma = block_sum(sig, 1);  // its barrier also publishes wk and vn
+    const double d_next = vn[b], alpha = vn[b + 1];
+    double tau = 0.0, beta = alpha, scale = 0.0;
+    if (!(sigma == 0.0)) {
+      const double norm = sqrt(alpha * alpha + sigma);
+      beta = alpha >= 0.0 ? -norm : norm;
+      tau = (beta - alpha) / beta;
+      scale = 1.0 / (alpha - beta);
+    }
+    __syncthreads();  // every thread has read alpha and used pk
+    for (int i = b + 2 + tid; i < m0; i += kTailThreads) vn[i] *= scale;
+    __syncthreads();
+    // rows k + 2 .. n - 1 of A^(k+1) (in place) and of p_{k+1}
+    for (int i = b + 1 + wave; i < m0; i += kWaves) {
+      const double vi = vk[i], wi = wk[i];
+      double acc = 0.0;
+      for (int j = b + 1 + lane; j < m0; j += 64) {
+        const double v = am[i * LD + j] - vi * wk[j] - wi * vk[j];
+        am[i * LD + j] = v;
+        if (k == n - 3 && tid == 0) s.d[n - 1] = v;  // the last step: i = j = n - 1
+        acc += v * (j == b + 1 ? 1.0 : vn[j]);
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) pk[i] = tau * acc;
+    }
+    // reflector k + 1 where the per-column launches keep it, and T's entries
+    double* vrow = ((k + 1) & 1 ? s.x : s.y) + static_cast<int64_t>(k + 1) * n;
+    for (int i = b + 1 + tid; i < m0; i += kTailThreads) vrow[o + i] = i == b + 1 ? 1.0 : vn[i];
+    if (tid == 0) {
+      s.d[k + 1] = d_next;
+      s.e[k + 1] = beta;
+      s.tau[k + 1] = tau;
+    }
+    __syncthreads();  // pk and am are the next step's
+    // the next step's reflector: v_{k+1} (first entry 1)
+    for (int i = b + 1 + tid; i < m0; i += kTailThreads) vk[i] = i == b + 1 ? 1.0 : vn[i];
+    tau_k = tau;
+    __syncthreads();
+  }
+}
+
 // ---- bisection -------------------------------------------------------------------------------
 // Number of eigenvalues of T below x (Sturm count of the LDL^T pivots of T - x I); a pivot smaller
 // in magnitude than pivmin counts as -pivmin.
@@ -1486,13 +1588,17 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   SolveArgs a{p.work, static_cast<double>(p.n_rows), p.lambda, p.w, 0, p.center, p.bf16};
   hipLaunchKernelGGL(fit_prep_kernel, dim3((n + kSolveRows - 1) / kSolveRows, layers), block, 0,
                      stream, p);
-  for (int k = -1; k <= n - 3; ++k) {
+  // steps k0 .. n-3 (a trailing block of n - k0 - 1 <= kTailN rows) in one launch
+  const int k0 = n - 1 - kTailN > -1 ? n - 1 - kTailN : -1;
+  for (int k = -1; k < k0; ++k) {
     a.step = k;
     const int rows = n - k - 2;
     const dim3 grid((rows + kSolveRows - 1) / kSolveRows, layers);
     if (n <= 64 * kTridiagPre) hipLaunchKernelGGL(fit_tridiag_pre_kernel, grid, block, 0, stream, a);
     else hipLaunchKernelGGL(fit_tridiag_kernel, grid, block, 0, stream, a);
   }
+  a.step = k0;
+  hipLaunchKernelGGL(fit_tridiag_tail_kernel, dim3(layers), dim3(kTailThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned rt = static_cast<unsigned>((rmax + 63) / 64);
