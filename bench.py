@@ -308,7 +308,10 @@ def time_fit(dev, steps, warmup, stream, fit_workload="fit_llama3_8b_head_shared
                      "tflops": round(flops / (gram_ms * 1e-3) / 1e12, 2)},
             "solve": {"kernels": "fit_prep/tridiag/bisect/inverse/back/project/normal/chol/out",
                       "ms_per_call": round(solve_ms / 2, 3), "calls": 2,
-                      "layers_per_call": len(R), "launches_per_call": n2 + w + 6}}
+                      "layers_per_call": len(R),
+                      # prep, the per-column Householder steps until 128 rows remain, their
+                      # one-launch tail, five stages, the Cholesky (one launch up to 128), the solves
+                      "launches_per_call": 1 + max(n2 - 128, 0) + 1 + 5 + (1 if w <= 128 else w) + 1}}
 
 
 def time_receive(wl, dev, steps, warmup, stream, model, batch, rope, inp, z_k, z_v, z_h,
