@@ -612,15 +612,18 @@ __global__ __launch_bounds__(256) void fit_gram_reduce_kernel(const FitGramParam
 //             for column k + 1 applies reflector k to the trailing block, forms reflector k + 1
 //             from the updated column and the product p = tau A v that the next launch needs.  Two
 //             matrix copies take turns as source and destination, so no workgroup reads what
-//             another workgroup of the same launch writes;
+//             another workgroup of the same launch writes.  The last steps (a trailing block of at
+//             most 128 rows) run in one launch with the block in LDS;
 //   bisect    the r largest eigenvalues of T by bisection on Sturm counts;
 //   inverse   their eigenvectors of T by inverse iteration (three solves with T - lambda I under
 //             partial pivoting); eigenvalues closer than 1e-7 ||T|| form a cluster, whose vectors
-//             one thread computes in turn, each orthogonalised against the cluster's earlier ones;
+//             one thread computes in turn, each orthogonalised against the cluster's earlier ones
+//             (for 2w <= 256 the working vectors live in LDS);
 //   back      V_r = Q Y, each column's largest-magnitude entry then made positive;
 //   project   P = G_c V_r;
 //   normal    Z^T Z + lam I = V_r^T P + lam I and A^T A + lam I;
-//   chol      right-looking Cholesky of both, one launch per column;
+//   chol      right-looking Cholesky of both, one launch per column (sizes up to 128: one
+//             launch, the matrix in LDS);
 //   out       the triangular solves for E and F and the outputs, rounded once.
 // ---------------------------------------------------------------------------------------------
 constexpr int kSolveThreads = 256;
