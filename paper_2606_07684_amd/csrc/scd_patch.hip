@@ -4,24 +4,27 @@
 // projections (act W_fold^T + c) and runs the aligner's own products.
 //
 // One workgroup computes a 256 (channels n) x 256 (tokens t) tile of C^T = W * H_hat^T with four
-// waves, each owning 128 channels x 128 tokens as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.
-// The weight tile is the MFMA A operand, so an accumulator register holds one token's channels;
-// weight rows are placed in LDS in a permuted order that gives each lane 16 consecutive channels
-// of one token.  A wave's 128 channels are whole heads, so every RoPE pair (i, i + d_h/2) meets in
-// one lane: bias, rotation and bf16 rounding happen in registers and each lane stores two 16-byte
-// vectors per block.
+// waves, each owning 128 channels x 128 tokens as 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  The
+// 16 x 16 x 32 shape does the same work per cycle as the 32 x 32 x 16 one with the same operand
+// traffic, and this part holds a clearly higher clock under it: at equal MFMA-busy fractions, a
+// build on the 32 x 32 shape ran this product at 1.6-1.7 GHz where the 16 x 16 shape ran at 1.9-2.0.
+// The weight tile is the MFMA A operand, so an accumulator holds four channels of one token;
+// weight rows are placed in LDS in a permuted order that gives each lane 8 consecutive channels of
+// one token across a pair of blocks.  A wave's 128 channels are whole heads, so every RoPE pair
+// (i, i + d_h/2) meets in one lane: bias, rotation and bf16 rounding happen in registers and each
+// lane stores 16-byte vectors.
 //
 // K advances 64 at a time.  An operand tile of one 64-wide step (256 rows x 64 bf16 = 32 KiB, its
 // 16-byte chunks XOR-swizzled so MFMA operand reads are conflict-free) fills one slot of a ring of
 // five, the whole 160 KiB of LDS.  Both operand tiles travel global -> LDS directly
 // (buffer_load_dwordx4 ... lds), eight lanes of a copy instruction reading one row's whole 128-byte
-// line.  Each step is four 16-wide k-slices; the workgroup barrier sits before the last one, so
-// the operand reads of the next step's first slice run under MFMAs.  The copies are spread over
-// the whole step, a few between MFMAs: the token tile of step k + 2 over the first three slices
-// (into the slot the previous barrier released) and the weight tile of step k + 2 over the last
-// (into the slot this step's barrier released).  Issued in one burst, the 64 copies of a step
-// (64 KiB per CU) queue behind the texture path for about as long as the burst of MFMAs they sit
-// between, and each stalled copy holds up the MFMAs behind it in the wave's instruction stream.
+// line.  Each step is two 32-wide k-slices; the workgroup barrier sits between them, so the
+// operand reads of the next step's first slice run under MFMAs.  The copies are spread over the
+// step, one every four MFMAs after the slice's operand reads: the token tile of step k + 2 in the
+// first slice (into the slot the previous barrier released) and the weight tile of step k + 2 in
+// the second (into the slot this step's barrier released).  Issued in one burst, the 64 copies of
+// a step (64 KiB per CU) would queue behind the texture path, and each stalled copy holds up the
+// MFMAs behind it in the wave's instruction stream.
 //
 // The epilogue first stages the tile's RoPE factors (256 tokens x d_h/2 pairs, fp32) and bias in
 // the then free LDS, so its stores never queue behind global loads (on this part loads and stores
@@ -44,18 +47,27 @@ constexpr int kWaves = 4;                   // one wave per SIMD
 constexpr int kThreads = 64 * kWaves;
 constexpr int kDmaIters = kBN * kChunks / kThreads;  // copy instructions per wave per operand tile
 constexpr int kWaveTok = 128;               // tokens per wave (each wave owns 128 channels)
-constexpr int kUB = kWaveTok / 32;          // 32-token MFMA blocks per wave
+constexpr int kUB = kWaveTok / 16;          // 16-token MFMA blocks per wave
+constexpr int kSB = 128 / 16;               // 16-channel MFMA blocks per wave
 static_assert(kBN == kBM, "square tiles: both operand tiles fill one slot");
 static_assert(kRing * kSlot * 2 <= 160 * 1024, "LDS");
 static_assert(kBM * 32 * 16 + kBN * 2 <= kRing * kSlot * 2, "epilogue staging fits the ring");
 // Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data format, no swizzle.
 constexpr int kBufferFlags = 0x00020000;
 
-// Chunk c of LDS row r sits at chunk position c ^ swz(r).  A swizzle must depend on r % 32 only
-// (fragment reads take it from the lane's row within a 32-row block); for 128-byte rows, r & 7 is
-// conflict-free for the MFMA operand reads.  The fragment reads plus the copies' LDS writes come
-// close to the LDS bandwidth, so this matters.
+// Chunk c of LDS row r sits at chunk position c ^ swz(r).  A swizzle must depend on r % 16 only
+// (fragment reads take it from the lane's row within a 16-row block); for 128-byte rows, r & 7 is
+// conflict-free for the MFMA operand reads (eight lanes of a read hit eight distinct chunk
+// positions of eight rows, all 32 banks once).
 __device__ __forceinline__ int swz(int r) { return r & 7; }
+
+// Weight row (within the tile) held by LDS row rho.  Element i of a 16 x 16 MFMA accumulator of
+// lane l is output row 4 (l / 16) + i of its block; with this order, blocks 2p and 2p + 1 of a
+// wave's 128 rows give lane l the channels 32p + 8 (l / 16) + (0..7), eight consecutive ones.
+__device__ __forceinline__ int weight_row_of_lds(int rho) {
+  const int s = (rho >> 4) & 7, m = rho & 15;
+  return (rho & 128) | (32 * (s >> 1) + 8 * (m >> 2) + 4 * (s & 1) + (m & 3));
+}
 
 // s_waitcnt immediates: at most n vector-memory operations outstanding (optionally with every LDS
 // access completed), or every LDS access completed.
@@ -64,33 +76,31 @@ constexpr int vmcnt_imm(int n, bool lds_done = false) {
 }
 constexpr int kLgkmDone = 0xF | (0x3 << 14) | (0x7 << 4);
 
-// Scheduling groups for one slice of 16 MFMAs: after each of the first eight MFMAs one LDS read
-// (operands of the next slice, which do not feed these MFMAs), then up to eight copies, one per
-// MFMA.  (The compiler cannot tell that the copies and the reads touch different LDS slots, so it
-// keeps them in program order: reads first.)
-#define SCD_MFMA_THEN_READ                          \
-  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-#define SCD_MFMA_THEN_COPY                           \
-  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); \
-  __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-template <int C>
-__device__ __forceinline__ void interleave_reads_copies() {
-  static_assert(C >= 0 && C <= 8, "at most one copy per MFMA of the second half");
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ SCD_MFMA_THEN_READ
-  if constexpr (C >= 1) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 2) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 3) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 4) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 5) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 6) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 7) { SCD_MFMA_THEN_COPY }
-  if constexpr (C >= 8) { SCD_MFMA_THEN_COPY }
-  if constexpr (C < 8) __builtin_amdgcn_sched_group_barrier(0x008, 8 - C, 0);
+// Scheduling groups for one slice of 64 MFMAs, in two halves of 32 with a scheduling fence
+// between them (one solver region of all 64 MFMAs, 16 reads and 8 copies is not ordered as asked):
+// in the first half one LDS read (operands of the next slice, which do not feed these MFMAs) after
+// every second MFMA, in the second half one copy after every fourth.  (The compiler cannot tell
+// that the copies and the reads touch different LDS slots, so it keeps them in program order:
+// reads first.)
+template <int I = 0>
+__device__ __forceinline__ void interleave_reads() {
+  if constexpr (I < 16) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    interleave_reads<I + 1>();
+  }
 }
-#undef SCD_MFMA_THEN_COPY
-#undef SCD_MFMA_THEN_READ
+template <int C, int I = 0>
+__device__ __forceinline__ void interleave_copies() {
+  static_assert(C >= 0 && C <= 8, "at most one copy per four MFMAs");
+  if constexpr (I < C) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    interleave_copies<C, I + 1>();
+  } else if constexpr (C < 8) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * (8 - C), 0);
+  }
+}
 
 // The product C = A B^T of one launch (both operands row-major with the contraction contiguous,
 // 256 x 256 tiles), with the epilogue the job flags select.  Two kernels run it: the Patch KV
@@ -132,7 +142,7 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   for (int j = 0; j < kDmaIters; ++j) {
     const int slot = (kWaves * j + wave) * 64 + lane;
     const int rho = slot / kChunks, c = (slot % kChunks) ^ swz(slot / kChunks);
-    const int n = row_of_lds(rho) < N - n0 ? row_of_lds(rho) : N - n0 - 1;
+    const int n = weight_row_of_lds(rho) < N - n0 ? weight_row_of_lds(rho) : N - n0 - 1;
     const int t = t0 + rho < M ? rho : static_cast<int>(M - 1 - t0);
     woff[j] = static_cast<uint32_t>((n * K + 8 * c) * 2);
     hoff[j] = static_cast<uint32_t>((t * K + 8 * c) * 2);
@@ -150,50 +160,45 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   };
   auto copy_tile = [&](bool tokens, int kc, int slot) { copy_part(tokens, kc, slot, 0, kDmaIters); };
 
-  f32x16 acc[4][kUB];
+  f32x4 acc[kSB][kUB];
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < kSB; ++s)
 #pragma unroll
     for (int u = 0; u < kUB; ++u)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[s][u][e] = 0.f;
+      for (int e = 0; e < 4; ++e) acc[s][u][e] = 0.f;
 
-  const int lr = lane & 31, lh = lane >> 5;
-  // Fragments of k-slice ks (16 wide) of the current stage: 4 weight blocks, 4 token blocks.  Lane
-  // half h reads chunk 2 ks + h of its row; every block starts at a multiple of 32 rows, so the
-  // row's swizzle is swz(lane % 32).
+  const int lr = lane & 15, lq = lane >> 4;
+  // Fragments of k-slice ks (32 wide) of the current stage: 8 weight blocks, 8 token blocks.  Lane
+  // group q = l / 16 reads chunk 4 ks + q of its row; every block starts at a multiple of 16 rows,
+  // so the row's swizzle is swz(lane % 16).
   auto frags = [&](const uint16_t* wb, const uint16_t* hb, int ks, bf16x8* af, bf16x8* bfr) {
-    const int co = 8 * ((2 * ks + lh) ^ swz(lr));
+    const int co = 8 * ((4 * ks + lq) ^ swz(lr));
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 32 * kLDK + co);
+    for (int s = 0; s < kSB; ++s)
+      af[s] = *reinterpret_cast<const bf16x8*>(wb + s * 16 * kLDK + co);
 #pragma unroll
     for (int u = 0; u < kUB; ++u)
-      bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 32 * kLDK + co);
+      bfr[u] = *reinterpret_cast<const bf16x8*>(hb + u * 16 * kLDK + co);
   };
-  auto mma = [&](const bf16x8* af, const bf16x8* bfr) {
+  // half h of a slice's MFMAs: weight blocks 4h .. 4h + 3 against every token block
+  auto mma = [&](const bf16x8* af, const bf16x8* bfr, int h) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int s = 4 * h; s < 4 * h + 4; ++s)
 #pragma unroll
       for (int u = 0; u < kUB; ++u)
-        acc[s][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
+        acc[s][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s], bfr[u], acc[s][u], 0, 0, 0);
   };
 
-  // Copies in issue order: token tile of step 0, weight tile of step 0, token tile of step 1, ...;
-  // the i-th goes to slot i mod 5.  Step kc reads slots 2kc and 2kc + 1 (mod 5), and after its
-  // barrier issues copies 2kc + 5 and 2kc + 6 into exactly those slots.  A step index past the end
-  // re-copies the last step into a slot that is never read for data (its reads only feed the
-  // discarded look-ahead of the final step), so every step issues the same number of copies and
-  // one vmcnt threshold holds throughout.
+  // Copies in issue order: T0 W0 T1 W1 T2 W2 ... (token and weight tiles); the i-th goes to slot
+  // i mod 5.  Step kc reads slots of T(kc) and W(kc); its first slice issues token tile kc + 2 into
+  // the slot of weight tile kc - 1 (released at the previous barrier) and its second slice weight
+  // tile kc + 2 into the slot of token tile kc (released at its own barrier).  At the barrier of
+  // step kc only token tile kc + 2 may still be in flight.  A step index past the end re-copies
+  // the last step into a slot that is never read for data (its reads only feed the discarded
+  // look-ahead of the final step), so every step issues the same copies and one counter
+  // threshold holds throughout.
   auto clamp = [&](int kc) { return kc < nk ? kc : nk - 1; };
-  // Copies in issue order: T0 W0 T1 W1 T2 W2 ...; the i-th goes to slot i mod 5.  Step kc spreads
-  // the copies of token tile kc + 2 over its first three slices (into the slot of weight tile
-  // kc - 1, released at the previous barrier) and issues weight tile kc + 2 in its last slice
-  // (into the slot of token tile kc, released at its own barrier).  At the barrier of step kc
-  // only token tile kc + 2 may still be in flight.  A step index past the end re-copies the last
-  // step into a slot that is never read for data, so every step issues the same copies and one
-  // counter threshold holds throughout.
-  constexpr int kC0 = (kDmaIters + 2) / 3, kC1 = (kDmaIters + 1) / 3;
   copy_tile(kTokens, 0, 0);
   copy_tile(kWeights, 0, 1);
   copy_tile(kTokens, clamp(1), 2);
@@ -203,40 +208,33 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   lds_barrier();
   const uint16_t* wrow = smem + (wn * 128 + lr) * kLDK;
   const uint16_t* hrow = smem + (wt * kWaveTok + lr) * kLDK;
-  bf16x8 a0[4], b0[kUB], a1[4], b1[kUB];
+  bf16x8 a0[kSB], b0[kUB], a1[kSB], b1[kUB];
   int sh = 0, sw = 1, sfree = 4;  // slots of step kc's token and weight tiles; slot for T(kc+2)
   frags(wrow + sw * kSlot, hrow + sh * kSlot, 0, a0, b0);
   for (int kc = 0; kc < nk; ++kc) {
     const int next_h = sh + 2 >= kRing ? sh + 2 - kRing : sh + 2;
     const int next_w = sw + 2 >= kRing ? sw + 2 - kRing : sw + 2;
-    const uint16_t* wb = wrow + sw * kSlot;
-    const uint16_t* hb = hrow + sh * kSlot;
-    const int tk = clamp(kc + 2);
     __builtin_amdgcn_s_waitcnt(kLgkmDone);
     __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    frags(wb, hb, 1, a1, b1);
-    copy_part(kTokens, tk, sfree, 0, kC0);
-    interleave_reads_copies<kC0>();
+    mma(a0, b0, 0);
+    frags(wrow + sw * kSlot, hrow + sh * kSlot, 1, a1, b1);
+    interleave_reads();
     __builtin_amdgcn_sched_barrier(0);
-    mma(a1, b1);
-    frags(wb, hb, 2, a0, b0);
-    copy_part(kTokens, tk, sfree, kC0, kC0 + kC1);
-    interleave_reads_copies<kC1>();
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    frags(wb, hb, 3, a1, b1);
-    copy_part(kTokens, tk, sfree, kC0 + kC1, kDmaIters);
-    interleave_reads_copies<kDmaIters - kC0 - kC1>();
+    mma(a0, b0, 1);
+    copy_tile(kTokens, clamp(kc + 2), sfree);
+    interleave_copies<kDmaIters>();
     __builtin_amdgcn_sched_barrier(0);
     // Step kc + 1's tiles have landed once at most token tile kc + 2's copies are pending.
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaIters, true));
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    mma(a1, b1);
+    mma(a1, b1, 0);
     frags(wrow + next_w * kSlot, hrow + next_h * kSlot, 0, a0, b0);
+    interleave_reads();
+    __builtin_amdgcn_sched_barrier(0);
+    mma(a1, b1, 1);
     copy_tile(kWeights, clamp(kc + 2), sh);
-    interleave_reads_copies<kDmaIters>();
+    interleave_copies<kDmaIters>();
     __builtin_amdgcn_sched_barrier(0);
     sfree = sw;
     sh = next_h;
@@ -246,19 +244,18 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   wait_vmem();
   lds_barrier();
 
-  // Epilogue.  Lane l holds, for block (s, u), token t0 + wt*kWaveTok + 32u + l%32 and channels
-  // n0 + wn*128 + 32s + 16*(l/32) + r, r = 0..15.
+  // Epilogue.  Lane l holds, for blocks (2p + b, u), token t0 + wt*kWaveTok + 16u + l%16 and
+  // channels n0 + wn*128 + 32p + 8*(l/16) + 4b + i, i = 0..3.
   const bool rope = (job.flags & kRopeOut) != 0;
   const bool silu = (job.flags & kSiluOut) != 0;
   const bool add_vec = (job.flags & kVecOut) != 0 && job.vec != nullptr;
   const uint16_t* bias = static_cast<const uint16_t*>(job.vec);
   uint16_t* C = static_cast<uint16_t*>(job.c);
   const int dh = p.head_dim, half = dh >> 1;
-  // Pairs of blocks that hold (i, i + d_h/2): (0,2),(1,3) for d_h = 128; (0,1),(2,3) for 64.
+  // Block pairs p that hold (i, i + d_h/2): (0,2),(1,3) for d_h = 128; (0,1),(2,3) for 64.
   const int pstride = half >> 5;  // 2 or 1
   const int nw = n0 + wn * 128;
-  const int hl = 16 * (lane >> 5);
-
+  const int ql = 8 * lq;
   // The tile's RoPE factors and bias are staged in the (now free) LDS first, so the epilogue's
   // stores never wait behind global loads.  Factors: 16-byte chunk c (pairs 2c, 2c + 1) of token
   // r's table row at byte (c * 256 + r) * 16, so the lanes of a read (consecutive tokens) hit
@@ -286,59 +283,55 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
   wait_vmem();
   lds_barrier();
 
-  auto load16 = [&](int nb, float* v) {
+  auto load8 = [&](int nb, float* v) {
     if (add_vec) {
-      const uint4* src = reinterpret_cast<const uint4*>(sbias + (nb - n0));
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint4 x = src[h];
-        v[8 * h + 0] = bf16_lo(x.x); v[8 * h + 1] = bf16_hi(x.x);
-        v[8 * h + 2] = bf16_lo(x.y); v[8 * h + 3] = bf16_hi(x.y);
-        v[8 * h + 4] = bf16_lo(x.z); v[8 * h + 5] = bf16_hi(x.z);
-        v[8 * h + 6] = bf16_lo(x.w); v[8 * h + 7] = bf16_hi(x.w);
-      }
+      const uint4 x = *reinterpret_cast<const uint4*>(sbias + (nb - n0));
+      v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x);
+      v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
+      v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z);
+      v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
     } else {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) v[e] = 0.f;
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
     }
   };
-  auto store16 = [&](int64_t t, int nb, const float* y) {
+  auto store8 = [&](int64_t t, int nb, const float* y) {
     if (nb >= N) return;
-    uint4 o0, o1;
-    o0.x = pack_bf16x2(y[0], y[1]);   o0.y = pack_bf16x2(y[2], y[3]);
-    o0.z = pack_bf16x2(y[4], y[5]);   o0.w = pack_bf16x2(y[6], y[7]);
-    o1.x = pack_bf16x2(y[8], y[9]);   o1.y = pack_bf16x2(y[10], y[11]);
-    o1.z = pack_bf16x2(y[12], y[13]); o1.w = pack_bf16x2(y[14], y[15]);
-    uint4* dst = reinterpret_cast<uint4*>(C + t * N + nb);
-    dst[0] = o0;
-    dst[1] = o1;
+    uint4 o;
+    o.x = pack_bf16x2(y[0], y[1]);
+    o.y = pack_bf16x2(y[2], y[3]);
+    o.z = pack_bf16x2(y[4], y[5]);
+    o.w = pack_bf16x2(y[6], y[7]);
+    *reinterpret_cast<uint4*>(C + t * N + nb) = o;
   };
 
-  // One pair of blocks (S, S + PS) holds channels (i, i + d_h/2); S and PS are compile-time so the
-  // accumulators stay in registers.  rl is the token's row within the tile.
-  auto finish_pair = [&](auto s_c, auto ps_c, int u, int64_t t, int rl) {
-    constexpr int S = decltype(s_c)::value;
-    constexpr int SP = S + decltype(ps_c)::value;
-    const int nb = nw + 32 * S + hl, nbp = nw + 32 * SP + hl;
-    float a[16], b[16];
-    load16(nb, a);
-    load16(nbp, b);
+  // One pair of block pairs (P, P + PS) holds channels (i, i + d_h/2); P and PS are compile-time so
+  // the accumulators stay in registers.  rl is the token's row within the tile.
+  auto finish_pair = [&](auto p_c, auto ps_c, int u, int64_t t, int rl) {
+    constexpr int P = decltype(p_c)::value;
+    constexpr int PP = P + decltype(ps_c)::value;
+    const int nb = nw + 32 * P + ql, nbp = nw + 32 * PP + ql;
+    float a[8], b[8];
+    load8(nb, a);
+    load8(nbp, b);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      a[r] += acc[S][u][r];
-      b[r] += acc[SP][u][r];
+    for (int i = 0; i < 4; ++i) {
+      a[i] += acc[2 * P][u][i];
+      a[4 + i] += acc[2 * P + 1][u][i];
+      b[i] += acc[2 * PP][u][i];
+      b[4 + i] += acc[2 * PP + 1][u][i];
     }
     if (silu) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
+      for (int r = 0; r < 8; ++r) {
         a[r] = silu_bf16(a[r]);
         b[r] = silu_bf16(b[r]);
       }
     }
     if (rope) {
-      const int c0 = ((32 * S + hl) & (half - 1)) >> 1;  // chunk of the pair of channel r = 0
+      const int c0 = ((32 * P + ql) & (half - 1)) >> 1;  // chunk of the pair of channel r = 0
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+      for (int q = 0; q < 4; ++q) {
         const float4 cs = *reinterpret_cast<const float4*>(stage + ((c0 + q) * kBM + rl) * 16);
         const float x0 = a[2 * q], y0 = b[2 * q], x1 = a[2 * q + 1], y1 = b[2 * q + 1];
         a[2 * q] = x0 * cs.x - y0 * cs.y;
@@ -347,13 +340,13 @@ __device__ __forceinline__ void patch_gemm_bf16(const GemmParams& p, uint16_t* s
         b[2 * q + 1] = y1 * cs.z + x1 * cs.w;
       }
     }
-    store16(t, nb, a);
-    store16(t, nbp, b);
+    store8(t, nb, a);
+    store8(t, nbp, b);
   };
 
 #pragma unroll
   for (int u = 0; u < kUB; ++u) {
-    const int rl = wt * kWaveTok + 32 * u + (lane & 31);
+    const int rl = wt * kWaveTok + 16 * u + lr;
     const int64_t t = t0 + rl;
     if (t >= M) continue;
     if (pstride == 2) {
