@@ -118,46 +118,67 @@ __device__ __forceinline__ void decode_tile(const GemmParams& p, const LdsBatch&
           acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bz, acc[s], 0, 0, 0);
         }
       }
-      if (FULL || row < c.M) {
+      // No row guard before the stores: the lane exchange below needs every lane.
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int S = PS == 2 ? q : 2 * q;  // first-half block; its partner is S + PS
-          const int cl = g * 128 + 32 * S + hl, clp = cl + 32 * PS;  // local channels
-          float a[16], b[16];
+      for (int q = 0; q < 2; ++q) {
+        const int S = PS == 2 ? q : 2 * q;  // first-half block; its partner is S + PS
+        const int cl = g * 128 + 32 * S + hl, clp = cl + 32 * PS;  // local channels
+        float a[16], b[16];
 #pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            unpack8(*reinterpret_cast<const uint4*>(mus + cl + 8 * k), a + 8 * k);
-            unpack8(*reinterpret_cast<const uint4*>(mus + clp + 8 * k), b + 8 * k);
-          }
+        for (int k = 0; k < 2; ++k) {
+          unpack8(*reinterpret_cast<const uint4*>(mus + cl + 8 * k), a + 8 * k);
+          unpack8(*reinterpret_cast<const uint4*>(mus + clp + 8 * k), b + 8 * k);
+        }
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            a[r] += acc[S][r];
-            b[r] += acc[S + PS][r];
-          }
-          if constexpr (!ROPE) {
-            if (c.silu) {
-#pragma unroll
-              for (int r = 0; r < 16; ++r) {
-                a[r] = silu_bf16(a[r]);
-                b[r] = silu_bf16(b[r]);
-              }
-            }
-          }
-          if constexpr (ROPE) {
+        for (int r = 0; r < 16; ++r) {
+          a[r] += acc[S][r];
+          b[r] += acc[S + PS][r];
+        }
+        if constexpr (!ROPE) {
+          if (c.silu) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-              const float2 f = cs[q][r];
-              const float x = a[r], y = b[r];
-              a[r] = x * f.x - y * f.y;
-              b[r] = y * f.x + x * f.y;
+              a[r] = silu_bf16(a[r]);
+              b[r] = silu_bf16(b[r]);
             }
           }
-          u32x4* da = reinterpret_cast<u32x4*>(c.C + row * c.N + c.n0 + cl);
-          u32x4* db = reinterpret_cast<u32x4*>(c.C + row * c.N + c.n0 + clp);
-          da[0] = as_u32x4(pack8(a));
-          da[1] = as_u32x4(pack8(a + 8));
-          db[0] = as_u32x4(pack8(b));
-          db[1] = as_u32x4(pack8(b + 8));
+        }
+        if constexpr (ROPE) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float2 f = cs[q][r];
+            const float x = a[r], y = b[r];
+            a[r] = x * f.x - y * f.y;
+            b[r] = y * f.x + x * f.y;
+          }
+        }
+        // Lane t and lane t + 16 (t % 32 < 16) swap halves (v_permlane16_swap): lane t keeps its
+        // row's channels 0..7 of the 16 and takes row t + 16's, lane t + 16 takes row t's channels
+        // 8..15 and keeps its own.  One store instruction then writes 16 rows x 64 contiguous bytes
+        // (four lanes per row) instead of 32 rows x two separate 16-byte pieces, which halves the
+        // write requests to L2 (32 -> 64 bytes each); the per-CU cache's queue of pending requests
+        // was what held the stores back.
+        const u32x4 ax = as_u32x4(pack8(a)), ay = as_u32x4(pack8(a + 8));
+        const u32x4 bx = as_u32x4(pack8(b)), by = as_u32x4(pack8(b + 8));
+        u32x4 alo, ahi, blo, bhi;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const auto sa = __builtin_amdgcn_permlane16_swap(ax[i], ay[i], false, false);
+          const auto sb = __builtin_amdgcn_permlane16_swap(bx[i], by[i], false, false);
+          alo[i] = sa[0];
+          ahi[i] = sa[1];
+          blo[i] = sb[0];
+          bhi[i] = sb[1];
+        }
+        const int sub = 8 * ((lane >> 4) & 1);
+        const int64_t r0 = t0 + wave * 32 + (lane & 15), r1 = r0 + 16;
+        if (FULL || r0 < c.M) {
+          *reinterpret_cast<u32x4*>(c.C + r0 * c.N + c.n0 + cl + sub) = alo;
+          *reinterpret_cast<u32x4*>(c.C + r0 * c.N + c.n0 + clp + sub) = blo;
+        }
+        if (FULL || r1 < c.M) {
+          *reinterpret_cast<u32x4*>(c.C + r1 * c.N + c.n0 + cl + sub) = ahi;
+          *reinterpret_cast<u32x4*>(c.C + r1 * c.N + c.n0 + clp + sub) = bhi;
         }
       }
     }
