@@ -84,11 +84,8 @@ __device__ inline int row_position_lds(const GemmParams& p, const LdsBatch& lb, 
 
 // MFMA 32x32 output rows are (8a + 4h + b) for accumulator element r = 4a + b of lane half h.
 // Storing operand row 16h + 4a + b at LDS row 8a + 4h + b of each 32-row block makes element r of
-// lane half h hold operand row 16h + r: 16 consecutive rows (output channels) per lane.
-__device__ inline int lds_row_of(int n) {
-  const int o = n & 31;
-  return (n & ~31) | (8 * ((o >> 2) & 3) + 4 * (o >> 4) + (o & 3));
-}
+// lane half h hold operand row 16h + r: 16 consecutive rows (output channels) per lane.  This is
+// the operand row held by LDS row rho.
 __device__ inline int row_of_lds(int rho) {
   const int o = rho & 31;
   return (rho & ~31) | (16 * ((o >> 2) & 1) + 4 * (o >> 3) + (o & 3));
