@@ -485,6 +485,23 @@ class Codec:
             ev[3].record(stream)
 
 
+def reduce_events(events, split):
+    """Per-phase times and consumer spans (ms) from each step's four events: encode from every
+    step, the decode/Patch split from the steps with an event between them (split), the consumer
+    span (decode start to Patch end) from the others, or from every step if all are split."""
+    phase = {k: [] for k in PHASES}
+    consumer = []
+    every = all(split)
+    for ev, sp in zip(events, split):
+        phase["encode"].append(ev[0].elapsed_time(ev[1]))
+        if sp:
+            phase["reuse_decode"].append(ev[1].elapsed_time(ev[2]))
+            phase["patch"].append(ev[2].elapsed_time(ev[3]))
+        if not sp or every:
+            consumer.append(ev[1].elapsed_time(ev[3]))
+    return phase, consumer
+
+
 def measure(wl, dev, steps, warmup, stream, codec=None):
     """W warm-up steps, then K timed steps bracketed by synchronisations (wall clock), with HIP
     events on the stream between the entry points.  Returns the workload's block."""
@@ -510,15 +527,7 @@ def measure(wl, dev, steps, warmup, stream, codec=None):
         codec.step(stream, events[i], split[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    phase = {k: [] for k in PHASES}
-    consumer = []
-    for ev, sp in zip(events, split):
-        phase["encode"].append(ev[0].elapsed_time(ev[1]))
-        if sp:
-            phase["reuse_decode"].append(ev[1].elapsed_time(ev[2]))
-            phase["patch"].append(ev[2].elapsed_time(ev[3]))
-        if not sp or steps == 1:
-            consumer.append(ev[1].elapsed_time(ev[3]))
+    phase, consumer = reduce_events(events, split)
     mean = {k: sum(v) / len(v) for k, v in phase.items()}
     cons_ms = sum(consumer) / len(consumer)
     alg = algorithmic(wl)

@@ -37,3 +37,40 @@ def test_algorithmic_figures_at_the_llama3_8b_shape():
     gemm_b = n_patch * (T * h + 2 * D * h + 2 * D + 2 * T * D) * eb
     assert alg["patch"] == (act_b + gemm_b, n_patch * (2 * T * r * h + 2 * T * h * 2 * D))
     assert alg["patch"][1] == 584_115_552_256
+
+
+class _Ev:
+    """A stand-in for a timing event: a timestamp in ms."""
+
+    def __init__(self, t):
+        self.t = t
+
+    def elapsed_time(self, other):
+        return other.t - self.t
+
+
+def test_consumer_span_and_phase_split_come_from_alternate_steps():
+    # Even steps carry an event between the decode and Patch calls; the GPU idles 0.005 ms at it.
+    # Encode 0.4, decode 0.3, Patch 0.5 ms every step.
+    events, split = [], []
+    t = 0.0
+    for i in range(6):
+        sp = i % 2 == 0
+        gap = 0.005 if sp else 0.0
+        e0 = _Ev(t)
+        e1 = _Ev(t + 0.4)
+        e2 = _Ev(t + 0.4 + 0.3)
+        e3 = _Ev(t + 0.4 + 0.3 + gap + 0.5)
+        events.append([e0, e1, e2, e3])
+        split.append(sp)
+        t += 2.0
+    phase, consumer = bench.reduce_events(events, split)
+    assert len(phase["encode"]) == 6
+    assert len(phase["reuse_decode"]) == len(phase["patch"]) == len(consumer) == 3
+    # the consumer span has no event gap in it; the phase split comes from the split steps only
+    assert all(abs(c - 0.8) < 1e-12 for c in consumer)
+    assert all(abs(x - 0.3) < 1e-12 for x in phase["reuse_decode"])
+    assert all(abs(x - 0.505) < 1e-12 for x in phase["patch"])
+    # one step (every step split): the consumer span comes from it
+    phase1, consumer1 = bench.reduce_events(events[:1], [True])
+    assert len(consumer1) == 1 and abs(consumer1[0] - 0.805) < 1e-12
