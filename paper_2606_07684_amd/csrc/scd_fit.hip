@@ -627,7 +627,11 @@ __global__ __launch_bounds__(256) void fit_gram_reduce_kernel(const FitGramParam
 //   out       the triangular solves for E and F and the outputs, rounded once.
 // ---------------------------------------------------------------------------------------------
 constexpr int kSolveThreads = 256;
-constexpr int kSolveRows = 16;  // rows per workgroup of a tridiagonal or a Cholesky step
+constexpr int kSolveRows = 16;  // rows per workgroup of the prep and of a tridiagonal step, n <= 512
+// Rows per workgroup of a tridiagonal step for n > 512 and of a per-column Cholesky step: the
+// trailing block is then large and one layer's 16-row workgroups would leave most CUs idle, each
+// workgroup bound by its CU's share of the memory bandwidth.
+constexpr int kSolveRowsWide = 4;
 constexpr int kBackCols = 8;    // columns of Y per workgroup of the back-transformation
 constexpr int kMaxN = 2 * kFitMaxSolveWidth;
 constexpr int kInverseSolves = 3;
@@ -744,18 +748,19 @@ __global__ __launch_bounds__(kSolveThreads) void fit_prep_kernel(const FitSolveP
 // Every global load of a launch is issued at its start (the reflector and p of the previous launch,
 // row k+1 and, for n <= 64 PRE, this workgroup's rows of the source), so the launch waits on one
 // round of loads rather than three.
-template <int PRE>
+template <int PRE, int ROWS>
 __device__ __forceinline__ void tridiag_step(const SolveArgs& a) {
   __shared__ double vk[kMaxN], wk[kMaxN], vn[kMaxN];
   __shared__ double red[2][kSolveThreads / 64];
   const int layer = blockIdx.y, n = 2 * a.w, k = a.step, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  constexpr int kWaves = kSolveThreads / 64, kRowsPerWave = kSolveRows / kWaves;
+  constexpr int kWaves = kSolveThreads / 64, kRowsPerWave = ROWS / kWaves;
+  static_assert(ROWS % kWaves == 0, "whole rows per wave");
   const Slots s = slots(a.work, a.w, layer);
   const double* src = k <= 0 ? s.z : ((k - 1) & 1 ? s.y : s.x);
   double* dst = (k & 1) ? s.y : s.x;  // k = -1 is odd: Y (only its reflector row is written)
   double* p_next = ((k + 1) & 1) ? s.p1 : s.p0;
-  const int r0 = k + 2 + blockIdx.x * kSolveRows;
+  const int r0 = k + 2 + blockIdx.x * ROWS;
   // loads: reflector k and p_k into vk / wk, row k+1 of the source into vn, own rows to registers
   if (k >= 0) {
     const double* vrow = reflector_rows(s, k) + static_cast<int64_t>(k) * n;
@@ -822,7 +827,7 @@ __device__ __forceinline__ void tridiag_step(const SolveArgs& a) {
   // this workgroup's rows of A^(k+1) and of p_{k+1}
   for (int q = 0; q < kRowsPerWave; ++q) {
     const int i = r0 + wave + kWaves * q;
-    if (i >= n || i >= r0 + kSolveRows) break;
+    if (i >= n || i >= r0 + ROWS) break;
     const double* arow = src + static_cast<int64_t>(i) * n;
     double* orow = dst + static_cast<int64_t>(i) * n;
     const double vi = vk[i], wi = wk[i];
@@ -858,10 +863,10 @@ __device__ __forceinline__ void tridiag_step(const SolveArgs& a) {
 
 constexpr int kTridiagPre = 8;  // row entries per lane held in registers: n <= 512
 __global__ __launch_bounds__(kSolveThreads) void fit_tridiag_pre_kernel(const SolveArgs a) {
-  tridiag_step<kTridiagPre>(a);
+  tridiag_step<kTridiagPre, kSolveRows>(a);
 }
 __global__ __launch_bounds__(kSolveThreads) void fit_tridiag_kernel(const SolveArgs a) {
-  tridiag_step<0>(a);
+  tridiag_step<0, kSolveRowsWide>(a);
 }
 
 // The last steps, from step k0 on (trailing block of at most kTailN rows), in one launch: one
@@ -1378,10 +1383,10 @@ __global__ __launch_bounds__(kSolveThreads) void fit_normal_kernel(const SolveAr
 
 // ---- Cholesky, one column per launch --------------------------------------------------------------
 // grid.y = 0: A^T A + lam I (X, size w), 1: Z^T Z + lam I (Y, size r).  Step k reads column k on and
-// below the diagonal, updates rows (k, s) of the lower triangle (a workgroup's kSolveRows rows), and
-// stores L[i][k] twice, in places nothing reads before the solves: at [k][i] in the upper triangle
-// (column k of L as a row) and at [i][k] of a row-major copy of L just past the matrix.  L[k][k]
-// goes to ldiag.  A non-positive pivot leaves NaN, which reaches every output of the layer.
+// below the diagonal, updates rows (k, s) of the lower triangle (a workgroup's kSolveRowsWide rows),
+// and stores L[i][k] twice, in places nothing reads before the solves: at [k][i] in the upper
+// triangle (column k of L as a row) and at [i][k] of a row-major copy of L just past the matrix.
+// L[k][k] goes to ldiag.  A non-positive pivot leaves NaN, which reaches every output of the layer.
 __global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs a) {
   __shared__ double lc[kFitMaxSolveWidth];
   const int layer = blockIdx.z, w = a.w, k = a.step, tid = threadIdx.x;
@@ -1397,8 +1402,8 @@ __global__ __launch_bounds__(kSolveThreads) void fit_chol_kernel(const SolveArgs
   for (int i = k + 1 + tid; i < sz; i += kSolveThreads) lc[i] = mat[static_cast<int64_t>(i) * sz + k] / lkk;
   __syncthreads();
   const int lane = tid & 63, wave = tid >> 6;
-  const int r0 = k + 1 + blockIdx.x * kSolveRows;
-  for (int i = r0 + wave; i < r0 + kSolveRows && i < sz; i += kSolveThreads / 64) {
+  const int r0 = k + 1 + blockIdx.x * kSolveRowsWide;
+  for (int i = r0 + wave; i < r0 + kSolveRowsWide && i < sz; i += kSolveThreads / 64) {
     const double li = lc[i];
     double* row = mat + static_cast<int64_t>(i) * sz;
     for (int j = k + 1 + lane; j <= i; j += 64) row[j] -= li * lc[j];
@@ -1596,7 +1601,8 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   for (int k = -1; k < k0; ++k) {
     a.step = k;
     const int rows = n - k - 2;
-    const dim3 grid((rows + kSolveRows - 1) / kSolveRows, layers);
+    const int rpw = n <= 64 * kTridiagPre ? kSolveRows : kSolveRowsWide;
+    const dim3 grid((rows + rpw - 1) / rpw, layers);
     if (n <= 64 * kTridiagPre) hipLaunchKernelGGL(fit_tridiag_pre_kernel, grid, block, 0, stream, a);
     else hipLaunchKernelGGL(fit_tridiag_kernel, grid, block, 0, stream, a);
   }
@@ -1625,7 +1631,7 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
     for (int k = 0; k < sz; ++k) {
       a.step = k;
       const int rows = sz - k - 1;
-      const int gx = rows > 0 ? (rows + kSolveRows - 1) / kSolveRows : 1;
+      const int gx = rows > 0 ? (rows + kSolveRowsWide - 1) / kSolveRowsWide : 1;
       hipLaunchKernelGGL(fit_chol_kernel, dim3(gx, 2, layers), block, 0, stream, a);
     }
   }
