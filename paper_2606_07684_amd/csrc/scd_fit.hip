@@ -632,7 +632,9 @@ constexpr int kSolveRows = 16;  // rows per workgroup of the prep and of a tridi
 // trailing block is then large and one layer's 16-row workgroups would leave most CUs idle, each
 // workgroup bound by its CU's share of the memory bandwidth.
 constexpr int kSolveRowsWide = 4;
-constexpr int kBackCols = 8;    // columns of Y per workgroup of the back-transformation
+// columns of Y per workgroup of the back-transformation: 8 for n <= 512 (many layers, short
+// chains), 2 above (one layer's few workgroups carry long chains)
+constexpr int kBackColsNarrow = 8, kBackColsWide = 2;
 constexpr int kMaxN = 2 * kFitMaxSolveWidth;
 constexpr int kInverseSolves = 3;
 constexpr double kEps = 2.220446049250313e-16;  // 2^-52
@@ -1223,8 +1225,11 @@ __global__ __launch_bounds__(64) void fit_inverse_lds_kernel(const SolveArgs a) 
 
 // ---- back-transformation and sign ---------------------------------------------------------------
 // kBackCols columns of Y per workgroup, held in LDS while the reflectors n-3 .. 0 are applied in
-// turn (Y <- (I - tau_j v_j v_j^T) Y); thread t keeps rows i = t / kBackCols (mod 32) of column
-// t % kBackCols.  Then each column's first entry of largest magnitude is made positive.
+// turn (Y <- (I - tau_j v_j v_j^T) Y); thread t keeps rows i = t / kBackCols (mod kSolveThreads /
+// kBackCols) of column t % kBackCols.  Then each column's first entry of largest magnitude is made
+// positive.  Each reflector costs every column about 3n LDS accesses, so few columns per
+// workgroup (and more workgroups) shorten the chain.
+template <int kBackCols>
 __global__ __launch_bounds__(kSolveThreads) void fit_back_kernel(const SolveArgs a) {
   __shared__ double yc[kMaxN * kBackCols];
   __shared__ double vb[kMaxN];
@@ -1235,26 +1240,52 @@ __global__ __launch_bounds__(kSolveThreads) void fit_back_kernel(const SolveArgs
   const int r = static_cast<int>(s.job->rank);
   const int c0 = blockIdx.x * kBackCols;
   if (c0 >= r) return;
-  constexpr int kGroups = kSolveThreads / kBackCols;  // 32 row groups
+  constexpr int kGroups = kSolveThreads / kBackCols;  // row groups
   const int c = tid % kBackCols, g = tid / kBackCols, lane = tid & 63, wave = tid >> 6;
   const bool live = c0 + c < r;
   for (int e = tid; e < n * kBackCols; e += kSolveThreads) {
     const int i = e / kBackCols, cc = e % kBackCols;
     yc[e] = c0 + cc < r ? s.z[static_cast<int64_t>(i) * r + c0 + cc] : 0.0;
   }
-  for (int jr = n - 3; jr >= 0; --jr) {
-    const double t = s.tau[jr];
-    if (t == 0.0) continue;
+  // Reflector jr - 1 (its tau and this thread's entries of its row) is loaded into registers while
+  // reflector jr is applied, so the chain of n - 2 reflectors does not wait on a global load at
+  // each link; the barriers inside the chain only order LDS accesses (lds_barrier), so the loads
+  // stay in flight across them.
+  constexpr int kPer = kMaxN / kSolveThreads;
+  double nxt[kPer];
+  double tnext = 0.0;
+  auto fetch = [&](int jr) {
+    if (jr < 0) return;
+    tnext = s.tau[jr];
     const double* vrow = reflector_rows(s, jr) + static_cast<int64_t>(jr) * n;
-    __syncthreads();  // the previous reflector's vb and red reads are done
-    for (int i = jr + 1 + tid; i < n; i += kSolveThreads) vb[i] = vrow[i];
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int i = jr + 1 + tid + q * kSolveThreads;
+      nxt[q] = i < n ? vrow[i] : 0.0;
+    }
+  };
+  __syncthreads();  // Y is in LDS
+  fetch(n - 3);
+  for (int jr = n - 3; jr >= 0; --jr) {
+    const double t = tnext;
+    double cur[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) cur[q] = nxt[q];
+    fetch(jr - 1);
+    if (t == 0.0) continue;
+    lds_barrier();  // the previous reflector's vb and red reads are done
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int i = jr + 1 + tid + q * kSolveThreads;
+      if (i < n) vb[i] = cur[q];
+    }
+    lds_barrier();
     double part = 0.0;
     for (int i = jr + 1 + g; i < n; i += kGroups) part += vb[i] * yc[i * kBackCols + c];
-    // the 8 row groups of a wave that share column c sit kBackCols lanes apart
+    // the row groups of a wave that share column c sit kBackCols lanes apart
     for (int o = kBackCols; o < 64; o <<= 1) part += __shfl_xor(part, o, 64);
     if (lane < kBackCols) red[wave][lane] = part;
-    __syncthreads();
+    lds_barrier();
     double dot = 0.0;
     for (int q = 0; q < kSolveThreads / 64; ++q) dot += red[q][c];
     const double f = t * dot;
@@ -1618,8 +1649,14 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
                        stream, a);
   else
     hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
-  hipLaunchKernelGGL(fit_back_kernel, dim3((rmax + kBackCols - 1) / kBackCols, layers), block, 0,
-                     stream, a);
+  if (n <= 512)
+    hipLaunchKernelGGL(fit_back_kernel<kBackColsNarrow>,
+                       dim3((rmax + kBackColsNarrow - 1) / kBackColsNarrow, layers), block, 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL(fit_back_kernel<kBackColsWide>,
+                       dim3((rmax + kBackColsWide - 1) / kBackColsWide, layers), block, 0, stream,
+                       a);
   hipLaunchKernelGGL(fit_project_kernel, dim3(n / 64, rt, layers), block, 0, stream, a);
   const unsigned tw = static_cast<unsigned>(p.w / 64);
   hipLaunchKernelGGL(fit_normal_kernel, dim3(rt * rt > tw * tw ? rt * rt : tw * tw, 2, layers),
