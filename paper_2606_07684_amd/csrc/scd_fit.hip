@@ -1169,38 +1169,16 @@ __device__ inline bool cluster_of(const double* lam, int r, int j, double ctol, 
   return true;
 }
 
-// Vectors in the workspace: Y[i][m] (Z[0, n r)), the LU factors of T - sigma I in U0 (Z[n r,
-// 2 n r)), U1 and U2 (M[0, n r) and M[n r, 2 n r)), all indexed [i][m].
-__global__ __launch_bounds__(64) void fit_inverse_kernel(const SolveArgs a) {
-  __shared__ double d[kMaxN], e[kMaxN];
-  const int layer = blockIdx.y, n = 2 * a.w;
-  const Slots s = slots(a.work, a.w, layer);
-  const int r = static_cast<int>(s.job->rank);
-  for (int i = threadIdx.x; i < n; i += 64) {
-    d[i] = s.d[i];
-    e[i] = i < n - 1 ? s.e[i] : 0.0;
-  }
-  __syncthreads();
-  const int j = blockIdx.x * 64 + threadIdx.x;
-  const double tnorm = s.job->tnorm;
-  int last;
-  if (!cluster_of(s.lam, r, j, kClusterTol * tnorm, &last)) return;
-  const int64_t nr = static_cast<int64_t>(n) * r;
-  // vector m works in place at its own column of Y, its factors in their columns of U0..U2
-  auto col = [&](double* base, int m) { return Strided{base + m, r}; };
-  inverse_cluster(
-      d, e, n, s.lam, j, last, tnorm,
-      [&](int m) { return InverseWork{col(s.z, m), col(s.z + nr, m), col(s.m, m), col(s.m + nr, m)}; },
-      [&](int m) { return col(s.z, m); });
-}
-
-// The same for n <= kInverseLdsN: each working thread keeps its vector and LU factors in LDS
-// ([i][thread], kInverseLdsThreads interleaved, so the threads' accesses fall in distinct banks)
-// and copies each finished vector to Y.
+// Inverse iteration, one eigenvector per working thread: the thread keeps its vector and the LU
+// factors of T - sigma I in LDS ([i][thread], THREADS interleaved, so the threads' accesses fall in
+// distinct banks) and copies each finished vector to Y[i][m].  Two instances: 16 threads per
+// workgroup for n <= 256, and one thread per workgroup (96 KiB of LDS) for larger n; the chain of
+// dependent accesses would otherwise wait on global memory at each link.
 constexpr int kInverseLdsN = 256, kInverseLdsThreads = 16;
+template <int N, int THREADS>
 __global__ __launch_bounds__(64) void fit_inverse_lds_kernel(const SolveArgs a) {
-  __shared__ double d[kInverseLdsN], e[kInverseLdsN];
-  __shared__ double vec[4 * kInverseLdsN * kInverseLdsThreads];
+  __shared__ double d[N], e[N];
+  __shared__ double vec[4 * N * THREADS];
   const int layer = blockIdx.y, n = 2 * a.w;
   const Slots s = slots(a.work, a.w, layer);
   const int r = static_cast<int>(s.job->rank);
@@ -1210,13 +1188,13 @@ __global__ __launch_bounds__(64) void fit_inverse_lds_kernel(const SolveArgs a) 
   }
   __syncthreads();
   const int t = threadIdx.x;
-  const int j = blockIdx.x * kInverseLdsThreads + t;
-  if (t >= kInverseLdsThreads) return;
+  const int j = blockIdx.x * THREADS + t;
+  if (t >= THREADS) return;
   const double tnorm = s.job->tnorm;
   int last;
   if (!cluster_of(s.lam, r, j, kClusterTol * tnorm, &last)) return;
-  constexpr int64_t kPlane = static_cast<int64_t>(kInverseLdsN) * kInverseLdsThreads;
-  auto lds = [&](int q) { return Strided{vec + q * kPlane + t, kInverseLdsThreads}; };
+  constexpr int64_t kPlane = static_cast<int64_t>(N) * THREADS;
+  auto lds = [&](int q) { return Strided{vec + q * kPlane + t, THREADS}; };
   inverse_cluster(
       d, e, n, s.lam, j, last, tnorm,
       [&](int) { return InverseWork{lds(0), lds(1), lds(2), lds(3)}; },
@@ -1644,11 +1622,11 @@ hipError_t launch_fit_solve(const FitSolveParams& p, hipStream_t stream) {
   const unsigned rt = static_cast<unsigned>((rmax + 63) / 64);
   hipLaunchKernelGGL(fit_bisect_kernel, dim3((rmax + 3) / 4, layers), wave, 0, stream, a);
   if (n <= kInverseLdsN)
-    hipLaunchKernelGGL(fit_inverse_lds_kernel,
+    hipLaunchKernelGGL((fit_inverse_lds_kernel<kInverseLdsN, kInverseLdsThreads>),
                        dim3((rmax + kInverseLdsThreads - 1) / kInverseLdsThreads, layers), wave, 0,
                        stream, a);
   else
-    hipLaunchKernelGGL(fit_inverse_kernel, dim3(rt, layers), wave, 0, stream, a);
+    hipLaunchKernelGGL((fit_inverse_lds_kernel<kMaxN, 1>), dim3(rmax, layers), wave, 0, stream, a);
   if (n <= 512)
     hipLaunchKernelGGL(fit_back_kernel<kBackColsNarrow>,
                        dim3((rmax + kBackColsNarrow - 1) / kBackColsNarrow, layers), block, 0,
