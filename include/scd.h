@@ -285,8 +285,9 @@ scd_status_t scd_reuse_decode_streamed(const scd_model_t* model, const scd_batch
  *    one token.
  *  - scd_fit_solve takes those sums for N = n_rows rows (n_tokens * g) and solves the fit in fp64
  *    (Householder tridiagonalisation of the centred Gram, bisection and inverse iteration for its
- *    top r eigenpairs, Cholesky ridge solves; each stage one launch over all layers, the
- *    tridiagonalisation and the Cholesky one launch per column), writing w_enc, w_dec and, when
+ *    top r eigenpairs, Cholesky ridge solves; each stage one launch over all layers, except the
+ *    tridiagonalisation, one launch per column until at most 128 rows remain, and the Cholesky of
+ *    sizes above 128, one launch per column), writing w_enc, w_dec and, when
  *    center = 1, mu_enc and mu_dec in the model's dtype (rounded once).  Needs basis_width <= 1024
  *    and 16 <= rank <= basis_width, rank % 16 == 0, lambda >= 0.  lambda = 0 with a singular
  *    A^T A (fewer independent rows than w) leaves NaN in the layer's outputs.  Eigenvalues within
@@ -317,8 +318,9 @@ scd_status_t scd_fit_solve(const scd_model_t* model, int32_t branch, int64_t n_r
  * scd_fit_solve_noalloc_max_bytes() bytes (64 MiB) that the library holds on each GPU it runs on
  * until the process ends; layers are solved in as many stream-ordered rounds of launches as that
  * array needs (4 (2w)^2 + 8 (2w) fp64 values per layer).  A basis width whose per-layer matrices
- * exceed the array (w > 512) returns SCD_ERR_WORKSPACE.  The call uses the calling thread's current device, which must own the
- * stream and the buffers; its first call on a device looks the array's address up.  It allocates
+ * exceed the array (w > 512) returns SCD_ERR_WORKSPACE.  The call uses the calling thread's
+ * current device, which must own the stream and the buffers; its first call on a device looks the
+ * array's address up.  It allocates
  * nothing and never synchronises.  Every call on one GPU shares that GPU's array: calls that may
  * run at the same time on one GPU (different streams, or other threads) race on it and must be
  * serialised by the caller. */
